@@ -1,0 +1,195 @@
+"""Seeded synthetic inputs for response-replay attention.
+
+This module only draws random numbers and lays them out; it computes nothing
+of the attention method.  Both the HIP path and the CPU oracle read the bytes
+it produces, so the two always see identical inputs.
+
+Recipe (all draws fp32 from numpy's PCG64, bf16 configs rounded to nearest-even):
+
+* streams: 0 page table, 1 K pool, 2 V pool, 3 Q, 4 dO, 5 planted keys, 6 sparse indices;
+* every physical KV page ``p`` is drawn from ``SeedSequence([seed, stream, p])`` so
+  pages can be generated in parallel and independently of the pool size;
+* Q and dO are drawn in chunks of 2**20 values from ``SeedSequence([seed, stream, chunk])``;
+* page table: identity, a seeded permutation of all logical pages, or (``sample``) a
+  seeded sample without replacement from a pool with free pages;
+* planted keys: a fraction of prefix positions ``j`` each picks a target query row ``t`` and
+  head ``h`` and gets ``k[j, h // G] += gain * q[t, h]`` before rounding, which raises that
+  one score by about ``gain * sqrt(D)`` and makes the per-shard log-normalizers differ by
+  tens of nats;
+* sparse replay: each query row draws ``topk`` distinct prefix positions, sorted ascending.
+"""
+from __future__ import annotations
+
+import os
+from concurrent.futures import ThreadPoolExecutor
+
+import numpy as np
+
+STREAM_TABLE, STREAM_K, STREAM_V, STREAM_Q, STREAM_DO, STREAM_PLANT, STREAM_IDX = range(7)
+_CHUNK = 1 << 20
+
+
+def _threads() -> int:
+    try:
+        n = len(os.sched_getaffinity(0))
+    except AttributeError:  # pragma: no cover
+        n = os.cpu_count() or 1
+    return max(1, min(16, n))
+
+
+def _rng(*key: int) -> np.random.Generator:
+    return np.random.Generator(np.random.PCG64(np.random.SeedSequence(list(key))))
+
+
+def to_bf16_bits(x: np.ndarray) -> np.ndarray:
+    """Round fp32 to bf16 (nearest, ties to even) and return the raw 16-bit patterns."""
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    u = x.view(np.uint32)
+    out = np.empty(x.shape, dtype=np.uint16)
+    flat_u, flat_o = u.reshape(-1), out.reshape(-1)
+
+    def work(lo, hi):
+        v = flat_u[lo:hi]
+        flat_o[lo:hi] = ((v + np.uint32(0x7FFF) + ((v >> np.uint32(16)) & np.uint32(1)))
+                         >> np.uint32(16)).astype(np.uint16)
+
+    n = flat_u.size
+    step = max(_CHUNK, -(-n // _threads()))
+    with ThreadPoolExecutor(_threads()) as ex:
+        list(ex.map(lambda lo: work(lo, min(n, lo + step)), range(0, n, step)))
+    return out
+
+
+def bf16_bits_to_f32(b: np.ndarray) -> np.ndarray:
+    return (b.astype(np.uint32) << np.uint32(16)).view(np.float32)
+
+
+def normal_chunks(seed: int, stream: int, n: int) -> np.ndarray:
+    """n standard normals, chunk c drawn from SeedSequence([seed, stream, c])."""
+    out = np.empty(n, dtype=np.float32)
+
+    def fill(c):
+        lo = c * _CHUNK
+        hi = min(n, lo + _CHUNK)
+        _rng(seed, stream, c).standard_normal(hi - lo, dtype=np.float32, out=out[lo:hi])
+
+    with ThreadPoolExecutor(_threads()) as ex:
+        list(ex.map(fill, range(-(-n // _CHUNK))))
+    return out
+
+
+def page_table(cfg, n_logical: int | None = None) -> np.ndarray:
+    """Logical page -> physical page id (int32)."""
+    n_logical = cfg.n_logical_pages if n_logical is None else n_logical
+    rng = _rng(cfg.seed, STREAM_TABLE)
+    if cfg.table == "identity":
+        t = np.arange(n_logical)
+    elif cfg.table == "perm":
+        t = rng.permutation(cfg.n_phys_pages)[:n_logical]
+    elif cfg.table == "sample":
+        t = rng.choice(cfg.n_phys_pages, size=n_logical, replace=False)
+    else:
+        raise ValueError(cfg.table)
+    return t.astype(np.int32)
+
+
+def _pool(cfg, stream: int, width: int, n_heads: int, plants=None) -> np.ndarray:
+    """Physical pool [n_phys, S, n_heads, width] filled page by page.
+
+    ``plants`` maps physical page -> list of (slot, head, fp32 vector) additions made
+    before rounding."""
+    S = cfg.page_size
+    per_page = S * n_heads * width
+    bf16 = cfg.dtype == "bf16"
+    out = np.empty((cfg.n_phys_pages, S, n_heads, width), dtype=np.uint16 if bf16 else np.float32)
+
+    def fill(p):
+        x = _rng(cfg.seed, stream, p).standard_normal(per_page, dtype=np.float32)
+        x = x.reshape(S, n_heads, width)
+        if plants is not None and p in plants:
+            for slot, g, vec in plants[p]:
+                x[slot, g] += vec
+        if bf16:
+            u = x.view(np.uint32)
+            out[p] = ((u + np.uint32(0x7FFF) + ((u >> np.uint32(16)) & np.uint32(1)))
+                      >> np.uint32(16)).astype(np.uint16)
+        else:
+            out[p] = x
+
+    with ThreadPoolExecutor(_threads()) as ex:
+        list(ex.map(fill, range(cfg.n_phys_pages)))
+    return out
+
+
+def _dense_tensor(cfg, stream: int, shape) -> np.ndarray:
+    x = normal_chunks(cfg.seed, stream, int(np.prod(shape))).reshape(shape)
+    return to_bf16_bits(x) if cfg.dtype == "bf16" else x
+
+
+def plant_targets(cfg, q_f32: np.ndarray, table: np.ndarray):
+    """Planted prefix keys: returns (positions, target rows, target heads) and the
+    per-physical-page additions used while drawing the K pool."""
+    n = int(round(cfg.plant_frac * cfg.prefix_len))
+    if n == 0:
+        return None, None
+    rng = _rng(cfg.seed, STREAM_PLANT)
+    pos = np.sort(rng.choice(cfg.prefix_len, size=n, replace=False))
+    rows = rng.integers(0, cfg.resp_len, size=n)
+    heads = rng.integers(0, cfg.n_q_heads, size=n)
+    plants: dict[int, list] = {}
+    for j, t, h in zip(pos.tolist(), rows.tolist(), heads.tolist()):
+        p = int(table[j // cfg.page_size])
+        plants.setdefault(p, []).append(
+            (j % cfg.page_size, h // cfg.group, cfg.plant_gain * q_f32[t, h]))
+    return (pos, rows, heads), plants
+
+
+def dense_inputs(cfg, with_dout: bool = True) -> dict:
+    """q [R,Hq,D], k_pool/v_pool [n_phys,S,Hkv,D|Dv], page_table [n_logical], d_out [R,Hq,Dv].
+
+    bf16 tensors are returned as uint16 bit patterns, fp32 ones as float32."""
+    R, Hq, Hkv = cfg.resp_len, cfg.n_q_heads, cfg.n_kv_heads
+    table = page_table(cfg)
+    q = _dense_tensor(cfg, STREAM_Q, (R, Hq, cfg.head_dim))
+    q_f32 = bf16_bits_to_f32(q) if cfg.dtype == "bf16" else q
+    planted, plants = plant_targets(cfg, q_f32, table)
+    k_pool = _pool(cfg, STREAM_K, cfg.head_dim, Hkv, plants)
+    v_pool = _pool(cfg, STREAM_V, cfg.head_dim_v, Hkv)
+    out = dict(q=q, k_pool=k_pool, v_pool=v_pool, page_table=table, planted=planted)
+    if with_dout:
+        out["d_out"] = _dense_tensor(cfg, STREAM_DO, (R, Hq, cfg.head_dim_v))
+    return out
+
+
+def sparse_indices(cfg) -> np.ndarray:
+    """[R, topk] int32: per query row, topk distinct prefix positions in ascending order."""
+    R, k, P = cfg.resp_len, cfg.topk, cfg.prefix_len
+    if k > P:
+        raise ValueError("topk exceeds the prefix")
+    out = np.empty((R, k), dtype=np.int32)
+
+    def fill(t):
+        rng = _rng(cfg.seed, STREAM_IDX, t)
+        got = np.empty(0, dtype=np.int64)
+        while got.size < k:
+            extra = rng.integers(0, P, size=k + 64)
+            got = np.unique(np.concatenate([got, extra]))
+        sel = rng.choice(got.size, size=k, replace=False)
+        out[t] = np.sort(got[sel])
+
+    with ThreadPoolExecutor(_threads()) as ex:
+        list(ex.map(fill, range(R)))
+    return out
+
+
+def sparse_inputs(cfg, with_dout: bool = True) -> dict:
+    """q [R,H,Dk], latent_pool [n_phys,S,1,Dk] (keys = all Dk channels, values = the
+    first Dv), page_table, idx [R,topk], d_out [R,H,Dv]."""
+    R, H = cfg.resp_len, cfg.n_q_heads
+    table = page_table(cfg)
+    q = _dense_tensor(cfg, STREAM_Q, (R, H, cfg.head_dim))
+    latent = _pool(cfg, STREAM_K, cfg.head_dim, 1)
+    out = dict(q=q, latent_pool=latent, page_table=table, idx=sparse_indices(cfg))
+    if with_dout:
+        out["d_out"] = _dense_tensor(cfg, STREAM_DO, (R, H, cfg.head_dim_v))
+    return out
