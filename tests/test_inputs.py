@@ -16,11 +16,11 @@ def test_c1_shapes_and_determinism():
 
 
 def test_bf16_rounding_is_nearest_even():
-    x = np.array([1.0, 1.0 + 2 ** -8, 1.0 + 3 * 2 ** -8, -2.5, 1.0 + 2 ** -7 + 2 ** -9],
+    x = np.array([1.0, 1.0 + 2 ** -8, 1.0 + 3 * 2 ** -8, -2.5, 1.0 + 2 ** -8 + 2 ** -10],
                  dtype=np.float32)
     got = inputs.bf16_bits_to_f32(inputs.to_bf16_bits(x))
     # ties go to the even mantissa; above-half rounds up
-    assert got.tolist() == [1.0, 1.0, 1.0 + 2 ** -6, -2.5, 1.0 + 2 ** -6]
+    assert got.tolist() == [1.0, 1.0, 1.0 + 2 ** -6, -2.5, 1.0 + 2 ** -7]
 
 
 def test_tables_are_injective():
