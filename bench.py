@@ -1,0 +1,213 @@
+#!/usr/bin/env python3
+"""Response-replay attention benchmark on one MI355X.
+
+One step = the whole replay hot path over one batch of synthetic input: the
+split-KV forward over a 2,097,152-position paged bf16 prefix (8 contiguous
+shards x 4 splits + the causal response split), the two-level LSE merge, and
+the backward (dq accumulated over the shards, response dK/dV).  Inputs are
+resident in HBM before the timed region.  Prints one JSON line.
+
+FLOP convention: fwd = 4*Hq*D*sum_i |V_i|; bwd = Hq*D*(6*sum_i |V_i & prefix| +
+10*sum_i |V_i & response|) (recompute counted, prefix dK/dV not counted).
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import platform
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "replay attention TFLOP/s (fwd+bwd) & % of bf16 MFMA peak at 2M-position prefix"
+PEAK_BF16_TFLOPS = 2500.0
+PEAK_HBM_GBS = 8000.0
+
+
+def visible_counts(cfg):
+    """sum_i |V_i & prefix| and sum_i |V_i & response| over the response rows."""
+    R, P = cfg.resp_len, cfg.prefix_len
+    return R * P, R * (R + 1) // 2
+
+
+def flops(cfg):
+    pre, resp = visible_counts(cfg)
+    Hq, D = cfg.n_q_heads, cfg.head_dim
+    fwd = 4 * Hq * D * (pre + resp)
+    bwd = Hq * D * (6 * pre + 10 * resp)
+    return fwd, bwd
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def cpu_baseline(cfg, host, n_rows=4):
+    """The fp64 oracle as it stands, on this host's cores, over a bounded sample:
+    forward and dq of the first n_rows query rows (all heads) against the full prefix."""
+    import numpy as np
+    import oracle as O
+    try:
+        from threadpoolctl import threadpool_info
+        blas_threads = max((i.get("num_threads", 1) for i in threadpool_info()), default=1)
+    except Exception:  # pragma: no cover
+        blas_threads = os.cpu_count() or 1
+    rows = np.arange(n_rows)
+    kw = dict(page_size=cfg.page_size, q_pos0=cfg.q_pos0, scale=cfg.scale)
+    t0 = time.perf_counter()
+    o, l = O.attn_fwd(host["q"], host["k_pool"], host["v_pool"], host["page_table"], rows=rows, **kw)
+    R, Hq, Dv = cfg.resp_len, cfg.n_q_heads, cfg.head_dim_v
+    o_full = np.zeros((R, Hq, Dv))
+    l_full = np.zeros((Hq, R))
+    o_full[rows], l_full[:, rows] = o, l
+    O.attn_bwd(host["q"], host["k_pool"], host["v_pool"], host["page_table"], host["d_out"],
+               rows=rows, resp_keys=np.zeros(0, np.int64), out=o_full, lse=l_full,
+               prefix_len=cfg.prefix_len, **kw)
+    dt = time.perf_counter() - t0
+    vis = sum(cfg.prefix_len + i + 1 for i in rows)
+    fl = (4 + 6) * Hq * cfg.head_dim * vis
+    return {"value": fl / dt / 1e12, "unit": "TFLOP/s", "cores": int(blas_threads),
+            "kind": "oracle",
+            "sample": f"fp64 numpy oracle: forward + dq of query rows 0..{n_rows - 1} (all "
+                      f"{Hq} heads) over the full {cfg.kv_len}-key paged store; "
+                      f"{fl / 1e9:.1f} GFLOP in {dt:.1f} s",
+            "seconds": dt}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--config", default="c3")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-rows", type=int, default=4)
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU: this build has no multi-GPU path "
+              "(--gpus must be 1)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2607_14952_amd import binding, configs, inputs
+    from paper_2607_14952_amd.replay import ReplayStep, device_inputs
+
+    binding.load_library()
+    if not torch.cuda.is_available():
+        print("no GPU visible", file=sys.stderr)
+        sys.exit(1)
+    cfg = configs.get(args.config)
+    log(f"generating inputs for {cfg.name}")
+    t = time.perf_counter()
+    host = inputs.dense_inputs(cfg)
+    log(f"inputs ready in {time.perf_counter() - t:.1f} s; copying to HBM")
+    dev = device_inputs(host)
+    stream = torch.cuda.current_stream()
+    step = ReplayStep(cfg, dev, backward=True, stream=stream)
+    fwd_fl, bwd_fl = flops(cfg)
+
+    for w in range(args.warmup):
+        step.step()
+        torch.cuda.synchronize()
+        log(f"warmup {w + 1}/{args.warmup} done")
+
+    E = lambda: torch.cuda.Event(enable_timing=True)  # noqa: E731
+    n_r = len(step.shards)
+    ev = [[E() for _ in range(3 + n_r + 1)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for s in range(args.steps):
+        e = ev[s]
+        e[0].record(stream)
+        step.forward_splits()
+        e[1].record(stream)
+        step.merge()
+        e[2].record(stream)
+        for r in range(n_r):
+            step.backward_range(r)
+            e[3 + r].record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    log(f"timed {args.steps} steps in {wall:.3f} s")
+
+    fwd_ms = [e[0].elapsed_time(e[1]) for e in ev]
+    merge_ms = [e[1].elapsed_time(e[2]) for e in ev]
+    bwd_ms = [[e[2 + r].elapsed_time(e[3 + r]) for r in range(n_r)] for e in ev]
+    step_ms = [e[0].elapsed_time(e[3 + n_r - 1]) for e in ev]
+    ms_per_step = wall * 1e3 / args.steps
+    value = (fwd_fl + bwd_fl) / (ms_per_step * 1e-3) / 1e12
+
+    avg = lambda xs: sum(xs) / len(xs)  # noqa: E731
+    fwd_avg = avg(fwd_ms)
+    pre_ranges = [r for r, (b, e) in enumerate(step.shards) if e <= cfg.prefix_len]
+    dq_launch_ms = avg([bwd_ms[s][r] for s in range(args.steps) for r in pre_ranges])
+    shard_len = step.shards[pre_ranges[0]][1] - step.shards[pre_ranges[0]][0]
+    dq_launch_fl = 6 * cfg.n_q_heads * cfg.head_dim * cfg.resp_len * shard_len
+    fwd_tf = fwd_fl / (fwd_avg * 1e-3) / 1e12
+    dq_tf = dq_launch_fl / (dq_launch_ms * 1e-3) / 1e12
+    fwd_total, dq_total = fwd_avg, dq_launch_ms * len(pre_ranges)
+    if fwd_total >= dq_total:
+        roof = {"kernel": "fwd_bf16_d256_kernel (all 33 splits, one launch)",
+                "achieved": fwd_tf, "flop_per_launch": fwd_fl, "avg_launch_ms": fwd_avg}
+    else:
+        roof = {"kernel": "bwd_dq_bf16_d256_kernel (one 262,144-key shard per launch)",
+                "achieved": dq_tf, "flop_per_launch": dq_launch_fl, "avg_launch_ms": dq_launch_ms}
+    roofline = {"bound": "mfma", "achieved": round(roof["achieved"], 2),
+                "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                "frac": round(roof["achieved"] / PEAK_BF16_TFLOPS, 4), "traffic": None,
+                "kernel": roof["kernel"], "flop_per_launch": roof["flop_per_launch"],
+                "avg_launch_ms": round(roof["avg_launch_ms"], 3)}
+    # merge bytes: split partials read + shard results written and re-read + output
+    R, Hq, Dv = cfg.resp_len, cfg.n_q_heads, cfg.head_dim_v
+    ns, nsh = len(step.splits), len(step.shards)
+    merge_bytes = (ns * R * Hq * (Dv + 1) * 4 + nsh * R * Hq * (Dv + 1) * 4 * 2
+                   + R * Hq * (Dv * 2 + 4))
+    result = {
+        "metric": METRIC,
+        "value": round(value, 2),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 3),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": f"{cfg.name}: bf16 GQA {cfg.n_q_heads}q/{cfg.n_kv_heads}kv, "
+                               f"head_dim {cfg.head_dim}, prefix {cfg.prefix_len} in "
+                               f"{cfg.page_size}-position pages (seeded permutation), "
+                               f"{cfg.n_shards} shards x {cfg.splits_per_shard} splits + "
+                               f"response split, response {cfg.resp_len} causal, fwd+bwd",
+                   "prefix_len": cfg.prefix_len, "resp_len": cfg.resp_len,
+                   "n_q_heads": cfg.n_q_heads, "n_kv_heads": cfg.n_kv_heads,
+                   "head_dim": cfg.head_dim, "page_size": cfg.page_size,
+                   "splits": ns, "shards": nsh, "parallelism": "single-gpu"},
+        "frac_of_peak": round(value / PEAK_BF16_TFLOPS, 4),
+        "roofline": roofline,
+        "phases_ms": {"fwd_splits": round(fwd_avg, 3), "merge": round(avg(merge_ms), 3),
+                      "bwd_ranges": [round(avg([b[r] for b in bwd_ms]), 3) for r in range(n_r)],
+                      "step_events": round(avg(step_ms), 3)},
+        "fwd_tflops": round(fwd_tf, 2),
+        "dq_tflops": round(dq_tf, 2),
+        "merge_gbs": round(merge_bytes / (avg(merge_ms) * 1e-3) / 1e9, 1),
+        "flop_per_step": {"fwd": fwd_fl, "bwd": bwd_fl},
+        "gpu": torch.cuda.get_device_name(0),
+    }
+    if not args.no_cpu_baseline:
+        del dev, step
+        torch.cuda.empty_cache()
+        log("timing the CPU oracle sample")
+        cb = cpu_baseline(cfg, host, args.cpu_rows)
+        cb["cpu"] = platform.processor() or platform.machine()
+        result["cpu_baseline"] = {k: (round(v, 6) if isinstance(v, float) else v)
+                                  for k, v in cb.items()}
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,183 @@
+/*
+ * longstraw.h -- C ABI of the MI355X response-replay attention library.
+ *
+ * A response suffix of n_q query tokens (causal among themselves) attends
+ * exactly over a paged KV store whose first prefix_len positions are a
+ * retained, stop-gradient prefix (paper, Sec. "Conditional Replay as an
+ * Efficiency Boundary", Eq. gradient-boundary).  Query row i sits at logical
+ * position q_pos0 + i and sees key position j iff j <= q_pos0 + i.  Query head
+ * h reads KV head h / (n_q_heads / n_kv_heads).  Scores are
+ * s_ij = softmax_scale * q_i . k_j.
+ *
+ * Memory and ownership
+ *   - Every pointer argument named as device memory is a device address owned
+ *     by the caller; the library allocates nothing and keeps no reference after
+ *     a call returns.  Host arrays (splits) are read before the call returns.
+ *   - Pools and the page table are read-only to the library.
+ *   - All device pointers must be 16-byte aligned.
+ *   - Calls are asynchronous and ordered on `stream` (a hipStream_t passed as
+ *     void*, NULL = the null stream).  Only LS_FLAG_CHECKED synchronizes.
+ *
+ * Layouts (row-major, innermost last)
+ *   q          [n_q, n_q_heads, head_dim]              dtype
+ *   k_pool     [n_phys_pages, page_size, n_kv_heads, head_dim]   dtype
+ *   v_pool     [n_phys_pages, page_size, n_kv_heads, head_dim_v] dtype
+ *   page_table [n_logical_pages] int32: logical page -> physical page.
+ *              Logical position j lives at (page_table[j / page_size], j % page_size)
+ *              (Sec. "From Logical Shards to Physical Pages").
+ *   out_part   [n_splits, n_q, n_q_heads, head_dim_v] fp32 (normalized)
+ *   lse_part   [n_splits, n_q_heads, n_q] fp32 (natural log)
+ *   out        [n_q, n_q_heads, head_dim_v]  bf16 or fp32
+ *   lse        [n_q_heads, n_q] fp32
+ *   d_out      [n_q, n_q_heads, head_dim_v]  dtype
+ *   dq         [n_q, n_q_heads, head_dim] fp32
+ *   dk_resp    [kv_len - prefix_len, n_kv_heads, head_dim]   fp32, row j - prefix_len
+ *   dv_resp    [kv_len - prefix_len, n_kv_heads, head_dim_v] fp32
+ *
+ * Errors
+ *   Every entry point returns an ls_status; 0 is success.  All argument checks
+ *   run on the host before anything is launched, so a rejected call has no
+ *   effect.  ls_last_error() returns a thread-local description of the last
+ *   failure.  A device fault surfaces at the caller's next synchronization.
+ *   Without LS_FLAG_CHECKED a page-table entry outside [0, n_phys_pages) is
+ *   undefined behaviour.
+ *
+ * Supported shapes: dtype LS_F32 with head_dim, head_dim_v <= 256 (any GQA
+ * group); dtype LS_BF16 with head_dim = head_dim_v = 256 and n_q_heads /
+ * n_kv_heads dividing 32.
+ */
+#ifndef LONGSTRAW_H
+#define LONGSTRAW_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define LS_ABI_VERSION 1
+
+typedef enum {
+  LS_OK = 0,
+  LS_ERR_INVALID_ARG = -1, /* null/misaligned pointer, bad shape, bad ranges */
+  LS_ERR_UNSUPPORTED = -2, /* (dtype, head_dim, group) without a kernel */
+  LS_ERR_WORKSPACE = -3,   /* workspace missing or too small */
+  LS_ERR_ALIAS = -4,       /* an output overlaps an input or another output */
+  LS_ERR_STALE = -5,       /* pool_epoch != expected_epoch */
+  LS_ERR_PAGE_OOB = -6,    /* checked mode: page id outside [0, n_phys_pages) */
+  LS_ERR_HIP = -7          /* the HIP runtime reported an error */
+} ls_status;
+
+typedef enum { LS_BF16 = 0, LS_F32 = 1 } ls_dtype;
+
+enum {
+  LS_FLAG_CHECKED = 1u,        /* validate the page table (synchronous D2H copy) */
+  LS_FLAG_ACCUMULATE_DQ = 4u,  /* backward: dq += contribution instead of dq = */
+  LS_FLAG_ACCUMULATE_DKV = 8u  /* backward: dk/dv_resp += instead of = */
+};
+
+/* One replay call: a block of n_q response rows against one paged KV store. */
+typedef struct {
+  int32_t abi_version; /* must equal LS_ABI_VERSION */
+  int32_t dtype;       /* ls_dtype of q, k_pool, v_pool, d_out */
+  int32_t n_q;         /* query rows in this call (>= 0) */
+  int32_t n_q_heads;
+  int32_t n_kv_heads;  /* divides n_q_heads */
+  int32_t head_dim;    /* D, key/query width */
+  int32_t head_dim_v;  /* Dv, value width */
+  int32_t page_size;   /* S, positions per page (> 0) */
+  int64_t n_phys_pages;
+  int64_t n_logical_pages;
+  int64_t prefix_len;  /* positions < prefix_len are stop-gradient (no dK/dV) */
+  int64_t q_pos0;      /* logical position of query row 0; prefix_len <= q_pos0 */
+  float softmax_scale;
+  uint32_t flags;
+  const void* q;             /* device */
+  const void* k_pool;        /* device */
+  const void* v_pool;        /* device */
+  const int32_t* page_table; /* device */
+  uint64_t pool_epoch;       /* version of the pool contents ...            */
+  uint64_t expected_epoch;   /* ... must match what the caller captured on   */
+} ls_attn_params;
+
+/* A logical key range [kv_begin, kv_end). */
+typedef struct {
+  int64_t kv_begin;
+  int64_t kv_end;
+} ls_split;
+
+int ls_abi_version(void);
+const char* ls_status_string(int32_t status);
+const char* ls_last_error(void);
+
+/*
+ * ls_gather_kv: copy logical positions [pos_begin, pos_end) of the K and V
+ * pools into dense device buffers k_out [n, n_kv_heads, head_dim] and
+ * v_out [n, n_kv_heads, head_dim_v] (n = pos_end - pos_begin), bit for bit.
+ * Exposes the page-table walk of the attention kernels on its own (the
+ * logical-to-physical page map, Sec. "From Logical Shards to Physical Pages").
+ * Requires 0 <= pos_begin <= pos_end <= n_logical_pages * page_size.
+ */
+ls_status ls_gather_kv(const ls_attn_params* p, int64_t pos_begin, int64_t pos_end,
+                       void* k_out, void* v_out, void* stream);
+
+/*
+ * ls_prefix_attn_fwd: for every split r and row i, the normalized local
+ * output and natural-log normalizer over the keys of the split visible to
+ * the row (Eq. qwen-local-attn):
+ *     l_r,i = log sum_{j in split, j <= q_pos0+i} exp(s_ij)
+ *     o_r,i = sum exp(s_ij) v_j / exp(l_r,i)
+ * A row that sees no key of a split gets o = 0, l = -inf.  Splits are
+ * disjoint, sorted, non-empty ranges within [0, q_pos0 + n_q); they need not
+ * cover it (use several calls for several key partitions).  n_splits >= 1.
+ * out_part and lse_part are device buffers in the layouts above.
+ */
+ls_status ls_prefix_attn_fwd(const ls_attn_params* p, const ls_split* splits, int32_t n_splits,
+                             float* out_part, float* lse_part, void* stream);
+
+/*
+ * ls_lse_merge: compose n_splits partial results (Eq. qwen-lse-parts and
+ * Eq. qwen-global-attn):
+ *     m = max_r l_r,  a = sum_r exp(l_r - m),  n = sum_r exp(l_r - m) o_r,
+ *     o = n / a,      l = m + log a
+ * Parts with l_r = -inf carry weight 0; a row whose every part is empty gets
+ * o = 0 and l = -inf.  out_dtype is LS_BF16 or LS_F32 (an fp32 result can be
+ * merged again: the merge is associative).  out_part/lse_part as produced by
+ * ls_prefix_attn_fwd with n_q_heads = n_heads and head_dim_v = dv.  flags must
+ * be 0.
+ */
+ls_status ls_lse_merge(const float* out_part, const float* lse_part, int32_t n_splits,
+                       int32_t n_q, int32_t n_heads, int32_t dv, int32_t out_dtype,
+                       void* out, float* lse, uint32_t flags, void* stream);
+
+/* Bytes of device workspace ls_prefix_attn_bwd needs for these params. */
+size_t ls_prefix_attn_bwd_workspace_size(const ls_attn_params* p);
+
+/*
+ * ls_prefix_attn_bwd: gradients of L = sum(d_out * O), where O / lse are the
+ * merged forward results over every visible key (out in out_dtype, lse fp32),
+ * restricted to the keys in [kv_begin, kv_end):
+ *   dq      += or = scale * sum_j dS_ij k_j  over keys of the range,
+ *              with P_ij = exp(s_ij - lse_i), Delta_i = d_out_i . out_i,
+ *              dS_ij = P_ij (d_out_i . v_j - Delta_i);
+ *              the contributions of a partition of the keys sum to the full
+ *              dq (Eq. qwen-dq-reduce);
+ *   dk_resp, dv_resp: for response keys j >= prefix_len in the range,
+ *              dv_j = sum_i P_ij d_out_i,  dk_j = scale * sum_i dS_ij q_i,
+ *              written at row j - prefix_len; prefix keys get nothing
+ *              (Eq. gradient-boundary and the lazy gradient pages).
+ * dk_resp/dv_resp may both be NULL when the range holds no response key.
+ * LS_FLAG_ACCUMULATE_DQ / LS_FLAG_ACCUMULATE_DKV select += over =.
+ * workspace: device memory of ls_prefix_attn_bwd_workspace_size() bytes.
+ */
+ls_status ls_prefix_attn_bwd(const ls_attn_params* p, int64_t kv_begin, int64_t kv_end,
+                             const void* d_out, const void* out, int32_t out_dtype,
+                             const float* lse, float* dq, float* dk_resp, float* dv_resp,
+                             void* workspace, size_t workspace_bytes, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* LONGSTRAW_H */

@@ -1,0 +1,239 @@
+"""Thin Python binding of ``liblongstraw.so`` (argument marshalling only).
+
+Torch tensors supply device memory and the stream; every step of the replay
+path runs in the library's HIP kernels.  There is no fallback: if the library
+is missing or a call fails, an exception is raised.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from ctypes import POINTER, c_float, c_int32, c_int64, c_size_t, c_uint32, c_uint64, c_void_p
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "liblongstraw.so")
+
+ABI_VERSION = 1
+LS_BF16, LS_F32 = 0, 1
+FLAG_CHECKED = 1
+FLAG_ACCUMULATE_DQ = 4
+FLAG_ACCUMULATE_DKV = 8
+STATUS = {0: "LS_OK", -1: "LS_ERR_INVALID_ARG", -2: "LS_ERR_UNSUPPORTED", -3: "LS_ERR_WORKSPACE",
+          -4: "LS_ERR_ALIAS", -5: "LS_ERR_STALE", -6: "LS_ERR_PAGE_OOB", -7: "LS_ERR_HIP"}
+EXPORTS = ["ls_abi_version", "ls_status_string", "ls_last_error", "ls_gather_kv",
+           "ls_prefix_attn_fwd", "ls_lse_merge", "ls_prefix_attn_bwd_workspace_size",
+           "ls_prefix_attn_bwd"]
+
+
+class AttnParams(ctypes.Structure):
+    _fields_ = [("abi_version", c_int32), ("dtype", c_int32), ("n_q", c_int32),
+                ("n_q_heads", c_int32), ("n_kv_heads", c_int32), ("head_dim", c_int32),
+                ("head_dim_v", c_int32), ("page_size", c_int32), ("n_phys_pages", c_int64),
+                ("n_logical_pages", c_int64), ("prefix_len", c_int64), ("q_pos0", c_int64),
+                ("softmax_scale", c_float), ("flags", c_uint32), ("q", c_void_p),
+                ("k_pool", c_void_p), ("v_pool", c_void_p), ("page_table", c_void_p),
+                ("pool_epoch", c_uint64), ("expected_epoch", c_uint64)]
+
+
+class Split(ctypes.Structure):
+    _fields_ = [("kv_begin", c_int64), ("kv_end", c_int64)]
+
+
+class LongStrawError(RuntimeError):
+    def __init__(self, status: int, detail: str):
+        super().__init__(f"{STATUS.get(status, status)}: {detail}")
+        self.status = status
+        self.name = STATUS.get(status, str(status))
+
+
+_lib = None
+
+
+def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
+    """Load the HIP library (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise FileNotFoundError(
+            f"{path} not found: build it with `python -m paper_2607_14952_amd.build`")
+    lib = ctypes.CDLL(path)
+    P = POINTER(AttnParams)
+    lib.ls_abi_version.restype = c_int32
+    lib.ls_status_string.restype = ctypes.c_char_p
+    lib.ls_status_string.argtypes = [c_int32]
+    lib.ls_last_error.restype = ctypes.c_char_p
+    lib.ls_gather_kv.restype = c_int32
+    lib.ls_gather_kv.argtypes = [P, c_int64, c_int64, c_void_p, c_void_p, c_void_p]
+    lib.ls_prefix_attn_fwd.restype = c_int32
+    lib.ls_prefix_attn_fwd.argtypes = [P, POINTER(Split), c_int32, c_void_p, c_void_p, c_void_p]
+    lib.ls_lse_merge.restype = c_int32
+    lib.ls_lse_merge.argtypes = [c_void_p, c_void_p, c_int32, c_int32, c_int32, c_int32, c_int32,
+                                 c_void_p, c_void_p, c_uint32, c_void_p]
+    lib.ls_prefix_attn_bwd_workspace_size.restype = c_size_t
+    lib.ls_prefix_attn_bwd_workspace_size.argtypes = [P]
+    lib.ls_prefix_attn_bwd.restype = c_int32
+    lib.ls_prefix_attn_bwd.argtypes = [P, c_int64, c_int64, c_void_p, c_void_p, c_int32, c_void_p,
+                                       c_void_p, c_void_p, c_void_p, c_void_p, c_size_t, c_void_p]
+    if lib.ls_abi_version() != ABI_VERSION:
+        raise RuntimeError("liblongstraw ABI version mismatch")
+    _lib = lib
+    return lib
+
+
+def check(status: int) -> None:
+    if status != 0:
+        raise LongStrawError(status, load_library().ls_last_error().decode())
+
+
+# ----------------------------------------------------------------- torch helpers
+def _torch():
+    import torch
+    return torch
+
+
+def _ptr(t):
+    return None if t is None else t.data_ptr()
+
+
+def _stream(stream):
+    torch = _torch()
+    s = torch.cuda.current_stream() if stream is None else stream
+    return s.cuda_stream
+
+
+def _dtype_code(t) -> int:
+    torch = _torch()
+    if t.dtype == torch.bfloat16:
+        return LS_BF16
+    if t.dtype == torch.float32:
+        return LS_F32
+    raise TypeError(f"unsupported dtype {t.dtype}")
+
+
+class PagedKV:
+    """A paged KV store: pools [n_phys, S, Hkv, D|Dv] and an int32 page table,
+    all device tensors owned by the caller (read-only to the library)."""
+
+    def __init__(self, k_pool, v_pool, page_table, epoch: int = 0):
+        self.k_pool, self.v_pool, self.page_table = k_pool, v_pool, page_table
+        self.epoch = epoch
+
+    @property
+    def page_size(self):
+        return self.k_pool.shape[1]
+
+
+def make_params(q, kv: PagedKV, *, n_q=None, n_q_heads=None, prefix_len: int, q_pos0: int,
+                scale: float, flags: int = 0, expected_epoch=None) -> AttnParams:
+    p = AttnParams()
+    p.abi_version = ABI_VERSION
+    p.dtype = _dtype_code(kv.k_pool)
+    p.n_q = q.shape[0] if n_q is None else n_q
+    p.n_q_heads = q.shape[1] if n_q_heads is None else n_q_heads
+    p.n_kv_heads = kv.k_pool.shape[2]
+    p.head_dim = kv.k_pool.shape[3]
+    p.head_dim_v = kv.v_pool.shape[3]
+    p.page_size = kv.k_pool.shape[1]
+    p.n_phys_pages = kv.k_pool.shape[0]
+    p.n_logical_pages = kv.page_table.shape[0]
+    p.prefix_len = prefix_len
+    p.q_pos0 = q_pos0
+    p.softmax_scale = scale
+    p.flags = flags
+    p.q = _ptr(q)
+    p.k_pool = _ptr(kv.k_pool)
+    p.v_pool = _ptr(kv.v_pool)
+    p.page_table = _ptr(kv.page_table)
+    p.pool_epoch = kv.epoch
+    p.expected_epoch = kv.epoch if expected_epoch is None else expected_epoch
+    return p
+
+
+# ----------------------------------------------------------------- entry points
+def gather_kv(kv: PagedKV, pos_begin: int, pos_end: int, *, flags: int = 0, stream=None):
+    """ls_gather_kv: dense copies of logical positions [pos_begin, pos_end)."""
+    torch = _torch()
+    n = pos_end - pos_begin
+    k = torch.empty((n,) + tuple(kv.k_pool.shape[2:]), dtype=kv.k_pool.dtype, device=kv.k_pool.device)
+    v = torch.empty((n,) + tuple(kv.v_pool.shape[2:]), dtype=kv.v_pool.dtype, device=kv.v_pool.device)
+    dummy_q = torch.empty((0, 1, 1), dtype=kv.k_pool.dtype, device=kv.k_pool.device)
+    p = make_params(dummy_q, kv, n_q=0, n_q_heads=kv.k_pool.shape[2], prefix_len=0, q_pos0=0,
+                    scale=1.0, flags=flags)
+    p.q = None
+    check(load_library().ls_gather_kv(ctypes.byref(p), pos_begin, pos_end, _ptr(k), _ptr(v),
+                                      _stream(stream)))
+    return k, v
+
+
+def prefix_attn_fwd(q, kv: PagedKV, splits, *, prefix_len: int, q_pos0: int, scale: float,
+                    flags: int = 0, out_part=None, lse_part=None, expected_epoch=None,
+                    stream=None):
+    """ls_prefix_attn_fwd: per-split normalized output [S, R, Hq, Dv] fp32 and
+    log-normalizer [S, Hq, R] fp32."""
+    torch = _torch()
+    R, Hq = q.shape[0], q.shape[1]
+    Dv = kv.v_pool.shape[3]
+    n = len(splits)
+    if out_part is None:
+        out_part = torch.empty((n, R, Hq, Dv), dtype=torch.float32, device=q.device)
+    if lse_part is None:
+        lse_part = torch.empty((n, Hq, R), dtype=torch.float32, device=q.device)
+    arr = (Split * n)(*[Split(int(b), int(e)) for b, e in splits])
+    p = make_params(q, kv, prefix_len=prefix_len, q_pos0=q_pos0, scale=scale, flags=flags,
+                    expected_epoch=expected_epoch)
+    check(load_library().ls_prefix_attn_fwd(ctypes.byref(p), arr, n, _ptr(out_part),
+                                            _ptr(lse_part), _stream(stream)))
+    return out_part, lse_part
+
+
+def lse_merge(out_part, lse_part, *, out_dtype=None, out=None, lse=None, flags: int = 0,
+              stream=None):
+    """ls_lse_merge over the leading (split) dimension."""
+    torch = _torch()
+    n, R, H, Dv = out_part.shape
+    out_dtype = torch.float32 if out_dtype is None else out_dtype
+    if out is None:
+        out = torch.empty((R, H, Dv), dtype=out_dtype, device=out_part.device)
+    if lse is None:
+        lse = torch.empty((H, R), dtype=torch.float32, device=out_part.device)
+    check(load_library().ls_lse_merge(_ptr(out_part), _ptr(lse_part), n, R, H, Dv,
+                                      _dtype_code(out), _ptr(out), _ptr(lse), flags,
+                                      _stream(stream)))
+    return out, lse
+
+
+def bwd_workspace(q, kv: PagedKV, **kw):
+    torch = _torch()
+    p = make_params(q, kv, prefix_len=0, q_pos0=0, scale=1.0)
+    n = load_library().ls_prefix_attn_bwd_workspace_size(ctypes.byref(p))
+    return torch.empty(max(n, 16), dtype=torch.uint8, device=q.device)
+
+
+def prefix_attn_bwd(q, kv: PagedKV, d_out, out, lse, *, prefix_len: int, q_pos0: int,
+                    scale: float, kv_begin: int = 0, kv_end=None, flags: int = 0, dq=None,
+                    dk_resp=None, dv_resp=None, workspace=None, expected_epoch=None,
+                    stream=None):
+    """ls_prefix_attn_bwd: dq over keys [kv_begin, kv_end) and dK/dV of the
+    response keys in that range (rows j - prefix_len of dk_resp / dv_resp)."""
+    torch = _torch()
+    R, Hq, D = q.shape
+    Hkv, Dv = kv.k_pool.shape[2], kv.v_pool.shape[3]
+    kv_len = q_pos0 + R
+    kv_end = kv_len if kv_end is None else kv_end
+    if dq is None:
+        dq = torch.empty((R, Hq, D), dtype=torch.float32, device=q.device)
+    if kv_end > prefix_len:
+        n_resp = kv_len - prefix_len
+        if dk_resp is None:
+            dk_resp = torch.zeros((n_resp, Hkv, D), dtype=torch.float32, device=q.device)
+        if dv_resp is None:
+            dv_resp = torch.zeros((n_resp, Hkv, Dv), dtype=torch.float32, device=q.device)
+    if workspace is None:
+        workspace = bwd_workspace(q, kv)
+    p = make_params(q, kv, prefix_len=prefix_len, q_pos0=q_pos0, scale=scale, flags=flags,
+                    expected_epoch=expected_epoch)
+    check(load_library().ls_prefix_attn_bwd(
+        ctypes.byref(p), kv_begin, kv_end, _ptr(d_out), _ptr(out), _dtype_code(out), _ptr(lse),
+        _ptr(dq), _ptr(dk_resp), _ptr(dv_resp), _ptr(workspace), workspace.numel(),
+        _stream(stream)))
+    return dq, dk_resp, dv_resp

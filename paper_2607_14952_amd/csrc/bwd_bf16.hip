@@ -1,0 +1,392 @@
+// bf16 backward for head_dim = 256 on gfx950 (prefix held as stop-gradient
+// state, Eq. gradient-boundary; dq composed over key ranges, Eq. qwen-dq-reduce).
+//
+// dq kernel: workgroup = 4 waves = 128 packed query rows of one KV head, lane
+// l owns row l % 32.  Per 32-key tile it recomputes S^T = K Q^T, forms
+// P = exp2(s*scale*log2e - lse2) with the merged log-normalizer, dP^T = V dO^T,
+// dS = P (dP - Delta) and accumulates dq^T += K^T dS^T.  K and V tiles are
+// staged in double-buffered LDS row-major (A operands of the first two
+// products) and K once more key-transposed (A operand of the third).
+//
+// dk/dv kernel: one wave per 32 response keys of one KV head; lane l owns key
+// l % 32.  Per block of 32 packed query rows it computes S = Q K^T and
+// dP = dO V^T (scores untransposed, rows in registers), then
+// dv^T += dO^T P and dk^T += Q^T dS with Q and dO staged row-major and
+// row-transposed in LDS.  Only keys >= prefix_len ever get a gradient.
+#include <math.h>
+
+#include "ls_internal.h"
+#include "mfma_common.h"
+
+namespace ls {
+namespace {
+
+constexpr int kD = 256;
+
+// ============================================================== dq kernel
+constexpr int kQBM = 128;
+constexpr int kQBN = 32;
+constexpr int kRowBytes = kD * 2;                 // 512 B: one key row
+constexpr int kTileBytes = kQBN * kRowBytes;      // 16 KiB
+constexpr int kQStage = 3 * kTileBytes;           // K, V row-major + K transposed
+
+struct DqRegs {
+  u32x4 k[4];   // keys 4m .. 4m+3 (m = lane & 7), chunk c = (lane >> 3) + 8*wave
+  u32x4 v[4];
+};
+
+__device__ __forceinline__ void dq_load(const BwdArgs& a, int g, int64_t t0, int64_t k_hi,
+                                        int tid, DqRegs& R) {
+  const int lane = tid & 63, w = tid >> 6;
+  const int m = lane & 7, c = (lane >> 3) + 8 * w;
+  const int64_t S = int64_t(1) << a.log2_page;
+  const bool one_page = ((t0 & (S - 1)) + kQBN) <= S;
+  int64_t base = 0;
+  if (one_page) base = phys_pos(a.page_table, t0, a.log2_page);
+  const __bf16* kp = static_cast<const __bf16*>(a.k_pool) + (int64_t)g * kD + c * 8;
+  const __bf16* vp = static_cast<const __bf16*>(a.v_pool) + (int64_t)g * kD + c * 8;
+  const u32x4 zero = {0u, 0u, 0u, 0u};
+#pragma unroll
+  for (int kk = 0; kk < 4; ++kk) {
+    const int key = 4 * m + kk;
+    const int64_t j = t0 + key;
+    if (j < k_hi) {
+      const int64_t pr = one_page ? base + key : phys_pos(a.page_table, j, a.log2_page);
+      R.k[kk] = *reinterpret_cast<const u32x4*>(kp + pr * a.k_pos_stride);
+      R.v[kk] = *reinterpret_cast<const u32x4*>(vp + pr * a.v_pos_stride);
+    } else {
+      R.k[kk] = zero;
+      R.v[kk] = zero;
+    }
+  }
+}
+
+__device__ __forceinline__ void dq_store(char* stage, int tid, const DqRegs& R) {
+  const int lane = tid & 63, w = tid >> 6;
+  const int m = lane & 7, c = (lane >> 3) + 8 * w;
+  char* Ks = stage;
+  char* Vs = stage + kTileBytes;
+  char* Kt = stage + 2 * kTileBytes;
+#pragma unroll
+  for (int kk = 0; kk < 4; ++kk) {
+    const int key = 4 * m + kk;
+    const int off = key * kRowBytes + ((c ^ (key & 7)) << 4);
+    *reinterpret_cast<u32x4*>(Ks + off) = R.k[kk];
+    *reinterpret_cast<u32x4*>(Vs + off) = R.v[kk];
+  }
+  // K^T [d][32 key slots], 64 B per d row, 16-byte chunk x stored at x ^ ((d >> 1) & 3)
+  const int slot = swap23(4 * m);
+  const int sc = slot >> 3, sb = (slot & 7) * 2;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    const int d = 8 * c + e;
+    const int dw = e >> 1;
+    const u32x2 val = pick4(R.k[0][dw], R.k[1][dw], R.k[2][dw], R.k[3][dw], (e & 1) != 0);
+    *reinterpret_cast<u32x2*>(Kt + d * (kQBN * 2) + ((sc ^ ((d >> 1) & 3)) << 4) + sb) = val;
+  }
+}
+
+__global__ __launch_bounds__(256, 1) void bwd_dq_bf16_d256_kernel(BwdArgs a) {
+  __shared__ __attribute__((aligned(16))) char smem[2 * kQStage];
+
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int l32 = lane & 31, hh = lane >> 5;
+  const int g = blockIdx.y;
+  const int lg = a.log2_group;
+  const int rows_total = a.n_q << lg;
+  const int row0 = blockIdx.x * kQBM;
+  const int prow = row0 + w * 32 + l32;
+  const bool row_ok = prow < rows_total;
+  const int tok = prow >> lg;
+  const int head = (g << lg) + (prow & ((1 << lg) - 1));
+  const int tok_first = row0 >> lg;
+  const int tok_last = min(a.n_q - 1, (row0 + kQBM - 1) >> lg);
+  const int64_t kb = a.kv_begin;
+  const int64_t k_hi = min(a.kv_end, a.q_pos0 + tok_last + 1);
+  const int64_t k_all = min(a.kv_end, a.q_pos0 + tok_first + 1);
+  const int64_t my_lim = min(a.kv_end, a.q_pos0 + tok + 1);
+  const int n_tiles = k_hi > kb ? (int)((k_hi - kb + kQBN - 1) / kQBN) : 0;
+
+  float* dq = a.dq + ((int64_t)tok * a.n_q_heads + head) * kD;
+  if (n_tiles == 0) {
+    if (row_ok && !a.accumulate_dq) {
+      const f32x4 z = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int c = 0; c < 32; ++c) *reinterpret_cast<f32x4*>(dq + c * 8 + hh * 4) = z;
+    }
+    return;
+  }
+
+  bf16x8 qreg[16], dreg[16];
+  {
+    const int64_t rh = (int64_t)tok * a.n_q_heads + head;
+    const __bf16* qrow = static_cast<const __bf16*>(a.q) + rh * kD + hh * 8;
+    const __bf16* drow = static_cast<const __bf16*>(a.d_out) + rh * kD + hh * 8;
+#pragma unroll
+    for (int ks = 0; ks < 16; ++ks) {
+      if (row_ok) {
+        qreg[ks] = *reinterpret_cast<const bf16x8*>(qrow + ks * 16);
+        dreg[ks] = *reinterpret_cast<const bf16x8*>(drow + ks * 16);
+      } else {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) qreg[ks][e] = dreg[ks][e] = (__bf16)0.f;
+      }
+    }
+  }
+  const int64_t stat = (int64_t)head * a.n_q + (row_ok ? tok : 0);
+  const float lse2 = row_ok ? a.lse2[stat] : INFINITY;
+  const float delta = row_ok ? a.delta[stat] : 0.f;
+
+  f32x16 acc[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) acc[i] = zero16();
+
+  DqRegs R;
+  dq_load(a, g, kb, k_hi, tid, R);
+  dq_store(smem, tid, R);
+  __syncthreads();
+
+  const int swz = l32 & 7;
+  const int tswz = (l32 >> 1) & 3;
+  for (int t = 0; t < n_tiles; ++t) {
+    const int64_t t0 = kb + (int64_t)t * kQBN;
+    if (t + 1 < n_tiles) dq_load(a, g, t0 + kQBN, k_hi, tid, R);
+    const char* Ks = smem + (t & 1) * kQStage;
+    const char* Vs = Ks + kTileBytes;
+    const char* Kt = Ks + 2 * kTileBytes;
+
+    f32x16 s = zero16(), dp = zero16();
+#pragma unroll
+    for (int ks = 0; ks < 16; ++ks) {
+      const int off = l32 * kRowBytes + (((2 * ks + hh) ^ swz) << 4);
+      const bf16x8 kv = *reinterpret_cast<const bf16x8*>(Ks + off);
+      const bf16x8 vv = *reinterpret_cast<const bf16x8*>(Vs + off);
+      s = mfma32(kv, qreg[ks], s);
+      dp = mfma32(vv, dreg[ks], dp);
+    }
+    const bool edge = t0 + kQBN > k_all;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      float p = __builtin_amdgcn_exp2f(fmaf(s[r], a.scale_log2, -lse2));
+      if (edge && t0 + acc_key(r, hh) >= my_lim) p = 0.f;
+      s[r] = p * (dp[r] - delta);          // dS
+    }
+    const bf16x8 ds0 = pack8(s, 0), ds1 = pack8(s, 1);
+#pragma unroll
+    for (int db = 0; db < 8; ++db) {
+      const char* row = Kt + (32 * db + l32) * (kQBN * 2);
+      const bf16x8 k0 = *reinterpret_cast<const bf16x8*>(row + (((0 + hh) ^ tswz) << 4));
+      const bf16x8 k1 = *reinterpret_cast<const bf16x8*>(row + (((2 + hh) ^ tswz) << 4));
+      acc[db] = mfma32(k0, ds0, acc[db]);
+      acc[db] = mfma32(k1, ds1, acc[db]);
+    }
+    if (t + 1 < n_tiles) dq_store(smem + ((t + 1) & 1) * kQStage, tid, R);
+    __syncthreads();
+  }
+
+  if (row_ok) {
+#pragma unroll
+    for (int db = 0; db < 8; ++db) {
+#pragma unroll
+      for (int q4 = 0; q4 < 4; ++q4) {
+        f32x4* dst = reinterpret_cast<f32x4*>(dq + 32 * db + 8 * q4 + 4 * hh);
+        f32x4 v;
+        v[0] = acc[db][4 * q4 + 0] * a.scale;
+        v[1] = acc[db][4 * q4 + 1] * a.scale;
+        v[2] = acc[db][4 * q4 + 2] * a.scale;
+        v[3] = acc[db][4 * q4 + 3] * a.scale;
+        if (a.accumulate_dq) v += *dst;
+        *dst = v;
+      }
+    }
+  }
+}
+
+// ============================================================== dk/dv kernel
+constexpr int kKB = 32;                       // response keys per wave
+constexpr int kRB = 32;                       // packed query rows per step
+constexpr int kKVBytes = kKB * kRowBytes;     // 16 KiB each for K, V
+constexpr int kRowTileBytes = kRB * kRowBytes;
+
+__global__ __launch_bounds__(64, 1) void bwd_dkdv_bf16_d256_kernel(BwdArgs a, int64_t key0,
+                                                                   int64_t key_end) {
+  __shared__ __attribute__((aligned(16))) char smem[2 * kKVBytes + 4 * kRowTileBytes];
+  char* Ks = smem;                              // [32 keys][256] row-major, chunk ^ (key & 7)
+  char* Vs = smem + kKVBytes;
+  char* Qs = smem + 2 * kKVBytes;               // [32 rows][256] row-major, chunk ^ (row & 7)
+  char* Ds = Qs + kRowTileBytes;                // dO, same layout
+  char* Qt = Ds + kRowTileBytes;                // [256 d][32 row slots], chunk ^ ((d >> 1) & 3)
+  char* Dt = Qt + kRowTileBytes;                // dO^T, same layout
+
+  const int lane = threadIdx.x, l32 = lane & 31, hh = lane >> 5;
+  const int g = blockIdx.y;
+  const int lg = a.log2_group;
+  const int rows_total = a.n_q << lg;
+  const int64_t j0 = key0 + (int64_t)blockIdx.x * kKB;
+  const int64_t j_mine = j0 + l32;
+  const u32x4 zero = {0u, 0u, 0u, 0u};
+
+  // stage the 32 keys' K and V rows (row-major, swizzled)
+  {
+    const __bf16* kp = static_cast<const __bf16*>(a.k_pool) + (int64_t)g * kD;
+    const __bf16* vp = static_cast<const __bf16*>(a.v_pool) + (int64_t)g * kD;
+    const int c = lane & 31;
+    for (int key = hh; key < kKB; key += 2) {
+      const int64_t j = j0 + key;
+      u32x4 kv = zero, vv = zero;
+      if (j < key_end) {
+        const int64_t pr = phys_pos(a.page_table, j, a.log2_page);
+        kv = *reinterpret_cast<const u32x4*>(kp + pr * a.k_pos_stride + c * 8);
+        vv = *reinterpret_cast<const u32x4*>(vp + pr * a.v_pos_stride + c * 8);
+      }
+      const int off = key * kRowBytes + ((c ^ (key & 7)) << 4);
+      *reinterpret_cast<u32x4*>(Ks + off) = kv;
+      *reinterpret_cast<u32x4*>(Vs + off) = vv;
+    }
+  }
+
+  f32x16 dk[8], dv[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) dk[i] = dv[i] = zero16();
+
+  // rows (token, head) with token >= j0 - q_pos0 can see some key of the block
+  int64_t first_tok = j0 - a.q_pos0;
+  if (first_tok < 0) first_tok = 0;
+  const int row_begin = (int)((first_tok << lg) / kRB * kRB);
+  const int swz = l32 & 7;
+  const int tswz = (l32 >> 1) & 3;
+
+  for (int rb0 = row_begin; rb0 < rows_total; rb0 += kRB) {
+    __syncthreads();   // previous step's reads of Qs/Ds/Qt/Dt are done
+    // stage Q and dO rows: item (row quad m, chunk c): 8 quads x 32 chunks, 4 per lane
+#pragma unroll
+    for (int it = 0; it < 4; ++it) {
+      const int item = lane + 64 * it;
+      const int m = item & 7, c = item >> 3;
+      u32x4 qv[4], dvv[4];
+#pragma unroll
+      for (int kk = 0; kk < 4; ++kk) {
+        const int prow = rb0 + 4 * m + kk;
+        if (prow < rows_total) {
+          const int tok = prow >> lg;
+          const int head = (g << lg) + (prow & ((1 << lg) - 1));
+          const int64_t rh = (int64_t)tok * a.n_q_heads + head;
+          qv[kk] = *reinterpret_cast<const u32x4*>(static_cast<const __bf16*>(a.q) + rh * kD + c * 8);
+          dvv[kk] = *reinterpret_cast<const u32x4*>(static_cast<const __bf16*>(a.d_out) + rh * kD + c * 8);
+        } else {
+          qv[kk] = zero;
+          dvv[kk] = zero;
+        }
+        const int row = 4 * m + kk;
+        const int off = row * kRowBytes + ((c ^ (row & 7)) << 4);
+        *reinterpret_cast<u32x4*>(Qs + off) = qv[kk];
+        *reinterpret_cast<u32x4*>(Ds + off) = dvv[kk];
+      }
+      const int slot = swap23(4 * m);
+      const int sc = slot >> 3, sb = (slot & 7) * 2;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const int d = 8 * c + e;
+        const int dw = e >> 1;
+        const int off = d * (kRB * 2) + ((sc ^ ((d >> 1) & 3)) << 4) + sb;
+        *reinterpret_cast<u32x2*>(Qt + off) = pick4(qv[0][dw], qv[1][dw], qv[2][dw], qv[3][dw], (e & 1) != 0);
+        *reinterpret_cast<u32x2*>(Dt + off) = pick4(dvv[0][dw], dvv[1][dw], dvv[2][dw], dvv[3][dw], (e & 1) != 0);
+      }
+    }
+    __syncthreads();
+
+    // S[row][key] = Q K^T and dP[row][key] = dO V^T (lane = key, registers = rows)
+    f32x16 s = zero16(), dp = zero16();
+#pragma unroll
+    for (int ks = 0; ks < 16; ++ks) {
+      const int off = l32 * kRowBytes + (((2 * ks + hh) ^ swz) << 4);
+      const bf16x8 qa = *reinterpret_cast<const bf16x8*>(Qs + off);
+      const bf16x8 da = *reinterpret_cast<const bf16x8*>(Ds + off);
+      const bf16x8 kbv = *reinterpret_cast<const bf16x8*>(Ks + off);
+      const bf16x8 vbv = *reinterpret_cast<const bf16x8*>(Vs + off);
+      s = mfma32(qa, kbv, s);
+      dp = mfma32(da, vbv, dp);
+    }
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int prow = rb0 + acc_key(r, hh);   // register r holds packed row acc_key(r, h)
+      float p = 0.f, dsv = 0.f;
+      if (prow < rows_total) {
+        const int tok = prow >> lg;
+        const int head = (g << lg) + (prow & ((1 << lg) - 1));
+        if (a.q_pos0 + tok >= j_mine) {
+          const int64_t o = (int64_t)head * a.n_q + tok;
+          p = __builtin_amdgcn_exp2f(fmaf(s[r], a.scale_log2, -a.lse2[o]));
+          dsv = p * (dp[r] - a.delta[o]);
+        }
+      }
+      s[r] = p;
+      dp[r] = dsv;
+    }
+    const bf16x8 p0 = pack8(s, 0), p1 = pack8(s, 1);
+    const bf16x8 d0 = pack8(dp, 0), d1 = pack8(dp, 1);
+#pragma unroll
+    for (int db = 0; db < 8; ++db) {
+      const int rowoff = (32 * db + l32) * (kRB * 2);
+      const bf16x8 t0 = *reinterpret_cast<const bf16x8*>(Dt + rowoff + (((0 + hh) ^ tswz) << 4));
+      const bf16x8 t1 = *reinterpret_cast<const bf16x8*>(Dt + rowoff + (((2 + hh) ^ tswz) << 4));
+      dv[db] = mfma32(t0, p0, dv[db]);
+      dv[db] = mfma32(t1, p1, dv[db]);
+      const bf16x8 u0 = *reinterpret_cast<const bf16x8*>(Qt + rowoff + (((0 + hh) ^ tswz) << 4));
+      const bf16x8 u1 = *reinterpret_cast<const bf16x8*>(Qt + rowoff + (((2 + hh) ^ tswz) << 4));
+      dk[db] = mfma32(u0, d0, dk[db]);
+      dk[db] = mfma32(u1, d1, dk[db]);
+    }
+  }
+
+  if (j_mine < key_end) {
+    const int64_t r = (j_mine - a.prefix_len) * a.n_kv_heads + g;
+    float* dkr = a.dk_resp + r * kD;
+    float* dvr = a.dv_resp + r * kD;
+#pragma unroll
+    for (int db = 0; db < 8; ++db) {
+#pragma unroll
+      for (int q4 = 0; q4 < 4; ++q4) {
+        const int d0 = 32 * db + 8 * q4 + 4 * hh;
+        f32x4 kv, vv;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          kv[e] = dk[db][4 * q4 + e] * a.scale;
+          vv[e] = dv[db][4 * q4 + e];
+        }
+        if (a.accumulate_dkv) {
+          kv += *reinterpret_cast<const f32x4*>(dkr + d0);
+          vv += *reinterpret_cast<const f32x4*>(dvr + d0);
+        }
+        *reinterpret_cast<f32x4*>(dkr + d0) = kv;
+        *reinterpret_cast<f32x4*>(dvr + d0) = vv;
+      }
+    }
+  }
+}
+
+}  // namespace
+
+hipError_t launch_bwd_bf16_d256(const BwdArgs& a, bool need_dq, bool need_dkv,
+                                hipStream_t stream) {
+  if (need_dq) {
+    const unsigned row_tiles = (unsigned)(((int64_t)a.n_q * a.group + kQBM - 1) / kQBM);
+    hipLaunchKernelGGL(bwd_dq_bf16_d256_kernel, dim3(row_tiles, a.n_kv_heads), dim3(256), 0,
+                       stream, a);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  if (need_dkv) {
+    const int64_t key0 = a.kv_begin > a.prefix_len ? a.kv_begin : a.prefix_len;
+    const int64_t n_keys = a.kv_end - key0;
+    if (n_keys > 0) {
+      const unsigned blocks = (unsigned)((n_keys + kKB - 1) / kKB);
+      hipLaunchKernelGGL(bwd_dkdv_bf16_d256_kernel, dim3(blocks, a.n_kv_heads), dim3(64), 0,
+                         stream, a, key0, a.kv_end);
+      return hipGetLastError();
+    }
+  }
+  return hipSuccess;
+}
+
+}  // namespace ls

@@ -1,0 +1,75 @@
+// Internal declarations shared by the host entry points and the kernels of
+// the response-replay attention library.  Not part of the public ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace ls {
+
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kLn2 = 0.6931471805599453f;
+constexpr int kMaxSplitsPerLaunch = 64;
+
+// Everything a forward-split kernel needs; passed by value as a kernel argument.
+struct FwdArgs {
+  const void* q;
+  const void* k_pool;
+  const void* v_pool;
+  const int32_t* page_table;
+  float* out_part;          // [n_splits, n_q, Hq, Dv]
+  float* lse_part;          // [n_splits, Hq, n_q]
+  int64_t q_pos0;
+  int64_t k_pos_stride;     // elements between positions in a K page (Hkv * D)
+  int64_t v_pos_stride;     // elements between positions in a V page (Hkv * Dv)
+  int32_t n_q, n_q_heads, n_kv_heads, group, log2_group;
+  int32_t head_dim, head_dim_v;
+  int32_t log2_page;
+  float scale_log2;         // softmax_scale * log2(e)
+  int32_t n_splits;
+  int64_t split_begin[kMaxSplitsPerLaunch];
+  int64_t split_end[kMaxSplitsPerLaunch];
+};
+
+// Backward over one key range [kv_begin, kv_end).
+struct BwdArgs {
+  const void* q;
+  const void* k_pool;
+  const void* v_pool;
+  const int32_t* page_table;
+  const void* d_out;
+  const float* delta;       // [Hq, n_q]  d_out . out
+  const float* lse2;        // [Hq, n_q]  lse * log2(e); +inf for rows with no key
+  float* dq;                // [n_q, Hq, D]
+  float* dk_resp;           // [kv_len - prefix_len, Hkv, D]
+  float* dv_resp;           // [kv_len - prefix_len, Hkv, Dv]
+  int64_t q_pos0;
+  int64_t prefix_len;
+  int64_t kv_begin, kv_end;
+  int64_t k_pos_stride, v_pos_stride;
+  int32_t n_q, n_q_heads, n_kv_heads, group, log2_group;
+  int32_t head_dim, head_dim_v;
+  int32_t log2_page;
+  float scale;              // softmax_scale
+  float scale_log2;         // softmax_scale * log2(e)
+  int32_t accumulate_dq, accumulate_dkv;
+};
+
+// Launchers (return the hipError_t of the launch).
+hipError_t launch_gather(const void* k_pool, const void* v_pool, const int32_t* page_table,
+                         int64_t pos_begin, int64_t pos_end, int log2_page, int64_t k_row_elems,
+                         int64_t v_row_elems, int esize, void* k_out, void* v_out,
+                         hipStream_t stream);
+hipError_t launch_merge(const float* out_part, const float* lse_part, int n_splits, int n_q,
+                        int n_heads, int dv, bool out_bf16, void* out, float* lse,
+                        hipStream_t stream);
+hipError_t launch_fwd_f32(const FwdArgs& a, hipStream_t stream);
+hipError_t launch_fwd_bf16_d256(const FwdArgs& a, hipStream_t stream);
+hipError_t launch_bwd_prep(const void* d_out, const void* out, bool dout_bf16, bool out_bf16,
+                           const float* lse, int n_q, int n_heads, int dv, float* delta,
+                           float* lse2, hipStream_t stream);
+hipError_t launch_bwd_f32(const BwdArgs& a, bool need_dq, bool need_dkv, hipStream_t stream);
+hipError_t launch_bwd_bf16_d256(const BwdArgs& a, bool need_dq, bool need_dkv,
+                                hipStream_t stream);
+
+}  // namespace ls

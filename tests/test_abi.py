@@ -1,0 +1,157 @@
+"""C ABI of liblongstraw.so on the CPU: the library loads, exports every symbol
+the header declares, and rejects bad arguments on the host before any launch."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2607_14952_amd import binding as B
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "longstraw.h")
+
+pytestmark = pytest.mark.skipif(not os.path.exists(B.LIB_PATH),
+                                reason="liblongstraw.so not built (run __graft_entry__.build())")
+
+
+def declared_symbols():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(ls_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_header_declares_the_binding_exports():
+    assert declared_symbols() == sorted(B.EXPORTS)
+
+
+def test_library_exports_every_declared_symbol():
+    lib = ctypes.CDLL(B.LIB_PATH)
+    for name in declared_symbols():
+        assert hasattr(lib, name), name
+
+
+def test_only_ls_symbols_are_exported():
+    import subprocess
+    out = subprocess.run(["nm", "-D", "--defined-only", B.LIB_PATH], capture_output=True,
+                         text=True).stdout
+    funcs = [l.split()[-1] for l in out.splitlines() if " T " in l]
+    assert sorted(f for f in funcs if f.startswith("ls_")) == declared_symbols()
+    assert all(f.startswith("ls_") or f.startswith("_") for f in funcs), funcs
+
+
+def test_version_and_status_strings():
+    lib = B.load_library()
+    assert lib.ls_abi_version() == B.ABI_VERSION
+    for code, name in B.STATUS.items():
+        assert lib.ls_status_string(code).decode() == name
+
+
+FAKE = 1 << 20   # 16-byte aligned addresses that are never dereferenced
+
+
+def good_params(**kw):
+    p = B.AttnParams()
+    p.abi_version = B.ABI_VERSION
+    p.dtype = B.LS_BF16
+    p.n_q, p.n_q_heads, p.n_kv_heads = 64, 16, 2
+    p.head_dim = p.head_dim_v = 256
+    p.page_size = 256
+    p.n_phys_pages = p.n_logical_pages = 64
+    p.prefix_len = p.q_pos0 = 4096
+    p.softmax_scale = 1 / 16
+    p.flags = 0
+    p.q = FAKE
+    p.k_pool = FAKE * 64
+    p.v_pool = FAKE * 128
+    p.page_table = FAKE * 192
+    p.pool_epoch = p.expected_epoch = 3
+    for k, v in kw.items():
+        setattr(p, k, v)
+    return p
+
+
+def fwd(p, splits=((0, 4096), (4096, 4160)), out=FAKE * 256, lse=FAKE * 320):
+    lib = B.load_library()
+    arr = (B.Split * len(splits))(*[B.Split(b, e) for b, e in splits])
+    return lib.ls_prefix_attn_fwd(ctypes.byref(p), arr, len(splits), out, lse, None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(abi_version=99), -1),
+    (dict(dtype=7), -2),
+    (dict(n_q_heads=15), -1),
+    (dict(head_dim=128, head_dim_v=128), -2),
+    (dict(page_size=96), -2),
+    (dict(page_size=0), -1),
+    (dict(q_pos0=100), -1),                      # q_pos0 < prefix_len
+    (dict(n_logical_pages=16), -1),              # kv_len beyond the logical store
+    (dict(q=FAKE + 8), -1),                      # misaligned
+    (dict(k_pool=0), -1),
+    (dict(softmax_scale=-1.0), -1),
+    (dict(expected_epoch=2), -5),                # stale pool
+    (dict(n_q_heads=16 * 3, n_kv_heads=1), -2),  # bf16 group 48 does not divide 32
+])
+def test_forward_rejects(kw, status):
+    assert fwd(good_params(**kw)) == status
+    assert B.load_library().ls_last_error()
+
+
+@pytest.mark.parametrize("splits", [
+    ((0, 4096), (4000, 4160)),      # overlapping
+    ((4096, 4160), (0, 4096)),      # unsorted
+    ((0, 0),),                      # empty
+    ((0, 5000),),                   # beyond kv_len
+    ((-4, 10),),
+])
+def test_forward_rejects_bad_splits(splits):
+    assert fwd(good_params(), splits) == -1
+
+
+def test_forward_rejects_aliased_outputs():
+    assert fwd(good_params(), out=FAKE) == -4               # out_part over q
+    assert fwd(good_params(), out=FAKE * 256, lse=FAKE * 256) == -4
+
+
+def test_merge_rejects():
+    lib = B.load_library()
+    args = (FAKE, FAKE * 64, 4, 16, 16, 256, B.LS_BF16, FAKE * 128, FAKE * 192, 0, None)
+    assert lib.ls_lse_merge(*args[:6], 5, *args[7:]) == -2                      # out dtype
+    assert lib.ls_lse_merge(*args[:5], 254, *args[6:]) == -2                    # dv % 4
+    assert lib.ls_lse_merge(*args[:9], 2, None) == -2                           # flags
+    assert lib.ls_lse_merge(FAKE, FAKE * 64, 4, 16, 16, 256, B.LS_BF16, FAKE + 64,
+                            FAKE * 192, 0, None) == -4                          # out inside part
+    assert lib.ls_lse_merge(FAKE, FAKE * 64, 0, 16, 16, 256, B.LS_BF16, FAKE * 128,
+                            FAKE * 192, 0, None) == -1
+
+
+def test_backward_rejects():
+    lib = B.load_library()
+    p = good_params()
+    need = lib.ls_prefix_attn_bwd_workspace_size(ctypes.byref(p))
+    assert need >= 2 * 64 * 16 * 4
+    base = dict(d_out=FAKE * 400, out=FAKE * 420, lse=FAKE * 440, dq=FAKE * 460,
+                dk=FAKE * 480, dv=FAKE * 500, ws=FAKE * 520)
+
+    def call(p=p, kb=0, ke=4160, out_dtype=B.LS_BF16, ws_bytes=need, **kw):
+        a = dict(base, **kw)
+        return lib.ls_prefix_attn_bwd(ctypes.byref(p), kb, ke, a["d_out"], a["out"], out_dtype,
+                                      a["lse"], a["dq"], a["dk"], a["dv"], a["ws"], ws_bytes, None)
+
+    assert call(ws_bytes=need - 4) == -3
+    assert call(ws=None) == -3
+    assert call(dk=None) == -1                    # range holds response keys
+    assert call(ke=5000) == -1
+    assert call(kb=10, ke=5) == -1
+    assert call(out_dtype=9) == -2
+    assert call(dq=FAKE * 420) == -4              # dq over out
+    assert call(p=good_params(expected_epoch=9)) == -5
+
+
+def test_gather_rejects():
+    lib = B.load_library()
+    p = good_params(n_q=0)
+    assert lib.ls_gather_kv(ctypes.byref(p), 10, 5, FAKE * 300, FAKE * 400, None) == -1
+    assert lib.ls_gather_kv(ctypes.byref(p), 0, 64 * 256 + 1, FAKE * 300, FAKE * 400, None) == -1
+    assert lib.ls_gather_kv(ctypes.byref(p), 0, 16, FAKE * 64, FAKE * 400, None) == -4
+    assert lib.ls_gather_kv(ctypes.byref(p), 0, 0, FAKE * 300, FAKE * 400, None) == 0

@@ -1,0 +1,301 @@
+"""HIP path vs the fp64 oracle on identical seeded inputs (needs an MI355X).
+
+Every call goes through the C ABI (ctypes binding); the oracle never sees a
+value the GPU produced.  Bars: bit-exact for the page gather; bf16 inputs:
+out rel-L2 <= 5e-3, lse max-abs <= 1e-3, dq/dk/dv rel-L2 <= 1e-2; fp32 inputs:
+rel-L2 <= 1e-5 and lse max-abs <= 1e-5.
+"""
+from __future__ import annotations
+
+import numpy as np
+import pytest
+
+import oracle as O
+from paper_2607_14952_amd import binding as B
+from paper_2607_14952_amd import configs, inputs
+from paper_2607_14952_amd.replay import ReplayStep, device_inputs
+from tests._gpu import announce, host, lse_err, oracle_bkw, oracle_kw, rel_l2, tol
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu_ready():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    B.load_library()
+
+
+def _kv(dev, epoch=0):
+    return B.PagedKV(dev["k_pool"], dev["v_pool"], dev["page_table"], epoch)
+
+
+def check_forward(cfg, h, dev, splits, *, P, q_pos0):
+    """Per-split (o_r, l_r) and the merged (o, l) against the oracle."""
+    t = tol(cfg)
+    kv = _kv(dev)
+    announce(f"fwd {cfg.name} R={h['q'].shape[0]} splits={len(splits)} q_pos0={q_pos0}")
+    o_part, l_part = B.prefix_attn_fwd(dev["q"], kv, splits, prefix_len=P, q_pos0=q_pos0,
+                                       scale=cfg.scale)
+    out, lse = B.lse_merge(o_part, l_part, out_dtype=dev["q"].dtype)
+    import torch
+    torch.cuda.synchronize()
+    kw = dict(page_size=cfg.page_size, q_pos0=q_pos0, scale=cfg.scale)
+    for s, (b, e) in enumerate(splits):
+        o_ref, l_ref = O.attn_fwd(h["q"], h["k_pool"], h["v_pool"], h["page_table"],
+                                  kv_begin=b, kv_end=e, **kw)
+        assert rel_l2(host(o_part[s]), o_ref) <= t["out"], f"split {s} out"
+        assert lse_err(host(l_part[s]), l_ref) <= t["lse"], f"split {s} lse"
+    o_ref, l_ref = O.attn_fwd(h["q"], h["k_pool"], h["v_pool"], h["page_table"], **kw)
+    err_o, err_l = rel_l2(host(out), o_ref), lse_err(host(lse), l_ref)
+    assert err_o <= t["out"], f"merged out rel-L2 {err_o:.2e}"
+    assert err_l <= t["lse"], f"merged lse max-abs {err_l:.2e}"
+    return out, lse, o_ref, l_ref
+
+
+def check_backward(cfg, h, dev, out, lse, o_ref, l_ref, ranges, *, P, q_pos0):
+    t = tol(cfg)
+    kv = _kv(dev)
+    dq = dk = dv = None
+    announce(f"bwd {cfg.name} ranges={len(ranges)}")
+    for r, (b, e) in enumerate(ranges):
+        dq, dk, dv = B.prefix_attn_bwd(dev["q"], kv, dev["d_out"], out, lse, prefix_len=P,
+                                       q_pos0=q_pos0, scale=cfg.scale, kv_begin=b, kv_end=e,
+                                       flags=B.FLAG_ACCUMULATE_DQ if r else 0, dq=dq, dk_resp=dk,
+                                       dv_resp=dv)
+    import torch
+    torch.cuda.synchronize()
+    dq_ref, dk_ref, dv_ref = O.attn_bwd(h["q"], h["k_pool"], h["v_pool"], h["page_table"],
+                                        h["d_out"], page_size=cfg.page_size, prefix_len=P,
+                                        q_pos0=q_pos0, scale=cfg.scale, out=o_ref, lse=l_ref)
+    e_q, e_k, e_v = rel_l2(host(dq), dq_ref), rel_l2(host(dk), dk_ref), rel_l2(host(dv), dv_ref)
+    assert e_q <= t["grad"], f"dq rel-L2 {e_q:.2e}"
+    assert e_k <= t["grad"], f"dk rel-L2 {e_k:.2e}"
+    assert e_v <= t["grad"], f"dv rel-L2 {e_v:.2e}"
+    return dq, dk, dv
+
+
+def full_case(cfg, *, backward=True):
+    h = inputs.dense_inputs(cfg)
+    dev = device_inputs(h)
+    out, lse, o_ref, l_ref = check_forward(cfg, h, dev, cfg.splits(), P=cfg.prefix_len,
+                                           q_pos0=cfg.q_pos0)
+    if backward:
+        check_backward(cfg, h, dev, out, lse, o_ref, l_ref, cfg.shard_ranges(),
+                       P=cfg.prefix_len, q_pos0=cfg.q_pos0)
+
+
+# ------------------------------------------------------------------ page gather
+@pytest.mark.parametrize("cfg", [
+    configs.C1,
+    configs.C3.scaled(name="gather_bf16_perm", prefix_len=65536, resp_len=64),
+    configs.C3.scaled(name="gather_bf16_p16", page_size=16, prefix_len=4096, resp_len=64),
+], ids=lambda c: c.name)
+def test_gather_bit_exact(cfg):
+    h = inputs.dense_inputs(cfg, with_dout=False)
+    dev = device_inputs(h)
+    for b, e in ((0, cfg.kv_len), (37, 1111), (cfg.kv_len - 5, cfg.kv_len)):
+        announce(f"gather {cfg.name} [{b},{e})")
+        k, v = B.gather_kv(_kv(dev), b, e)
+        kr = O.gather(h["k_pool"], h["page_table"], cfg.page_size, np.arange(b, e))
+        vr = O.gather(h["v_pool"], h["page_table"], cfg.page_size, np.arange(b, e))
+        import torch
+        as_bits = (lambda t: t.view(torch.int16).cpu().numpy().view(np.uint16)) \
+            if cfg.dtype == "bf16" else (lambda t: t.cpu().numpy())
+        assert np.array_equal(as_bits(k), kr) and np.array_equal(as_bits(v), vr)
+
+
+# ------------------------------------------------------------------ full parity
+def test_c1_tiny_f32():
+    full_case(configs.C1)
+
+
+BF16_SMALL = configs.C3.scaled(name="bf16_small", prefix_len=8192, resp_len=300, n_shards=2,
+                               splits_per_shard=2, plant_frac=0.01)
+
+
+def test_bf16_small_planted():
+    full_case(BF16_SMALL)
+
+
+def test_bf16_page16_unaligned_splits():
+    cfg = BF16_SMALL.scaled(name="bf16_p16", page_size=16, prefix_len=3000, resp_len=77,
+                            plant_frac=0.0)
+    h = inputs.dense_inputs(cfg)
+    dev = device_inputs(h)
+    P = cfg.prefix_len
+    splits = [(0, 1000), (1000, 1003), (1003, 2999), (2999, P), (P, P + 40), (P + 40, P + 77)]
+    out, lse, o_ref, l_ref = check_forward(cfg, h, dev, splits, P=P, q_pos0=P)
+    check_backward(cfg, h, dev, out, lse, o_ref, l_ref, [(0, 1234), (1234, P + 50), (P + 50, P + 77)],
+                   P=P, q_pos0=P)
+
+
+@pytest.mark.parametrize("G,Hkv", [(1, 2), (2, 3), (4, 1), (16, 1), (32, 1)])
+def test_bf16_gqa_groups(G, Hkv):
+    cfg = BF16_SMALL.scaled(name=f"bf16_g{G}", n_q_heads=G * Hkv, n_kv_heads=Hkv,
+                            prefix_len=2048, resp_len=45, plant_frac=0.0, n_shards=1,
+                            splits_per_shard=2)
+    full_case(cfg)
+
+
+def test_bf16_single_row_and_response_only():
+    cfg = BF16_SMALL.scaled(name="bf16_r1", prefix_len=512, resp_len=1, plant_frac=0.0,
+                            n_shards=1, splits_per_shard=1)
+    full_case(cfg)
+    cfg = BF16_SMALL.scaled(name="bf16_noprefix", prefix_len=0, resp_len=200, plant_frac=0.0,
+                            n_shards=1, splits_per_shard=1)
+    h = inputs.dense_inputs(cfg)
+    dev = device_inputs(h)
+    out, lse, o_ref, l_ref = check_forward(cfg, h, dev, [(0, 200)], P=0, q_pos0=0)
+    check_backward(cfg, h, dev, out, lse, o_ref, l_ref, [(0, 200)], P=0, q_pos0=0)
+
+
+def test_bf16_empty_rows_in_split():
+    """A split inside the response: rows before it see nothing (lse -inf, o 0)."""
+    cfg = BF16_SMALL.scaled(name="bf16_empty", prefix_len=1024, resp_len=160, plant_frac=0.0)
+    h = inputs.dense_inputs(cfg)
+    dev = device_inputs(h)
+    P = cfg.prefix_len
+    announce("fwd empty-row split")
+    o_part, l_part = B.prefix_attn_fwd(dev["q"], _kv(dev), [(P + 100, P + 130)], prefix_len=P,
+                                       q_pos0=P, scale=cfg.scale)
+    o_ref, l_ref = O.attn_fwd(h["q"], h["k_pool"], h["v_pool"], h["page_table"],
+                              kv_begin=P + 100, kv_end=P + 130, **oracle_kw(cfg))
+    lp = host(l_part[0])
+    assert np.all(np.isneginf(lp[:, :100])) and np.all(host(o_part[0])[:100] == 0)
+    assert rel_l2(host(o_part[0]), o_ref) <= 5e-3 and lse_err(lp, l_ref) <= 1e-3
+
+
+def test_bf16_blockwise_q_pos0():
+    """Rows start after earlier response keys (a later response block): those keys are
+    visible to every row and get dK/dV; accumulating over blocks in reverse equals one
+    call over all rows."""
+    P, blk, nb = 2048, 96, 3
+    cfg = BF16_SMALL.scaled(name="bf16_blocks", prefix_len=P, resp_len=blk * nb, plant_frac=0.0)
+    h = inputs.dense_inputs(cfg)
+    dev = device_inputs(h)
+    import torch
+    kv = _kv(dev)
+    dk = torch.zeros((blk * nb, cfg.n_kv_heads, 256), dtype=torch.float32, device="cuda")
+    dv = torch.zeros_like(dk)
+    dq_all = np.zeros((blk * nb, cfg.n_q_heads, 256))
+    for b in reversed(range(nb)):
+        q0 = P + blk * b
+        rows = slice(blk * b, blk * (b + 1))
+        q = dev["q"][rows].contiguous()
+        d_out = dev["d_out"][rows].contiguous()
+        splits = [(0, P), (P, q0 + blk)] if b else [(0, P), (P, P + blk)]
+        announce(f"block {b} fwd")
+        o_part, l_part = B.prefix_attn_fwd(q, kv, splits, prefix_len=P, q_pos0=q0, scale=cfg.scale)
+        out, lse = B.lse_merge(o_part, l_part, out_dtype=torch.bfloat16)
+        announce(f"block {b} bwd")
+        dq, _, _ = B.prefix_attn_bwd(q, kv, d_out, out, lse, prefix_len=P, q_pos0=q0,
+                                     scale=cfg.scale, flags=B.FLAG_ACCUMULATE_DKV,
+                                     dk_resp=dk[: q0 + blk - P], dv_resp=dv[: q0 + blk - P])
+        torch.cuda.synchronize()
+        dq_all[rows] = host(dq)
+    dq_ref, dk_ref, dv_ref = O.attn_bwd(h["q"], h["k_pool"], h["v_pool"], h["page_table"],
+                                        h["d_out"], **oracle_bkw(cfg))
+    assert rel_l2(dq_all, dq_ref) <= 1e-2
+    assert rel_l2(host(dk), dk_ref) <= 1e-2
+    assert rel_l2(host(dv), dv_ref) <= 1e-2
+
+
+# ------------------------------------------------------------------ invariants
+def test_determinism_layout_and_causality():
+    cfg = BF16_SMALL.scaled(name="bf16_inv", prefix_len=4096, resp_len=130)
+    h = inputs.dense_inputs(cfg)
+    dev = device_inputs(h)
+    import torch
+
+    def run(d):
+        step = ReplayStep(cfg, d)
+        step.step()
+        torch.cuda.synchronize()
+        return [x.clone() for x in (step.out, step.lse, step.dq, step.dk, step.dv)]
+
+    announce("determinism")
+    a, b = run(dev), run(dev)
+    for x, y in zip(a, b):
+        assert torch.equal(x, y), "two runs differ"
+    # the same logical store under another physical layout gives identical bits
+    perm = np.random.default_rng(0).permutation(h["k_pool"].shape[0])
+    inv = np.argsort(perm)
+    h2 = dict(h, k_pool=h["k_pool"][perm], v_pool=h["v_pool"][perm],
+              page_table=inv[h["page_table"]].astype(np.int32))
+    announce("layout invariance")
+    c = run(device_inputs(h2))
+    for x, y in zip(a, c):
+        assert torch.equal(x, y), "physical layout changed the result"
+    # changing response token k's K/V leaves rows < k bitwise unchanged
+    k = 70
+    h3 = dict(h, k_pool=h["k_pool"].copy(), v_pool=h["v_pool"].copy())
+    j = cfg.prefix_len + k
+    page, slot = h["page_table"][j // cfg.page_size], j % cfg.page_size
+    h3["k_pool"][page, slot] ^= np.uint16(0x0100)
+    h3["v_pool"][page, slot] ^= np.uint16(0x0100)
+    announce("causality")
+    d = run(device_inputs(h3))
+    assert torch.equal(a[0][:k], d[0][:k]) and torch.equal(a[1][:, :k], d[1][:, :k])
+    assert not torch.equal(a[0][k:], d[0][k:])
+
+
+def test_checked_mode_rejects_bad_page():
+    cfg = BF16_SMALL.scaled(name="bf16_oob", prefix_len=1024, resp_len=32, plant_frac=0.0)
+    h = inputs.dense_inputs(cfg)
+    h["page_table"] = h["page_table"].copy()
+    h["page_table"][2] = cfg.n_phys_pages + 5
+    dev = device_inputs(h)
+    announce("checked mode")
+    with pytest.raises(B.LongStrawError) as ei:
+        B.prefix_attn_fwd(dev["q"], _kv(dev), [(0, cfg.kv_len)], prefix_len=cfg.prefix_len,
+                          q_pos0=cfg.q_pos0, scale=cfg.scale, flags=B.FLAG_CHECKED)
+    assert ei.value.name == "LS_ERR_PAGE_OOB"
+    with pytest.raises(B.LongStrawError) as ei:
+        B.prefix_attn_fwd(dev["q"], _kv(dev, epoch=1), [(0, cfg.kv_len)], prefix_len=cfg.prefix_len,
+                          q_pos0=cfg.q_pos0, scale=cfg.scale, expected_epoch=0)
+    assert ei.value.name == "LS_ERR_STALE"
+
+
+# ------------------------------------------------------------------ full-size, sampled
+def _sampled_parity(cfg, rows, backward):
+    h = inputs.dense_inputs(cfg, with_dout=backward)
+    if cfg.plant_frac:
+        rows = sorted(set(rows) | set(int(r) for r in h["planted"][1][:2]))
+    dev = device_inputs(h)
+    announce(f"{cfg.name} full step")
+    step = ReplayStep(cfg, dev, backward=backward)
+    step.step()
+    import torch
+    torch.cuda.synchronize()
+    rows = np.array(rows)
+    o_ref, l_ref = O.attn_fwd(h["q"], h["k_pool"], h["v_pool"], h["page_table"], rows=rows,
+                              **oracle_kw(cfg))
+    assert rel_l2(host(step.out)[rows], o_ref) <= 5e-3
+    assert lse_err(host(step.lse)[:, rows], l_ref) <= 1e-3
+    if backward:
+        R = cfg.resp_len
+        keys = np.array([cfg.kv_len - 2, cfg.kv_len - 1])
+        need = np.union1d(rows, [R - 2, R - 1])
+        o_full = np.zeros((R, cfg.n_q_heads, cfg.head_dim_v))
+        l_full = np.zeros((cfg.n_q_heads, R))
+        o_n, l_n = O.attn_fwd(h["q"], h["k_pool"], h["v_pool"], h["page_table"], rows=need,
+                              **oracle_kw(cfg))
+        o_full[need], l_full[:, need] = o_n, l_n
+        dq_ref, dk_ref, dv_ref = O.attn_bwd(h["q"], h["k_pool"], h["v_pool"], h["page_table"],
+                                            h["d_out"], rows=rows, resp_keys=keys, out=o_full,
+                                            lse=l_full, **oracle_bkw(cfg))
+        assert rel_l2(host(step.dq)[rows], dq_ref) <= 1e-2
+        assert rel_l2(host(step.dk)[keys - cfg.prefix_len], dk_ref) <= 1e-2
+        assert rel_l2(host(step.dv)[keys - cfg.prefix_len], dv_ref) <= 1e-2
+
+
+@pytest.mark.timeout(900)
+def test_c2_full_size_sampled():
+    _sampled_parity(configs.C2, [0, 1, 1000, 2047, 4095], backward=False)
+
+
+@pytest.mark.timeout(900)
+def test_c3_full_size_sampled():
+    _sampled_parity(configs.C3, [0, 2048, 4095], backward=True)
