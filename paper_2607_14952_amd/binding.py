@@ -10,7 +10,8 @@ import ctypes
 import os
 from ctypes import POINTER, c_float, c_int32, c_int64, c_size_t, c_uint32, c_uint64, c_void_p
 
-LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "liblongstraw.so")
+LIB_PATH = os.environ.get("LONGSTRAW_LIB") or os.path.join(
+    os.path.dirname(os.path.abspath(__file__)), "liblongstraw.so")
 
 ABI_VERSION = 1
 LS_BF16, LS_F32 = 0, 1

@@ -16,6 +16,10 @@ CSRC = os.path.join(PKG, "csrc")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "liblongstraw.so")
 SOURCES = ["api.hip", "small_kernels.hip", "f32_generic.hip", "fwd_bf16.hip", "bwd_bf16.hip"]
+# Per-source extra flags.  The MFMA kernels keep their accumulators in arch VGPRs
+# (AGPRs only as overflow), which avoids VGPR<->AGPR copies of the output tile.
+EXTRA = {"fwd_bf16.hip": ["-mllvm", "--amdgpu-mfma-vgpr-form=1"],
+         "bwd_bf16.hip": ["-mllvm", "--amdgpu-mfma-vgpr-form=1"]}
 ARCH = os.environ.get("LS_OFFLOAD_ARCH", "gfx950")
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
@@ -36,26 +40,28 @@ def _run(cmd):
     return out
 
 
-def build(verbose: bool = False, save_temps: bool = False) -> str:
+def build(verbose: bool = False, save_temps: bool = False, out: str = LIB, extra=None) -> str:
     os.makedirs(BUILD, exist_ok=True)
     objs = []
     cmds = []
     for src in SOURCES:
         obj = os.path.join(BUILD, src.replace(".hip", ".o"))
         objs.append(obj)
-        extra = ["-save-temps=obj"] if save_temps else []
-        cmds.append([HIPCC, *FLAGS, *extra, "-c", os.path.join(CSRC, src), "-o", obj])
+        flags = list(EXTRA.get(src, [])) if extra is None else list(extra.get(src, []))
+        if save_temps:
+            flags.append("-save-temps=obj")
+        cmds.append([HIPCC, *FLAGS, *flags, "-c", os.path.join(CSRC, src), "-o", obj])
     with ThreadPoolExecutor(min(len(cmds), os.cpu_count() or 4)) as ex:
         outs = list(ex.map(_run, cmds))
-    tmp = LIB + ".tmp"
+    tmp = out + ".tmp"
     outs.append(_run([HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-o", tmp]))
-    os.replace(tmp, LIB)
+    os.replace(tmp, out)
     if verbose:
         for o in outs:
             if o.strip():
                 print(o)
-        print("built", LIB)
-    return LIB
+        print("built", out)
+    return out
 
 
 if __name__ == "__main__":

@@ -4,9 +4,11 @@
 // dq kernel: workgroup = 4 waves = 128 packed query rows of one KV head, lane
 // l owns row l % 32.  Per 32-key tile it recomputes S^T = K Q^T, forms
 // P = exp2(s*scale*log2e - lse2) with the merged log-normalizer, dP^T = V dO^T,
-// dS = P (dP - Delta) and accumulates dq^T += K^T dS^T.  K and V tiles are
-// staged in double-buffered LDS row-major (A operands of the first two
-// products) and K once more key-transposed (A operand of the third).
+// dS = P (dP - Delta) and accumulates dq^T += K^T dS^T.  K and V tiles arrive
+// by direct global->LDS loads into a three-slot ring (row-major, swizzled);
+// the K^T operand of the third product comes from transposing LDS reads of
+// the same K tile.  The dq product of tile t-1 is issued in the same block as
+// the exponentials of tile t.
 //
 // dk/dv kernel: one wave per 32 response keys of one KV head; lane l owns key
 // l % 32.  Per block of 32 packed query rows it computes S = Q K^T and
@@ -25,69 +27,72 @@ constexpr int kD = 256;
 
 // ============================================================== dq kernel
 constexpr int kQBM = 128;
-constexpr int kQBN = 32;
+constexpr int kQBN = kTileKeys;                   // 32
 constexpr int kRowBytes = kD * 2;                 // 512 B: one key row
-constexpr int kTileBytes = kQBN * kRowBytes;      // 16 KiB
-constexpr int kQStage = 3 * kTileBytes;           // K, V row-major + K transposed
+constexpr int kQStage = 2 * kTileBytes;           // K tile + V tile (row-major, swizzled)
+constexpr int kQSlots = 3;
 
-struct DqRegs {
-  u32x4 k[4];   // keys 4m .. 4m+3 (m = lane & 7), chunk c = (lane >> 3) + 8*wave
-  u32x4 v[4];
-};
-
-__device__ __forceinline__ void dq_load(const BwdArgs& a, int g, int64_t t0, int64_t k_hi,
-                                        int tid, DqRegs& R) {
-  const int lane = tid & 63, w = tid >> 6;
-  const int m = lane & 7, c = (lane >> 3) + 8 * w;
-  const int64_t S = int64_t(1) << a.log2_page;
-  const bool one_page = ((t0 & (S - 1)) + kQBN) <= S;
-  int64_t base = 0;
-  if (one_page) base = phys_pos(a.page_table, t0, a.log2_page);
-  const __bf16* kp = static_cast<const __bf16*>(a.k_pool) + (int64_t)g * kD + c * 8;
-  const __bf16* vp = static_cast<const __bf16*>(a.v_pool) + (int64_t)g * kD + c * 8;
-  const u32x4 zero = {0u, 0u, 0u, 0u};
+// S^T = K Q^T and dP^T = V dO^T for one 32-key tile (operand reads issued ahead).
+__device__ __forceinline__ void scores_dp(const char* Ks, const char* Vs, const bf16x8* qreg,
+                                          const bf16x8* dreg, const TileOffsets& o, f32x16& s,
+                                          f32x16& dp) {
+  s = zero16();
+  dp = zero16();
 #pragma unroll
-  for (int kk = 0; kk < 4; ++kk) {
-    const int key = 4 * m + kk;
-    const int64_t j = t0 + key;
-    if (j < k_hi) {
-      const int64_t pr = one_page ? base + key : phys_pos(a.page_table, j, a.log2_page);
-      R.k[kk] = *reinterpret_cast<const u32x4*>(kp + pr * a.k_pos_stride);
-      R.v[kk] = *reinterpret_cast<const u32x4*>(vp + pr * a.v_pos_stride);
-    } else {
-      R.k[kk] = zero;
-      R.v[kk] = zero;
+  for (int ks = 0; ks < 16; ++ks) {
+    s = mfma32(tile_row16(Ks, o, ks), qreg[ks], s);
+    dp = mfma32(tile_row16(Vs, o, ks), dreg[ks], dp);
+  }
+}
+
+// dq^T += K^T dS^T for one 32-key tile; dS register block kk holds keys
+// 16kk + {4h..4h+3, 8+4h..8+4h+3}, matched by the transposed K reads.
+__device__ __forceinline__ void dq_update(const char* Ks, const bf16x8& d0, const bf16x8& d1,
+                                          f32x16* acc, const TileOffsets& o) {
+#pragma unroll
+  for (int db = 0; db < 8; ++db) {
+    acc[db] = mfma32(tile_col8(Ks, o, db, 0, 8), d0, acc[db]);
+    acc[db] = mfma32(tile_col8(Ks, o, db, 16, 24), d1, acc[db]);
+  }
+}
+
+// One pipelined step (ring slots are distinct; see the forward kernel).
+template <bool kPerKey, bool kFirst>
+__device__ __forceinline__ void dq_step(const BwdArgs& a, char* __restrict__ next,
+                                        const char* __restrict__ cur,
+                                        const char* __restrict__ prev_k, const TileFetch& kf,
+                                        const TileFetch& vf, int64_t t0_next, int64_t prow_next,
+                                        int64_t k_hi, int64_t t0, int64_t kb, int64_t k_all,
+                                        int64_t my_lim, const bf16x8* qreg, const bf16x8* dreg,
+                                        const TileOffsets& to, int hh, float lse2, float delta,
+                                        f32x16* acc, bf16x8& d0, bf16x8& d1) {
+  if (!kPerKey && t0_next + kQBN <= k_hi) {
+    kf.issue_page(next, prow_next);
+    vf.issue_page(next + kTileBytes, prow_next);
+  } else {
+    kf.issue_rows(next, a.page_table, a.log2_page, t0_next, k_hi);
+    vf.issue_rows(next + kTileBytes, a.page_table, a.log2_page, t0_next, k_hi);
+  }
+  f32x16 s, dp;
+  scores_dp(cur, cur + kTileBytes, qreg, dreg, to, s, dp);
+  const bool edge = t0 < kb || t0 + kQBN > k_all;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) {
+    float p = __builtin_amdgcn_exp2f(fmaf(s[r], a.scale_log2, -lse2));
+    if (edge) {
+      const int64_t j = t0 + acc_key(r, hh);
+      if (j < kb || j >= my_lim) p = 0.f;
     }
+    s[r] = p * (dp[r] - delta);          // dS
   }
+  if (!kFirst) dq_update(prev_k, d0, d1, acc, to);
+  d0 = pack8(s, 0);
+  d1 = pack8(s, 1);
 }
 
-__device__ __forceinline__ void dq_store(char* stage, int tid, const DqRegs& R) {
-  const int lane = tid & 63, w = tid >> 6;
-  const int m = lane & 7, c = (lane >> 3) + 8 * w;
-  char* Ks = stage;
-  char* Vs = stage + kTileBytes;
-  char* Kt = stage + 2 * kTileBytes;
-#pragma unroll
-  for (int kk = 0; kk < 4; ++kk) {
-    const int key = 4 * m + kk;
-    const int off = key * kRowBytes + ((c ^ (key & 7)) << 4);
-    *reinterpret_cast<u32x4*>(Ks + off) = R.k[kk];
-    *reinterpret_cast<u32x4*>(Vs + off) = R.v[kk];
-  }
-  // K^T [d][32 key slots], 64 B per d row, 16-byte chunk x stored at x ^ ((d >> 1) & 3)
-  const int slot = swap23(4 * m);
-  const int sc = slot >> 3, sb = (slot & 7) * 2;
-#pragma unroll
-  for (int e = 0; e < 8; ++e) {
-    const int d = 8 * c + e;
-    const int dw = e >> 1;
-    const u32x2 val = pick4(R.k[0][dw], R.k[1][dw], R.k[2][dw], R.k[3][dw], (e & 1) != 0);
-    *reinterpret_cast<u32x2*>(Kt + d * (kQBN * 2) + ((sc ^ ((d >> 1) & 3)) << 4) + sb) = val;
-  }
-}
-
+template <bool kPerKey>
 __global__ __launch_bounds__(256, 1) void bwd_dq_bf16_d256_kernel(BwdArgs a) {
-  __shared__ __attribute__((aligned(16))) char smem[2 * kQStage];
+  __shared__ __attribute__((aligned(1024))) char smem[kQSlots * kQStage];
 
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int l32 = lane & 31, hh = lane >> 5;
@@ -105,7 +110,8 @@ __global__ __launch_bounds__(256, 1) void bwd_dq_bf16_d256_kernel(BwdArgs a) {
   const int64_t k_hi = min(a.kv_end, a.q_pos0 + tok_last + 1);
   const int64_t k_all = min(a.kv_end, a.q_pos0 + tok_first + 1);
   const int64_t my_lim = min(a.kv_end, a.q_pos0 + tok + 1);
-  const int n_tiles = k_hi > kb ? (int)((k_hi - kb + kQBN - 1) / kQBN) : 0;
+  const int64_t k_lo = kb & ~int64_t(kQBN - 1);
+  const int n_tiles = k_hi > kb ? (int)((k_hi - k_lo + kQBN - 1) / kQBN) : 0;
 
   float* dq = a.dq + ((int64_t)tok * a.n_q_heads + head) * kD;
   if (n_tiles == 0) {
@@ -116,6 +122,25 @@ __global__ __launch_bounds__(256, 1) void bwd_dq_bf16_d256_kernel(BwdArgs a) {
     }
     return;
   }
+
+  TileFetch kf, vf;
+  kf.init(static_cast<const __bf16*>(a.k_pool) + (int64_t)g * kD, a.k_pos_stride, lane, w);
+  vf.init(static_cast<const __bf16*>(a.v_pool) + (int64_t)g * kD, a.v_pos_stride, lane, w);
+  auto page_row = [&](int t) -> int64_t {
+    return kPerKey ? 0 : phys_pos_uniform(a.page_table, k_lo + (int64_t)t * kQBN, a.log2_page);
+  };
+  const TileOffsets to = tile_offsets(lane);
+  {
+    const int64_t pr0 = page_row(0);
+    if (!kPerKey && k_lo + kQBN <= k_hi) {
+      kf.issue_page(smem, pr0);
+      vf.issue_page(smem + kTileBytes, pr0);
+    } else {
+      kf.issue_rows(smem, a.page_table, a.log2_page, k_lo, k_hi);
+      vf.issue_rows(smem + kTileBytes, a.page_table, a.log2_page, k_lo, k_hi);
+    }
+  }
+  int64_t prow_next = page_row(n_tiles > 1 ? 1 : 0);
 
   bf16x8 qreg[16], dreg[16];
   {
@@ -140,49 +165,33 @@ __global__ __launch_bounds__(256, 1) void bwd_dq_bf16_d256_kernel(BwdArgs a) {
   f32x16 acc[8];
 #pragma unroll
   for (int i = 0; i < 8; ++i) acc[i] = zero16();
+  bf16x8 d0, d1;
 
-  DqRegs R;
-  dq_load(a, g, kb, k_hi, tid, R);
-  dq_store(smem, tid, R);
+  wait_fetch();
   __syncthreads();
-
-  const int swz = l32 & 7;
-  const int tswz = (l32 >> 1) & 3;
-  for (int t = 0; t < n_tiles; ++t) {
-    const int64_t t0 = kb + (int64_t)t * kQBN;
-    if (t + 1 < n_tiles) dq_load(a, g, t0 + kQBN, k_hi, tid, R);
-    const char* Ks = smem + (t & 1) * kQStage;
-    const char* Vs = Ks + kTileBytes;
-    const char* Kt = Ks + 2 * kTileBytes;
-
-    f32x16 s = zero16(), dp = zero16();
-#pragma unroll
-    for (int ks = 0; ks < 16; ++ks) {
-      const int off = l32 * kRowBytes + (((2 * ks + hh) ^ swz) << 4);
-      const bf16x8 kv = *reinterpret_cast<const bf16x8*>(Ks + off);
-      const bf16x8 vv = *reinterpret_cast<const bf16x8*>(Vs + off);
-      s = mfma32(kv, qreg[ks], s);
-      dp = mfma32(vv, dreg[ks], dp);
-    }
-    const bool edge = t0 + kQBN > k_all;
-#pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      float p = __builtin_amdgcn_exp2f(fmaf(s[r], a.scale_log2, -lse2));
-      if (edge && t0 + acc_key(r, hh) >= my_lim) p = 0.f;
-      s[r] = p * (dp[r] - delta);          // dS
-    }
-    const bf16x8 ds0 = pack8(s, 0), ds1 = pack8(s, 1);
-#pragma unroll
-    for (int db = 0; db < 8; ++db) {
-      const char* row = Kt + (32 * db + l32) * (kQBN * 2);
-      const bf16x8 k0 = *reinterpret_cast<const bf16x8*>(row + (((0 + hh) ^ tswz) << 4));
-      const bf16x8 k1 = *reinterpret_cast<const bf16x8*>(row + (((2 + hh) ^ tswz) << 4));
-      acc[db] = mfma32(k0, ds0, acc[db]);
-      acc[db] = mfma32(k1, ds1, acc[db]);
-    }
-    if (t + 1 < n_tiles) dq_store(smem + ((t + 1) & 1) * kQStage, tid, R);
+  {
+    const int tn = n_tiles > 1 ? 1 : 0;
+    const int64_t prow_after = page_row(n_tiles > 2 ? 2 : n_tiles - 1);
+    dq_step<kPerKey, true>(a, smem + kQStage, smem, smem, kf, vf, k_lo + (int64_t)tn * kQBN,
+                           prow_next, k_hi, k_lo, kb, k_all, my_lim, qreg, dreg, to, hh, lse2,
+                           delta, acc, d0, d1);
+    prow_next = prow_after;
+    wait_fetch();
     __syncthreads();
   }
+  for (int t = 1; t < n_tiles; ++t) {
+    const int64_t t0 = k_lo + (int64_t)t * kQBN;
+    const int tn = t + 1 < n_tiles ? t + 1 : t;
+    const int64_t prow_after = page_row(tn + 1 < n_tiles ? tn + 1 : tn);
+    dq_step<kPerKey, false>(a, smem + ((t + 1) % kQSlots) * kQStage,
+                            smem + (t % kQSlots) * kQStage, smem + ((t - 1) % kQSlots) * kQStage,
+                            kf, vf, k_lo + (int64_t)tn * kQBN, prow_next, k_hi, t0, kb, k_all,
+                            my_lim, qreg, dreg, to, hh, lse2, delta, acc, d0, d1);
+    prow_next = prow_after;
+    wait_fetch();
+    __syncthreads();
+  }
+  dq_update(smem + ((n_tiles - 1) % kQSlots) * kQStage, d0, d1, acc, to);
 
   if (row_ok) {
 #pragma unroll
@@ -371,8 +380,12 @@ hipError_t launch_bwd_bf16_d256(const BwdArgs& a, bool need_dq, bool need_dkv,
                                 hipStream_t stream) {
   if (need_dq) {
     const unsigned row_tiles = (unsigned)(((int64_t)a.n_q * a.group + kQBM - 1) / kQBM);
-    hipLaunchKernelGGL(bwd_dq_bf16_d256_kernel, dim3(row_tiles, a.n_kv_heads), dim3(256), 0,
-                       stream, a);
+    if (a.log2_page < 5)
+      hipLaunchKernelGGL(bwd_dq_bf16_d256_kernel<true>, dim3(row_tiles, a.n_kv_heads), dim3(256),
+                         0, stream, a);
+    else
+      hipLaunchKernelGGL(bwd_dq_bf16_d256_kernel<false>, dim3(row_tiles, a.n_kv_heads), dim3(256),
+                         0, stream, a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }

@@ -1,20 +1,23 @@
 // bf16 split-KV forward for head_dim = 256 on gfx950 (Eq. qwen-local-attn).
 //
-// Workgroup = 4 waves = 128 packed query rows of one KV head: row r of the
-// group's packed rows is (token r / G, head g*G + r % G), so every K/V tile
-// staged in LDS feeds all G query heads that share it.  Each wave owns 32
-// rows; lane l owns row l % 32 (scores are computed transposed, S^T = K Q^T).
+// Workgroup = 4 waves = 128 packed query rows of one KV head: packed row r is
+// (token r / G, head g*G + r % G), so every K/V tile staged in LDS feeds all G
+// query heads that share it.  Each wave owns 32 rows; lane l owns row l % 32
+// (scores are computed transposed, S^T = K Q^T, so row statistics stay in one
+// lane).
 //
-// Per 64-key tile the K rows and V columns are fetched through the page table
-// (one table entry per tile when the tile lies in one page) into registers one
-// tile ahead, then written to a double-buffered LDS stage:
-//   K  : [64 keys][256 d]  row-major, 16-byte chunk c stored at c ^ (key & 7)
-//   V^T: [256 d][64 keys]  key-transposed (bits 3,2 swapped in each 16-key
-//        group), 16-byte chunk c stored at c ^ (d & 7)
-// so that every MFMA operand read is one conflict-free 16-byte LDS load.
-// Softmax statistics stay in fp32 registers (base-2 exponent with the scale
-// folded in); P is rounded to bf16 for the PV product; the split writes the
-// normalized fp32 output and the natural-log normalizer.
+// Keys are processed in 32-key tiles aligned to multiples of 32 (one page-table
+// entry per tile when pages hold >= 32 positions).  K and V rows are fetched
+// with direct global->LDS loads into a three-slot ring, one tile ahead; no
+// VGPRs stage them.  The K^T operand is one 16-byte LDS read per lane; the V^T
+// operand comes from transposing LDS reads of the row-major V tile.
+//
+// The loop is software-pipelined across tiles: iteration t issues the score
+// MFMAs of tile t, then the softmax of tile t (exp2 on the VALU) in the same
+// basic block as the PV MFMAs of tile t-1.  Statistics stay in fp32 registers
+// (base-2 exponent with the scale folded in); P is rounded to bf16 for the PV
+// product.  The split writes the normalized fp32 output and the natural-log
+// normalizer.
 #include <math.h>
 
 #include "ls_internal.h"
@@ -25,95 +28,110 @@ namespace {
 
 constexpr int kD = 256;
 constexpr int kBM = 128;
-constexpr int kBN = 64;
-constexpr int kKBytes = kBN * kD * 2;    // 32 KiB
-constexpr int kVBytes = kD * kBN * 2;    // 32 KiB
-constexpr int kStage = kKBytes + kVBytes;
+constexpr int kBN = kTileKeys;              // 32
+constexpr int kStage = 2 * kTileBytes;      // K tile + V tile
+constexpr int kSlots = 3;
 
-struct TileRegs {
-  u32x4 k[8];   // K: key (tid>>5) + 8i, chunk tid & 31
-  u32x4 v[8];   // V: key 4*(lane&15) + kk, chunk (lane>>4) + 4*wave + 16*i; index kk*2 + i
-};
-
-// Fetch keys [t0, t0 + 64) of KV head g (keys >= k_hi read as zero).
-__device__ __forceinline__ void load_tile(const FwdArgs& a, int g, int64_t t0, int64_t k_hi,
-                                          int tid, TileRegs& R) {
-  const int lane = tid & 63, w = tid >> 6;
-  const int64_t S = int64_t(1) << a.log2_page;
-  const bool one_page = ((t0 & (S - 1)) + kBN) <= S;
-  int64_t base = 0;
-  if (one_page) base = phys_pos(a.page_table, t0, a.log2_page);
-  const __bf16* kp = static_cast<const __bf16*>(a.k_pool) + (int64_t)g * kD;
-  const __bf16* vp = static_cast<const __bf16*>(a.v_pool) + (int64_t)g * kD;
-  const u32x4 zero = {0u, 0u, 0u, 0u};
-  {
-    const int c = tid & 31;
+// S^T (32 keys x this lane's row) = K Q^T over the 256-wide head.
+// The K operand reads run two steps ahead of the MFMA chain.
+__device__ __forceinline__ f32x16 scores(const char* Ks, const bf16x8* qreg, const TileOffsets& o) {
+  f32x16 s = zero16();
+  bf16x8 k0 = tile_row16(Ks, o, 0), k1 = tile_row16(Ks, o, 1);
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const int key = (tid >> 5) + 8 * i;
-      const int64_t j = t0 + key;
-      if (j < k_hi) {
-        const int64_t pr = one_page ? base + key : phys_pos(a.page_table, j, a.log2_page);
-        R.k[i] = *reinterpret_cast<const u32x4*>(kp + pr * a.k_pos_stride + c * 8);
-      } else {
-        R.k[i] = zero;
-      }
-    }
+  for (int ks = 0; ks < 16; ++ks) {
+    const bf16x8 kn = tile_row16(Ks, o, ks + 2 < 16 ? ks + 2 : 15);
+    s = mfma32(k0, qreg[ks], s);
+    k0 = k1;
+    k1 = kn;
   }
-  {
-    const int m = lane & 15, cq = lane >> 4;
+  __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
 #pragma unroll
-    for (int kk = 0; kk < 4; ++kk) {
-      const int key = 4 * m + kk;
-      const int64_t j = t0 + key;
-      const bool ok = j < k_hi;
-      const int64_t pr = ok ? (one_page ? base + key : phys_pos(a.page_table, j, a.log2_page)) : 0;
+  for (int ks = 0; ks < 14; ++ks) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+    __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+  }
+  __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+  return s;
+}
+
+// O^T += V^T P^T for one 32-key tile.  P's register block kk holds keys
+// 16kk + {4h..4h+3, 8+4h..8+4h+3}; the V^T operand reads the same keys.
+__device__ __forceinline__ void pv(const char* Vs, const bf16x8& p0, const bf16x8& p1,
+                                   f32x16* oacc, const TileOffsets& o) {
 #pragma unroll
-      for (int i = 0; i < 2; ++i) {
-        const int c = cq + 4 * w + 16 * i;
-        R.v[kk * 2 + i] =
-            ok ? *reinterpret_cast<const u32x4*>(vp + pr * a.v_pos_stride + c * 8) : zero;
-      }
-    }
+  for (int db = 0; db < 8; ++db) {
+    const bf16x8 v0 = tile_col8(Vs, o, db, 0, 8);
+    const bf16x8 v1 = tile_col8(Vs, o, db, 16, 24);
+    oacc[db] = mfma32(v0, p0, oacc[db]);
+    oacc[db] = mfma32(v1, p1, oacc[db]);
   }
 }
 
-__device__ __forceinline__ void store_tile(char* stage, int tid, const TileRegs& R) {
-  const int lane = tid & 63, w = tid >> 6;
-  char* Ks = stage;
-  char* Vt = stage + kKBytes;
-  {
-    const int c = tid & 31;
+// Keys outside [lo, lim) (split begin, causal edge or split end) get -inf.
+__device__ __forceinline__ void mask_tile(f32x16& s, int64_t t0, int64_t lo, int64_t lim, int hh) {
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const int key = (tid >> 5) + 8 * i;
-      *reinterpret_cast<u32x4*>(Ks + key * (kD * 2) + ((c ^ (key & 7)) << 4)) = R.k[i];
-    }
-  }
-  {
-    const int m = lane & 15, cq = lane >> 4;
-    const int slot = swap23(4 * m);             // 4 consecutive keys -> 4 consecutive slots
-    const int sc = slot >> 3, sb = (slot & 7) * 2;
-#pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      const int c = cq + 4 * w + 16 * i;
-      const u32x4& r0 = R.v[0 * 2 + i];
-      const u32x4& r1 = R.v[1 * 2 + i];
-      const u32x4& r2 = R.v[2 * 2 + i];
-      const u32x4& r3 = R.v[3 * 2 + i];
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const int dw = e >> 1;
-        const int dv = 8 * c + e;
-        const u32x2 val = pick4(r0[dw], r1[dw], r2[dw], r3[dw], (e & 1) != 0);
-        *reinterpret_cast<u32x2*>(Vt + dv * (kBN * 2) + ((sc ^ e) << 4) + sb) = val;
-      }
-    }
+  for (int r = 0; r < 16; ++r) {
+    const int64_t j = t0 + acc_key(r, hh);
+    if (j < lo || j >= lim) s[r] = -INFINITY;
   }
 }
 
+// Online softmax step over one tile (base-2, scale folded in): s becomes
+// exp2(s*c - m_new); returns alpha = exp2(m_old - m_new), the factor that
+// rescales earlier partial sums.  A row with no visible key so far keeps
+// m = -inf and P = 0.
+__device__ __forceinline__ float softmax_tile(f32x16& s, float c, float& m_run, float& l_run) {
+  float mx = s[0];
+#pragma unroll
+  for (int r = 1; r < 16; ++r) mx = fmaxf(mx, s[r]);
+  mx = half_max(mx);
+  const float m_new = fmaxf(m_run, mx * c);
+  const float m_use = m_new == -INFINITY ? 0.f : m_new;
+  const float alpha = __builtin_amdgcn_exp2f(m_run - m_use);
+  float psum = 0.f;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) {
+    s[r] = __builtin_amdgcn_exp2f(fmaf(s[r], c, -m_use));
+    psum += s[r];
+  }
+  l_run = fmaf(l_run, alpha, psum);
+  m_run = m_new;
+  return alpha;
+}
+
+// One pipelined step: scores of the tile in `ks_cur`, the PV product of the
+// previous tile (V in `vs_prev`, P in p0/p1), while the next tile streams into
+// `next`.  The three LDS regions are distinct ring slots; the restrict
+// qualifiers tell the compiler so, which lets it keep LDS reads running while
+// the direct loads into `next` are in flight.
+template <bool kPerKey, bool kFirst>
+__device__ __forceinline__ float step(const FwdArgs& a, char* __restrict__ next,
+                                      const char* __restrict__ ks_cur,
+                                      const char* __restrict__ vs_prev, const TileFetch& kf,
+                                      const TileFetch& vf, int64_t t0_next, int64_t prow_next,
+                                      int64_t k_hi, int64_t t0, int64_t kb, int64_t k_all,
+                                      int64_t my_lim, const bf16x8* qreg, const TileOffsets& to,
+                                      int hh, f32x16* oacc, bf16x8& p0, bf16x8& p1, float& m_run,
+                                      float& l_run) {
+  if (!kPerKey && t0_next + kBN <= k_hi) {
+    kf.issue_page(next, prow_next);
+    vf.issue_page(next + kTileBytes, prow_next);
+  } else {
+    kf.issue_rows(next, a.page_table, a.log2_page, t0_next, k_hi);
+    vf.issue_rows(next + kTileBytes, a.page_table, a.log2_page, t0_next, k_hi);
+  }
+  f32x16 s = scores(ks_cur, qreg, to);
+  if (t0 < kb || t0 + kBN > k_all) mask_tile(s, t0, kb, my_lim, hh);
+  const float alpha = softmax_tile(s, a.scale_log2, m_run, l_run);
+  if (!kFirst) pv(vs_prev, p0, p1, oacc, to);
+  p0 = pack8(s, 0);
+  p1 = pack8(s, 1);
+  return alpha;
+}
+
+template <bool kPerKey>
 __global__ __launch_bounds__(256, 1) void fwd_bf16_d256_kernel(FwdArgs a) {
-  __shared__ __attribute__((aligned(16))) char smem[2 * kStage];
+  __shared__ __attribute__((aligned(1024))) char smem[kSlots * kStage];
 
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int l32 = lane & 31, hh = lane >> 5;
@@ -131,10 +149,11 @@ __global__ __launch_bounds__(256, 1) void fwd_bf16_d256_kernel(FwdArgs a) {
   const int64_t k_hi = min(ke, a.q_pos0 + tok_last + 1);   // keys of the WG: [kb, k_hi)
   const int64_t k_all = min(ke, a.q_pos0 + tok_first + 1); // below: visible to every row
   const int64_t my_lim = min(ke, a.q_pos0 + tok + 1);
+  const int64_t k_lo = kb & ~int64_t(kBN - 1);              // tile origin
 
   float* out = a.out_part + (((int64_t)sp * a.n_q + tok) * a.n_q_heads + head) * kD;
   float* lse_out = a.lse_part + (int64_t)sp * a.n_q * a.n_q_heads + (int64_t)head * a.n_q + tok;
-  const int n_tiles = k_hi > kb ? (int)((k_hi - kb + kBN - 1) / kBN) : 0;
+  const int n_tiles = k_hi > kb ? (int)((k_hi - k_lo + kBN - 1) / kBN) : 0;
   if (n_tiles == 0) {
     if (row_ok) {
       const f32x4 z = {0.f, 0.f, 0.f, 0.f};
@@ -144,6 +163,30 @@ __global__ __launch_bounds__(256, 1) void fwd_bf16_d256_kernel(FwdArgs a) {
     }
     return;
   }
+
+  TileFetch kf, vf;
+  kf.init(static_cast<const __bf16*>(a.k_pool) + (int64_t)g * kD, a.k_pos_stride, lane, w);
+  vf.init(static_cast<const __bf16*>(a.v_pool) + (int64_t)g * kD, a.v_pos_stride, lane, w);
+  // Tile t lies in one page unless pages are shorter than a tile; its page row
+  // is looked up one iteration before the fetch, so consuming it never waits
+  // on the DMA loads in flight.  The tile that reaches k_hi takes per-row lookups.
+  auto page_row = [&](int t) -> int64_t {
+    return kPerKey ? 0 : phys_pos_uniform(a.page_table, k_lo + (int64_t)t * kBN, a.log2_page);
+  };
+  auto fetch = [&](int t, int slot, int64_t prow) {
+    const int64_t t0 = k_lo + (int64_t)t * kBN;
+    char* st = smem + slot * kStage;
+    if (!kPerKey && t0 + kBN <= k_hi) {
+      kf.issue_page(st, prow);
+      vf.issue_page(st + kTileBytes, prow);
+    } else {
+      kf.issue_rows(st, a.page_table, a.log2_page, t0, k_hi);
+      vf.issue_rows(st + kTileBytes, a.page_table, a.log2_page, t0, k_hi);
+    }
+  };
+  const TileOffsets to = tile_offsets(lane);
+  fetch(0, 0, page_row(0));
+  int64_t prow_next = page_row(n_tiles > 1 ? 1 : 0);
 
   // Q^T operand: lane holds q[row][16*ks + 8*hh .. +7]
   bf16x8 qreg[16];
@@ -164,81 +207,42 @@ __global__ __launch_bounds__(256, 1) void fwd_bf16_d256_kernel(FwdArgs a) {
 #pragma unroll
   for (int i = 0; i < 8; ++i) oacc[i] = zero16();
   float m_run = -INFINITY, l_run = 0.f;
+  bf16x8 p0, p1;   // packed P of the previous tile
 
-  TileRegs R;
-  load_tile(a, g, kb, k_hi, tid, R);
-  store_tile(smem, tid, R);
+  wait_fetch();
   __syncthreads();
 
-  for (int t = 0; t < n_tiles; ++t) {
-    const int64_t t0 = kb + (int64_t)t * kBN;
-    if (t + 1 < n_tiles) load_tile(a, g, t0 + kBN, k_hi, tid, R);
-
-    const char* Ks = smem + (t & 1) * kStage;
-    const char* Vt = Ks + kKBytes;
-
-    // S^T for keys [t0, t0+32) (s0) and [t0+32, t0+64) (s1)
-    f32x16 s0 = zero16(), s1 = zero16();
-    const int swz = l32 & 7;
-#pragma unroll
-    for (int ks = 0; ks < 16; ++ks) {
-      const int c = ((2 * ks + hh) ^ swz) << 4;
-      const bf16x8 k0 = *reinterpret_cast<const bf16x8*>(Ks + l32 * (kD * 2) + c);
-      const bf16x8 k1 = *reinterpret_cast<const bf16x8*>(Ks + (32 + l32) * (kD * 2) + c);
-      s0 = mfma32(k0, qreg[ks], s0);
-      s1 = mfma32(k1, qreg[ks], s1);
-    }
-
-    if (t0 + kBN > k_all) {   // tile crosses the causal edge or the split end
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int64_t j = t0 + acc_key(r, hh);
-        if (j >= my_lim) s0[r] = -INFINITY;
-        if (j + 32 >= my_lim) s1[r] = -INFINITY;
-      }
-    }
-
-    float mx = -INFINITY;
-#pragma unroll
-    for (int r = 0; r < 16; ++r) mx = fmaxf(mx, fmaxf(s0[r], s1[r]));
-    mx = fmaxf(mx, __shfl_xor(mx, 32));
-    const float m_new = fmaxf(m_run, mx * a.scale_log2);
-    const float m_use = m_new == -INFINITY ? 0.f : m_new;
-    const float alpha = __builtin_amdgcn_exp2f(m_run - m_use);
-    float psum = 0.f;
-#pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      s0[r] = __builtin_amdgcn_exp2f(fmaf(s0[r], a.scale_log2, -m_use));
-      s1[r] = __builtin_amdgcn_exp2f(fmaf(s1[r], a.scale_log2, -m_use));
-      psum += s0[r] + s1[r];
-    }
-    l_run = fmaf(l_run, alpha, psum);
-    m_run = m_new;
-    if (__any(alpha != 1.f)) {
+  // tile 0 (peeled: no previous P to multiply)
+  {
+    const int tn = n_tiles > 1 ? 1 : 0;
+    const int64_t prow_after = page_row(n_tiles > 2 ? 2 : n_tiles - 1);
+    step<kPerKey, true>(a, smem + kStage, smem, smem + kTileBytes, kf, vf, k_lo + (int64_t)tn * kBN,
+                        prow_next, k_hi, k_lo, kb, k_all, my_lim, qreg, to, hh, oacc, p0, p1,
+                        m_run, l_run);
+    prow_next = prow_after;
+    wait_fetch();
+    __syncthreads();
+  }
+  for (int t = 1; t < n_tiles; ++t) {
+    const int64_t t0 = k_lo + (int64_t)t * kBN;
+    const int tn = t + 1 < n_tiles ? t + 1 : t;   // the last iteration refetches its own tile
+    const int64_t prow_after = page_row(tn + 1 < n_tiles ? tn + 1 : tn);
+    const float alpha = step<kPerKey, false>(
+        a, smem + ((t + 1) % kSlots) * kStage, smem + (t % kSlots) * kStage,
+        smem + ((t - 1) % kSlots) * kStage + kTileBytes, kf, vf, k_lo + (int64_t)tn * kBN,
+        prow_next, k_hi, t0, kb, k_all, my_lim, qreg, to, hh, oacc, p0, p1, m_run, l_run);
+    prow_next = prow_after;
+    // (l_run < 0 never holds; it keeps the exponentials ahead of this branch)
+    if (__any(alpha != 1.f || l_run < 0.f)) {
 #pragma unroll
       for (int i = 0; i < 8; ++i) oacc[i] *= alpha;
     }
-
-    bf16x8 pb[4];
-    pb[0] = pack8(s0, 0);
-    pb[1] = pack8(s0, 1);
-    pb[2] = pack8(s1, 0);
-    pb[3] = pack8(s1, 1);
-#pragma unroll
-    for (int kk = 0; kk < 4; ++kk) {
-      const int c = ((2 * kk + hh) ^ swz) << 4;
-#pragma unroll
-      for (int db = 0; db < 8; ++db) {
-        const bf16x8 vv = *reinterpret_cast<const bf16x8*>(Vt + (32 * db + l32) * (kBN * 2) + c);
-        oacc[db] = mfma32(vv, pb[kk], oacc[db]);
-      }
-    }
-
-    if (t + 1 < n_tiles) store_tile(smem + ((t + 1) & 1) * kStage, tid, R);
+    wait_fetch();
     __syncthreads();
   }
+  pv(smem + ((n_tiles - 1) % kSlots) * kStage + kTileBytes, p0, p1, oacc, to);
 
-  const float l_tot = l_run + __shfl_xor(l_run, 32);
+  const float l_tot = half_sum(l_run);
   if (row_ok) {
     const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
 #pragma unroll
@@ -262,8 +266,11 @@ __global__ __launch_bounds__(256, 1) void fwd_bf16_d256_kernel(FwdArgs a) {
 
 hipError_t launch_fwd_bf16_d256(const FwdArgs& a, hipStream_t stream) {
   const unsigned row_tiles = (unsigned)(((int64_t)a.n_q * a.group + kBM - 1) / kBM);
-  hipLaunchKernelGGL(fwd_bf16_d256_kernel, dim3(row_tiles, a.n_kv_heads, a.n_splits), dim3(256),
-                     0, stream, a);
+  const dim3 grid(row_tiles, a.n_kv_heads, a.n_splits);
+  if (a.log2_page < 5)
+    hipLaunchKernelGGL(fwd_bf16_d256_kernel<true>, grid, dim3(256), 0, stream, a);
+  else
+    hipLaunchKernelGGL(fwd_bf16_d256_kernel<false>, grid, dim3(256), 0, stream, a);
   return hipGetLastError();
 }
 

@@ -68,10 +68,143 @@ __device__ __forceinline__ u32x2 pick4(uint32_t w0, uint32_t w1, uint32_t w2, ui
   return r;
 }
 
+typedef __attribute__((__vector_size__(4 * sizeof(short)))) short i16x4;
+#define LS_LDS(p) ((__attribute__((address_space(3))) void*)(p))
+#define LS_LDS4(p) ((__attribute__((address_space(3))) i16x4*)(p))
+
+// ---------------------------------------------------------------- key tiles in LDS
+// A tile holds 32 key rows of 256 bf16 (512 bytes each), row-major.  The
+// 16-byte chunk c of row k is stored at chunk c ^ tile_swz(k).  The swizzle is
+// a permutation of the 8 chunks of every 128-byte group; it spreads over all
+// 32 banks both (a) eight consecutive rows read at one chunk (16-byte operand
+// reads) and (b) four consecutive rows read as 32-byte halves of a 16-lane
+// transposed read.
+constexpr int kTileKeys = 32;
+constexpr int kTileRow = 512;
+constexpr int kTileBytes = kTileKeys * kTileRow;   // 16 KiB
+
+__device__ __forceinline__ int tile_swz(int k) { return ((k & 3) << 1) | ((k >> 2) & 1); }
+
+// Lane-constant byte offsets for reading a tile.  For the row-per-lane
+// operand (lane supplies row l32, 16-byte chunk 2*ks + h) the swizzle only
+// touches the low three chunk bits, so the offset is row_off[ks & 3] +
+// 128 * (ks >> 2).  For the transposed operand (tile_col8) every row a lane
+// names is congruent to 4h + s/4 modulo 8, so its swizzle is also constant;
+// the offset is col_off[db & 1] + 128 * (db >> 1) + 512 * (row group start).
+struct TileOffsets {
+  int row_off[4];
+  int col_off[2];
+};
+
+__device__ __forceinline__ TileOffsets tile_offsets(int lane) {
+  TileOffsets o;
+  const int l32 = lane & 31, h = lane >> 5;
+  const int sw = tile_swz(l32);
+#pragma unroll
+  for (int q = 0; q < 4; ++q) o.row_off[q] = l32 * kTileRow + (((2 * q + h) ^ sw) << 4);
+  const int s = lane & 15;
+  const int x = 2 * ((lane >> 4) & 1) + ((s & 3) >> 1);   // chunk of the 4 columns, mod 4
+  const int row = 4 * h + (s >> 2);
+  const int swc = tile_swz(row);
+  const int base = row * kTileRow + ((s & 1) << 3);
+  o.col_off[0] = base + ((x ^ swc) << 4);
+  o.col_off[1] = base + (((4 + x) ^ swc) << 4);
+  return o;
+}
+
+// Operand with one key row per lane: row l32, chunk 2*ks + h.
+__device__ __forceinline__ bf16x8 tile_row16(const char* tile, const TileOffsets& o, int ks) {
+  return *reinterpret_cast<const bf16x8*>(tile + o.row_off[ks & 3] + 128 * (ks >> 2));
+}
+
+// Operand with one column per lane and eight keys along k (transposed read):
+// lane l = 32h + c gets column 32*db + c of rows r + 4h + {0..3} for
+// r = r0 (elements 0..3) and r = r1 (elements 4..7), r0 and r1 multiples of 8.
+// Each half is one ds_read_b64_tr_b16: in every 16-lane group, source lane s
+// names row (group start + s/4), columns 4*(s%4) .. +3 of the group's 16
+// columns, and lane i of the group receives column i of the four rows.
+__device__ __forceinline__ bf16x8 tile_col8(const char* tile, const TileOffsets& o, int db, int r0,
+                                            int r1) {
+  const char* p = tile + o.col_off[db & 1] + 128 * (db >> 1);
+  const i16x4 a = __builtin_amdgcn_ds_read_tr16_b64_v4i16(LS_LDS4(p + r0 * kTileRow));
+  const i16x4 b = __builtin_amdgcn_ds_read_tr16_b64_v4i16(LS_LDS4(p + r1 * kTileRow));
+  return __builtin_bit_cast(bf16x8, __builtin_shufflevector(a, b, 0, 1, 2, 3, 4, 5, 6, 7));
+}
+
+// Max of x over the two lane halves (lane l and l ^ 32) without LDS traffic.
+__device__ __forceinline__ float half_max(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+
+__device__ __forceinline__ float half_sum(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
 // Physical row of logical position j in a paged store (page size 2^log2_page).
 __device__ __forceinline__ int64_t phys_pos(const int32_t* __restrict__ table, int64_t j,
                                             int log2_page) {
   return ((int64_t)table[j >> log2_page] << log2_page) | (j & ((int64_t(1) << log2_page) - 1));
 }
+
+// Physical row of a wave-uniform logical position.  The page table is never
+// written while a kernel runs, so it is read through the constant address
+// space: the compiler then uses a scalar load, which does not wait behind the
+// vector-memory (DMA) loads in flight.
+__device__ __forceinline__ int64_t phys_pos_uniform(const int32_t* table, int64_t j, int log2_page) {
+  const __attribute__((address_space(4))) int32_t* t =
+      (const __attribute__((address_space(4))) int32_t*)table;
+  return ((int64_t)t[j >> log2_page] << log2_page) | (j & ((int64_t(1) << log2_page) - 1));
+}
+
+// Direct global->LDS loads of the key rows [t0, t0 + 32) of one KV head into
+// a tile (swizzled layout above).  Each wave writes rows 8w .. 8w+7 with four
+// 1 KiB instructions: lane l of instruction i carries row 8w + 2i + l/32,
+// physical chunk l % 32 (logical chunk (l % 32) ^ tile_swz(row)).  Rows at or
+// beyond k_hi repeat row k_hi - 1.  Completion is tracked by vmcnt.
+struct TileFetch {
+  const char* pool;    // pool base + KV head offset (bytes)
+  int64_t row_bytes;   // bytes between positions
+  int64_t lane_off[4]; // row * row_bytes + chunk * 16 for the lane's 4 rows
+  int lds_row[4];      // first LDS row written by instruction i
+  int lane_row[4];     // row carried by this lane in instruction i
+
+  __device__ __forceinline__ void init(const void* pool_head, int64_t pos_stride_elems, int lane,
+                                       int w) {
+    pool = static_cast<const char*>(pool_head);
+    row_bytes = pos_stride_elems * 2;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      lds_row[i] = 8 * w + 2 * i;
+      lane_row[i] = lds_row[i] + (lane >> 5);
+      lane_off[i] = ((lane & 31) ^ tile_swz(lane_row[i])) * 16;
+    }
+  }
+
+  // Whole tile inside one page, whose physical row for t0 is `prow` (wave-uniform).
+  __device__ __forceinline__ void issue_page(char* tile, int64_t prow) const {
+    const char* src = pool + prow * row_bytes;
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      __builtin_amdgcn_global_load_lds(src + lane_row[i] * row_bytes + lane_off[i],
+                                       LS_LDS(tile + lds_row[i] * kTileRow), 16, 0, 0);
+  }
+
+  // Any tile: one page-table lookup per row; rows at or beyond k_hi repeat k_hi - 1.
+  __device__ __forceinline__ void issue_rows(char* tile, const int32_t* __restrict__ table,
+                                             int log2_page, int64_t t0, int64_t k_hi) const {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      int64_t j = t0 + lane_row[i];
+      if (j >= k_hi) j = k_hi - 1;
+      __builtin_amdgcn_global_load_lds(pool + phys_pos(table, j, log2_page) * row_bytes + lane_off[i],
+                                       LS_LDS(tile + lds_row[i] * kTileRow), 16, 0, 0);
+    }
+  }
+};
+
+// Wait for this wave's direct loads (vmcnt = 0).
+__device__ __forceinline__ void wait_fetch() { __builtin_amdgcn_s_waitcnt(0x0F70); }
 
 }  // namespace ls
