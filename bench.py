@@ -45,9 +45,10 @@ def log(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
-def cpu_baseline(cfg, host, n_rows=4):
+def cpu_baseline(cfg, host, n_rows=16, n_shards=2):
     """The fp64 oracle as it stands, on this host's cores, over a bounded sample:
-    forward and dq of the first n_rows query rows (all heads) against the full prefix."""
+    forward and dq of the first n_rows query rows (all heads) against the first
+    n_shards prefix shards, the same paged store and page table as the GPU run."""
     import numpy as np
     import oracle as O
     try:
@@ -56,23 +57,24 @@ def cpu_baseline(cfg, host, n_rows=4):
     except Exception:  # pragma: no cover
         blas_threads = os.cpu_count() or 1
     rows = np.arange(n_rows)
+    b, e = cfg.shard_ranges()[0][0], cfg.shard_ranges()[n_shards - 1][1]
     kw = dict(page_size=cfg.page_size, q_pos0=cfg.q_pos0, scale=cfg.scale)
     t0 = time.perf_counter()
-    o, l = O.attn_fwd(host["q"], host["k_pool"], host["v_pool"], host["page_table"], rows=rows, **kw)
+    o, l = O.attn_fwd(host["q"], host["k_pool"], host["v_pool"], host["page_table"], rows=rows,
+                      kv_begin=b, kv_end=e, **kw)
     R, Hq, Dv = cfg.resp_len, cfg.n_q_heads, cfg.head_dim_v
     o_full = np.zeros((R, Hq, Dv))
     l_full = np.zeros((Hq, R))
     o_full[rows], l_full[:, rows] = o, l
     O.attn_bwd(host["q"], host["k_pool"], host["v_pool"], host["page_table"], host["d_out"],
                rows=rows, resp_keys=np.zeros(0, np.int64), out=o_full, lse=l_full,
-               prefix_len=cfg.prefix_len, **kw)
+               prefix_len=cfg.prefix_len, kv_begin=b, kv_end=e, **kw)
     dt = time.perf_counter() - t0
-    vis = sum(cfg.prefix_len + i + 1 for i in rows)
-    fl = (4 + 6) * Hq * cfg.head_dim * vis
+    fl = (4 + 6) * Hq * cfg.head_dim * n_rows * (e - b)
     return {"value": fl / dt / 1e12, "unit": "TFLOP/s", "cores": int(blas_threads),
             "kind": "oracle",
-            "sample": f"fp64 numpy oracle: forward + dq of query rows 0..{n_rows - 1} (all "
-                      f"{Hq} heads) over the full {cfg.kv_len}-key paged store; "
+            "sample": f"fp64 numpy oracle: split forward + dq of query rows 0..{n_rows - 1} "
+                      f"(all {Hq} heads) over prefix keys [{b}, {e}) of the paged store; "
                       f"{fl / 1e9:.1f} GFLOP in {dt:.1f} s",
             "seconds": dt}
 
@@ -84,7 +86,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--config", default="c3")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-rows", type=int, default=4)
+    ap.add_argument("--cpu-rows", type=int, default=16)
+    ap.add_argument("--calib-copy", action="store_true",
+                    help="run a 1 GiB device copy first (reference for rocprofv3 byte counters)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU: this build has no multi-GPU path "
@@ -109,6 +113,12 @@ def main():
     step = ReplayStep(cfg, dev, backward=True, stream=stream)
     fwd_fl, bwd_fl = flops(cfg)
 
+    if args.calib_copy:
+        src = torch.ones(1 << 28, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     for w in range(args.warmup):
         step.step()
         torch.cuda.synchronize()
@@ -155,9 +165,13 @@ def main():
     else:
         roof = {"kernel": "bwd_dq_bf16_d256_kernel (one 262,144-key shard per launch)",
                 "achieved": dq_tf, "flop_per_launch": dq_launch_fl, "avg_launch_ms": dq_launch_ms}
+    from paper_2607_14952_amd import profiling
+    kname = "fwd_bf16_d256_kernel" if fwd_total >= dq_total else "bwd_dq_bf16_d256_kernel"
+    traffic = profiling.traffic_for(kname, os.path.join(ROOT, "profiles", f"traffic_{cfg.name}.json"))
     roofline = {"bound": "mfma", "achieved": round(roof["achieved"], 2),
                 "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                "frac": round(roof["achieved"] / PEAK_BF16_TFLOPS, 4), "traffic": None,
+                "frac": round(roof["achieved"] / PEAK_BF16_TFLOPS, 4),
+                "traffic": None if traffic is None else round(traffic),
                 "kernel": roof["kernel"], "flop_per_launch": roof["flop_per_launch"],
                 "avg_launch_ms": round(roof["avg_launch_ms"], 3)}
     # merge bytes: split partials read + shard results written and re-read + output

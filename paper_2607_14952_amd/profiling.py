@@ -1,0 +1,199 @@
+"""Summaries of rocprofv3 output (kernel statistics and byte counters).
+
+Usage:
+  python -m paper_2607_14952_amd.profiling stats <rocprof dir> <out.md> --command "..."
+  python -m paper_2607_14952_amd.profiling traffic <FETCH_SIZE dir> <WRITE_SIZE dir> <out.json>
+         --calib-bytes N --command "..."
+
+`traffic` scales each kernel's per-dispatch FETCH_SIZE / WRITE_SIZE by what the
+same counter reads for the calibration copy kernel of known size, and records
+a hash of the kernel sources so that stale counters are not reported.
+"""
+from __future__ import annotations
+
+import argparse
+import csv
+import glob
+import hashlib
+import json
+import os
+from collections import defaultdict
+
+CSRC = os.path.join(os.path.dirname(os.path.abspath(__file__)), "csrc")
+COPY_KERNEL_HINT = "copy"
+
+
+def source_hash() -> str:
+    h = hashlib.sha256()
+    for path in sorted(glob.glob(os.path.join(CSRC, "*"))):
+        if path.endswith((".hip", ".h", ".cpp")):
+            h.update(os.path.basename(path).encode())
+            with open(path, "rb") as f:
+                h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def _median(xs):
+    if not xs:
+        return None
+    ys = sorted(xs)
+    n = len(ys)
+    return ys[n // 2] if n % 2 else 0.5 * (ys[n // 2 - 1] + ys[n // 2])
+
+
+def _find(directory: str, suffix: str):
+    return sorted(glob.glob(os.path.join(directory, "**", f"*{suffix}"), recursive=True))
+
+
+def _col(row: dict, *names):
+    for n in names:
+        if n in row and row[n] != "":
+            return row[n]
+    raise KeyError(f"none of {names} in {list(row)}")
+
+
+def kernel_stats(directory: str):
+    files = _find(directory, "kernel_stats.csv")
+    if not files:
+        raise FileNotFoundError(f"no kernel_stats.csv under {directory}")
+    out = []
+    with open(files[0]) as f:
+        for row in csv.DictReader(f):
+            out.append(dict(name=_col(row, "Name", "KernelName", "Kernel_Name"),
+                            calls=int(_col(row, "Calls")),
+                            total_ns=float(_col(row, "TotalDurationNs")),
+                            avg_ns=float(_col(row, "AverageNs")),
+                            min_ns=float(_col(row, "MinNs")),
+                            max_ns=float(_col(row, "MaxNs")),
+                            pct=float(_col(row, "Percentage"))))
+    return out
+
+
+def dispatch_medians(directory: str):
+    """kernel name -> median dispatch duration (ns) from the kernel trace."""
+    files = _find(directory, "kernel_trace.csv")
+    if not files:
+        return {}
+    per = defaultdict(list)
+    with open(files[0]) as f:
+        for row in csv.DictReader(f):
+            name = _col(row, "Kernel_Name", "KernelName", "Name")
+            t = float(_col(row, "End_Timestamp")) - float(_col(row, "Start_Timestamp"))
+            per[name].append(t)
+    return {k: _median(v) for k, v in per.items()}
+
+
+def write_stats_md(directory: str, out_path: str, command: str, title: str) -> None:
+    rows = kernel_stats(directory)
+    med = dispatch_medians(directory)
+    lines = [f"# {title}", "", "Command (run from the repository root on one MI355X):", "",
+             "```", command, "```", "",
+             f"Kernel sources: `{source_hash()}` (sha256/16 of `paper_2607_14952_amd/csrc`).", "",
+             "| kernel | calls | avg ms | median ms | min ms | max ms | total ms | % |",
+             "|---|---:|---:|---:|---:|---:|---:|---:|"]
+    for r in sorted(rows, key=lambda r: -r["total_ns"]):
+        m = med.get(r["name"])
+        ms = f"{m / 1e6:.3f}" if m is not None else "-"
+        lines.append(f"| `{r['name'][:110]}` | {r['calls']} | {r['avg_ns'] / 1e6:.3f} | {ms} | "
+                     f"{r['min_ns'] / 1e6:.3f} | {r['max_ns'] / 1e6:.3f} | "
+                     f"{r['total_ns'] / 1e6:.2f} | {r['pct']:.2f} |")
+    with open(out_path, "w") as f:
+        f.write("\n".join(lines) + "\n")
+
+
+def counter_per_dispatch(directory: str, counter: str):
+    """kernel name -> list of per-dispatch counter values."""
+    files = _find(directory, "counter_collection.csv")
+    if not files:
+        raise FileNotFoundError(f"no counter_collection.csv under {directory}")
+    per = defaultdict(float)
+    names = {}
+    with open(files[0]) as f:
+        for row in csv.DictReader(f):
+            if _col(row, "Counter_Name", "CounterName") != counter:
+                continue
+            d = _col(row, "Dispatch_Id", "DispatchId", "Correlation_Id")
+            per[d] += float(_col(row, "Counter_Value", "CounterValue"))
+            names[d] = _col(row, "Kernel_Name", "KernelName", "Name")
+    out = defaultdict(list)
+    for d, v in per.items():
+        out[names[d]].append(v)
+    return out
+
+
+def write_traffic(fetch_dir: str, write_dir: str, out_path: str, calib_bytes: int,
+                  command: str) -> dict:
+    fetch = counter_per_dispatch(fetch_dir, "FETCH_SIZE")
+    write = counter_per_dispatch(write_dir, "WRITE_SIZE")
+
+    def calib(per):
+        cands = [(k, v) for k, v in per.items() if COPY_KERNEL_HINT in k.lower()]
+        if not cands:
+            raise RuntimeError("calibration copy kernel not found in the counter output")
+        k, v = max(cands, key=lambda kv: max(kv[1]))
+        return k, max(v)
+
+    ck_f, cf = calib(fetch)
+    ck_w, cw = calib(write)
+    scale_f = calib_bytes / (cf * 1024.0)
+    scale_w = calib_bytes / (cw * 1024.0)
+    kernels = {}
+    for name in sorted(set(fetch) | set(write)):
+        f = fetch.get(name, [])
+        w = write.get(name, [])
+        mf, mw = _median(f), _median(w)
+        kernels[name] = {
+            "dispatches": max(len(f), len(w)),
+            "fetch_kib_per_dispatch_median": mf,
+            "write_kib_per_dispatch_median": mw,
+            "fetch_kib_per_dispatch": f,
+            "write_kib_per_dispatch": w,
+            "hbm_bytes_per_dispatch": (mf or 0.0) * 1024 * scale_f + (mw or 0.0) * 1024 * scale_w,
+        }
+    doc = {"command": command, "source_hash": source_hash(), "calib_bytes": calib_bytes,
+           "calib_kernel": {"fetch": ck_f, "write": ck_w},
+           "calib_counter_kib": {"FETCH_SIZE": cf, "WRITE_SIZE": cw},
+           "scale": {"FETCH_SIZE": scale_f, "WRITE_SIZE": scale_w}, "kernels": kernels}
+    with open(out_path, "w") as fo:
+        json.dump(doc, fo, indent=1)
+    return doc
+
+
+def traffic_for(kernel_substr: str, path: str):
+    """HBM bytes per dispatch of the first kernel matching kernel_substr, or None
+    when the file is missing or was taken from other kernel sources."""
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        doc = json.load(f)
+    if doc.get("source_hash") != source_hash():
+        return None
+    for name, v in doc["kernels"].items():
+        if kernel_substr in name:
+            return v["hbm_bytes_per_dispatch"]
+    return None
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    sub = ap.add_subparsers(dest="cmd", required=True)
+    a = sub.add_parser("stats")
+    a.add_argument("directory")
+    a.add_argument("out")
+    a.add_argument("--command", required=True)
+    a.add_argument("--title", default="rocprofv3 kernel statistics")
+    b = sub.add_parser("traffic")
+    b.add_argument("fetch_dir")
+    b.add_argument("write_dir")
+    b.add_argument("out")
+    b.add_argument("--calib-bytes", type=int, required=True)
+    b.add_argument("--command", required=True)
+    args = ap.parse_args()
+    if args.cmd == "stats":
+        write_stats_md(args.directory, args.out, args.command, args.title)
+    else:
+        write_traffic(args.fetch_dir, args.write_dir, args.out, args.calib_bytes, args.command)
+
+
+if __name__ == "__main__":
+    main()
