@@ -79,6 +79,47 @@ def cpu_baseline(cfg, host, n_rows=16, n_shards=2):
             "seconds": dt}
 
 
+def run_blockwise(cfg, args):
+    """G members replayed blockwise (reverse 2,048-row blocks) against one resident
+    prefix; every member appends its response pages and pops them afterwards."""
+    import torch
+    from paper_2607_14952_amd import inputs
+    from paper_2607_14952_amd.blockwise import BlockwiseReplay, ResidentPrefix, block_flops
+    from paper_2607_14952_amd.replay import to_device
+    log(f"generating the resident prefix for {cfg.name}")
+    store = inputs.prefix_store(cfg)
+    prefix = ResidentPrefix(cfg, store)
+    del store
+    members = []
+    for m in range(cfg.members):
+        r = inputs.response_inputs(cfg, m)
+        members.append({k: to_device(v) for k, v in r.items()})
+    rep = BlockwiseReplay(cfg, prefix)
+    fl = sum(sum(block_flops(cfg, b)) for b in range(cfg.blocks)) * cfg.members
+    for w in range(args.warmup):
+        rep.run_member(members[0])
+        torch.cuda.synchronize()
+        log(f"warmup {w + 1}/{args.warmup} done")
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for m in range(cfg.members):
+        rep.run_member(members[m])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    value = fl / wall / 1e12
+    print(json.dumps({
+        "metric": "replay attention TFLOP/s (fwd+bwd), G blockwise members on a resident prefix",
+        "value": round(value, 2), "unit": "TFLOP/s", "n_gpus": 1, "steps": 1,
+        "warmup": args.warmup, "ms_per_step": round(wall * 1e3, 1), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": f"{cfg.name}: {cfg.members} members x {cfg.resp_len} tokens in "
+                               f"{cfg.rows_per_call}-row reverse blocks, prefix {cfg.prefix_len} "
+                               f"in a {cfg.n_phys_pages}-page pool (sampled, with free pages)",
+                   "parallelism": "single-gpu"},
+        "frac_of_peak": round(value / PEAK_BF16_TFLOPS, 4), "flop_per_step": fl,
+        "gpu": torch.cuda.get_device_name(0)}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -104,6 +145,9 @@ def main():
         print("no GPU visible", file=sys.stderr)
         sys.exit(1)
     cfg = configs.get(args.config)
+    if cfg.members > 1:
+        run_blockwise(cfg, args)
+        return
     log(f"generating inputs for {cfg.name}")
     t = time.perf_counter()
     host = inputs.dense_inputs(cfg)

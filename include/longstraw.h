@@ -13,7 +13,8 @@
  *   - Every pointer argument named as device memory is a device address owned
  *     by the caller; the library allocates nothing and keeps no reference after
  *     a call returns.  Host arrays (splits) are read before the call returns.
- *   - Pools and the page table are read-only to the library.
+ *   - Pools and the page table are read-only to the library, except that
+ *     ls_scatter_kv writes the pools.
  *   - All device pointers must be 16-byte aligned.
  *   - Calls are asynchronous and ordered on `stream` (a hipStream_t passed as
  *     void*, NULL = the null stream).  Only LS_FLAG_CHECKED synchronizes.
@@ -121,6 +122,20 @@ const char* ls_last_error(void);
  */
 ls_status ls_gather_kv(const ls_attn_params* p, int64_t pos_begin, int64_t pos_end,
                        void* k_out, void* v_out, void* stream);
+
+/*
+ * ls_scatter_kv: write dense rows k_src [n, n_kv_heads, head_dim] and
+ * v_src [n, n_kv_heads, head_dim_v] (device, dtype) into logical positions
+ * [pos_begin, pos_end) of the paged store, i.e. into physical page
+ * page_table[j / page_size], slot j % page_size (n = pos_end - pos_begin).
+ * This is the append step of a response branch (its K/V pages are added to
+ * the shared store and popped afterwards; Sec. "Four-Block Response Replay"):
+ * unlike every other call it WRITES p->k_pool and p->v_pool.  The prefix
+ * pages must not be targeted; the library does not check which pages the
+ * table names beyond LS_FLAG_CHECKED's range check.  Bit-exact copy.
+ */
+ls_status ls_scatter_kv(const ls_attn_params* p, int64_t pos_begin, int64_t pos_end,
+                        const void* k_src, const void* v_src, void* stream);
 
 /*
  * ls_prefix_attn_fwd: for every split r and row i, the normalized local

@@ -20,7 +20,7 @@ FLAG_ACCUMULATE_DQ = 4
 FLAG_ACCUMULATE_DKV = 8
 STATUS = {0: "LS_OK", -1: "LS_ERR_INVALID_ARG", -2: "LS_ERR_UNSUPPORTED", -3: "LS_ERR_WORKSPACE",
           -4: "LS_ERR_ALIAS", -5: "LS_ERR_STALE", -6: "LS_ERR_PAGE_OOB", -7: "LS_ERR_HIP"}
-EXPORTS = ["ls_abi_version", "ls_status_string", "ls_last_error", "ls_gather_kv",
+EXPORTS = ["ls_abi_version", "ls_status_string", "ls_last_error", "ls_gather_kv", "ls_scatter_kv",
            "ls_prefix_attn_fwd", "ls_lse_merge", "ls_prefix_attn_bwd_workspace_size",
            "ls_prefix_attn_bwd"]
 
@@ -65,6 +65,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.ls_last_error.restype = ctypes.c_char_p
     lib.ls_gather_kv.restype = c_int32
     lib.ls_gather_kv.argtypes = [P, c_int64, c_int64, c_void_p, c_void_p, c_void_p]
+    lib.ls_scatter_kv.restype = c_int32
+    lib.ls_scatter_kv.argtypes = [P, c_int64, c_int64, c_void_p, c_void_p, c_void_p]
     lib.ls_prefix_attn_fwd.restype = c_int32
     lib.ls_prefix_attn_fwd.argtypes = [P, POINTER(Split), c_int32, c_void_p, c_void_p, c_void_p]
     lib.ls_lse_merge.restype = c_int32
@@ -164,6 +166,19 @@ def gather_kv(kv: PagedKV, pos_begin: int, pos_end: int, *, flags: int = 0, stre
     check(load_library().ls_gather_kv(ctypes.byref(p), pos_begin, pos_end, _ptr(k), _ptr(v),
                                       _stream(stream)))
     return k, v
+
+
+def scatter_kv(kv: PagedKV, pos_begin: int, k_src, v_src, *, flags: int = 0, stream=None):
+    """ls_scatter_kv: write dense rows into logical positions [pos_begin, pos_begin + n)
+    of the paged store (the append step of a response branch)."""
+    torch = _torch()
+    n = k_src.shape[0]
+    dummy_q = torch.empty((0, 1, 1), dtype=kv.k_pool.dtype, device=kv.k_pool.device)
+    p = make_params(dummy_q, kv, n_q=0, n_q_heads=kv.k_pool.shape[2], prefix_len=0, q_pos0=0,
+                    scale=1.0, flags=flags)
+    p.q = None
+    check(load_library().ls_scatter_kv(ctypes.byref(p), pos_begin, pos_begin + n, _ptr(k_src),
+                                       _ptr(v_src), _stream(stream)))
 
 
 def prefix_attn_fwd(q, kv: PagedKV, splits, *, prefix_len: int, q_pos0: int, scale: float,

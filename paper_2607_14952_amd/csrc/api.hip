@@ -220,6 +220,42 @@ LS_API ls_status ls_gather_kv(const ls_attn_params* p, int64_t pos_begin, int64_
   return e == hipSuccess ? LS_OK : hip_fail(e, "gather launch");
 }
 
+LS_API ls_status ls_scatter_kv(const ls_attn_params* p, int64_t pos_begin, int64_t pos_end,
+                               const void* k_src, const void* v_src, void* stream) {
+  ls_status st = check_params(p, false);
+  if (st != LS_OK) return st;
+  if (!is_pow2(p->page_size))
+    return fail(LS_ERR_UNSUPPORTED, "page_size %d is not a power of two", p->page_size);
+  if (pos_begin < 0 || pos_end < pos_begin ||
+      pos_end > p->n_logical_pages * (int64_t)p->page_size)
+    return fail(LS_ERR_INVALID_ARG, "positions [%lld, %lld) outside the logical store",
+                (long long)pos_begin, (long long)pos_end);
+  int64_t n = pos_end - pos_begin;
+  if (n == 0) return LS_OK;
+  if (!k_src || !v_src || !aligned16(k_src) || !aligned16(v_src))
+    return fail(LS_ERR_INVALID_ARG, "k_src/v_src must be non-NULL and 16-byte aligned");
+  size_t es = esize(p->dtype);
+  int64_t krow = (int64_t)p->n_kv_heads * p->head_dim, vrow = (int64_t)p->n_kv_heads * p->head_dim_v;
+  if ((krow * (int64_t)es) % 16 || (vrow * (int64_t)es) % 16)
+    return fail(LS_ERR_UNSUPPORTED, "position rows must be a multiple of 16 bytes");
+  // the pools are the outputs here; the sources and the table must not overlap them
+  std::vector<Range> ins, outs;
+  size_t pk = (size_t)p->n_phys_pages * p->page_size * krow * es;
+  size_t pv = (size_t)p->n_phys_pages * p->page_size * vrow * es;
+  outs.push_back(rng("k_pool", p->k_pool, pk));
+  outs.push_back(rng("v_pool", p->v_pool, pv));
+  ins.push_back(rng("page_table", p->page_table, (size_t)p->n_logical_pages * 4));
+  ins.push_back(rng("k_src", k_src, (size_t)(n * krow) * es));
+  ins.push_back(rng("v_src", v_src, (size_t)(n * vrow) * es));
+  if ((st = check_alias(outs, ins)) != LS_OK) return st;
+  hipStream_t s = (hipStream_t)stream;
+  if ((st = check_pages(p, pos_end, s)) != LS_OK) return st;
+  hipError_t e = ls::launch_scatter(const_cast<void*>(p->k_pool), const_cast<void*>(p->v_pool),
+                                    p->page_table, pos_begin, pos_end, ilog2(p->page_size), krow,
+                                    vrow, (int)es, k_src, v_src, s);
+  return e == hipSuccess ? LS_OK : hip_fail(e, "scatter launch");
+}
+
 LS_API ls_status ls_prefix_attn_fwd(const ls_attn_params* p, const ls_split* splits,
                                     int32_t n_splits, float* out_part, float* lse_part,
                                     void* stream) {

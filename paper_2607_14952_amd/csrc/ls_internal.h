@@ -60,6 +60,10 @@ hipError_t launch_gather(const void* k_pool, const void* v_pool, const int32_t* 
                          int64_t pos_begin, int64_t pos_end, int log2_page, int64_t k_row_elems,
                          int64_t v_row_elems, int esize, void* k_out, void* v_out,
                          hipStream_t stream);
+hipError_t launch_scatter(void* k_pool, void* v_pool, const int32_t* page_table,
+                          int64_t pos_begin, int64_t pos_end, int log2_page, int64_t k_row_elems,
+                          int64_t v_row_elems, int esize, const void* k_src, const void* v_src,
+                          hipStream_t stream);
 hipError_t launch_merge(const float* out_part, const float* lse_part, int n_splits, int n_q,
                         int n_heads, int dv, bool out_bf16, void* out, float* lse,
                         hipStream_t stream);

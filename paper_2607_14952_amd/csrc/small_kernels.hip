@@ -39,6 +39,32 @@ __global__ __launch_bounds__(256) void gather_kernel(const char* __restrict__ k_
   }
 }
 
+// Inverse of the gather: dense rows -> their logical positions in the pool.
+__global__ __launch_bounds__(256) void scatter_kernel(char* __restrict__ k_pool,
+                                                      char* __restrict__ v_pool,
+                                                      const int32_t* __restrict__ page_table,
+                                                      int64_t pos_begin, int64_t n, int log2_page,
+                                                      int64_t k_row_bytes, int64_t v_row_bytes,
+                                                      const char* __restrict__ k_src,
+                                                      const char* __restrict__ v_src) {
+  const bool is_v = blockIdx.y == 1;
+  char* pool = is_v ? v_pool : k_pool;
+  const char* src = is_v ? v_src : k_src;
+  const int64_t row_bytes = is_v ? v_row_bytes : k_row_bytes;
+  const int64_t units = row_bytes >> 4;
+  const int64_t total = n * units;
+  const int64_t S = int64_t(1) << log2_page;
+  for (int64_t u = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; u < total;
+       u += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t r = u / units, c = u - r * units;
+    const int64_t j = pos_begin + r;
+    const int64_t page = page_table[j >> log2_page];
+    const int64_t phys_row = page * S + (j & (S - 1));
+    *reinterpret_cast<u32x4*>(pool + phys_row * row_bytes + c * 16) =
+        *reinterpret_cast<const u32x4*>(src + r * row_bytes + c * 16);
+  }
+}
+
 // ---------------------------------------------------------------- merge
 // One thread per 4 output values of one (row, head).  Eq. qwen-lse-parts:
 // m = max l_r, a = sum e^(l_r - m), n = sum e^(l_r - m) o_r; o = n / a,
@@ -122,6 +148,21 @@ hipError_t launch_gather(const void* k_pool, const void* v_pool, const int32_t* 
   hipLaunchKernelGGL(gather_kernel, dim3((unsigned)blocks, 2), dim3(256), 0, stream,
                      (const char*)k_pool, (const char*)v_pool, page_table, pos_begin, n, log2_page,
                      k_row_elems * esize, v_row_elems * esize, (char*)k_out, (char*)v_out);
+  return hipGetLastError();
+}
+
+hipError_t launch_scatter(void* k_pool, void* v_pool, const int32_t* page_table,
+                          int64_t pos_begin, int64_t pos_end, int log2_page, int64_t k_row_elems,
+                          int64_t v_row_elems, int esize, const void* k_src, const void* v_src,
+                          hipStream_t stream) {
+  const int64_t n = pos_end - pos_begin;
+  const int64_t units = n * ((k_row_elems > v_row_elems ? k_row_elems : v_row_elems) * esize / 16);
+  int64_t blocks = (units + 255) / 256;
+  if (blocks > 65536) blocks = 65536;
+  hipLaunchKernelGGL(scatter_kernel, dim3((unsigned)blocks, 2), dim3(256), 0, stream,
+                     (char*)k_pool, (char*)v_pool, page_table, pos_begin, n, log2_page,
+                     k_row_elems * esize, v_row_elems * esize, (const char*)k_src,
+                     (const char*)v_src);
   return hipGetLastError();
 }
 

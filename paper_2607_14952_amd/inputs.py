@@ -193,3 +193,38 @@ def sparse_inputs(cfg, with_dout: bool = True) -> dict:
     if with_dout:
         out["d_out"] = _dense_tensor(cfg, STREAM_DO, (R, H, cfg.head_dim_v))
     return out
+
+
+# ---------------------------------------------------------------- resident prefix + responses
+def member_seed(cfg, member: int) -> int:
+    """Seed of response `member` replayed against a shared prefix (config seed s -> 1000*s + m)."""
+    return 1000 * cfg.seed + member
+
+
+def prefix_store(cfg) -> dict:
+    """Pools [n_phys, S, Hkv, D|Dv] and the prefix part of the page table
+    ([n_prefix_pages] int32); physical pages not named by it form the free list
+    (ascending) from which response pages are appended."""
+    table = page_table(cfg, n_logical=cfg.n_prefix_pages)
+    k_pool = _pool(cfg, STREAM_K, cfg.head_dim, cfg.n_kv_heads)
+    v_pool = _pool(cfg, STREAM_V, cfg.head_dim_v, cfg.n_kv_heads)
+    used = np.zeros(cfg.n_phys_pages, dtype=bool)
+    used[table] = True
+    return dict(k_pool=k_pool, v_pool=v_pool, prefix_table=table,
+                free_pages=np.flatnonzero(~used).astype(np.int32))
+
+
+def response_inputs(cfg, member: int) -> dict:
+    """One response branch: q [R,Hq,D], its own K/V rows k [R,Hkv,D], v [R,Hkv,Dv]
+    and d_out [R,Hq,Dv], drawn from the member's seed."""
+    s = member_seed(cfg, member)
+    R = cfg.resp_len
+
+    def draw(stream, shape):
+        x = normal_chunks(s, stream, int(np.prod(shape))).reshape(shape)
+        return to_bf16_bits(x) if cfg.dtype == "bf16" else x
+
+    return dict(q=draw(STREAM_Q, (R, cfg.n_q_heads, cfg.head_dim)),
+                k=draw(STREAM_K, (R, cfg.n_kv_heads, cfg.head_dim)),
+                v=draw(STREAM_V, (R, cfg.n_kv_heads, cfg.head_dim_v)),
+                d_out=draw(STREAM_DO, (R, cfg.n_q_heads, cfg.head_dim_v)))

@@ -155,3 +155,14 @@ def test_gather_rejects():
     assert lib.ls_gather_kv(ctypes.byref(p), 0, 64 * 256 + 1, FAKE * 300, FAKE * 400, None) == -1
     assert lib.ls_gather_kv(ctypes.byref(p), 0, 16, FAKE * 64, FAKE * 400, None) == -4
     assert lib.ls_gather_kv(ctypes.byref(p), 0, 0, FAKE * 300, FAKE * 400, None) == 0
+
+
+def test_scatter_rejects():
+    lib = B.load_library()
+    p = good_params(n_q=0)
+    # source overlapping the K pool, bad ranges
+    assert lib.ls_scatter_kv(ctypes.byref(p), 0, 16, FAKE * 64, FAKE * 400, None) == -4
+    assert lib.ls_scatter_kv(ctypes.byref(p), 10, 5, FAKE * 300, FAKE * 400, None) == -1
+    assert lib.ls_scatter_kv(ctypes.byref(p), 0, 64 * 256 + 1, FAKE * 300, FAKE * 400, None) == -1
+    assert lib.ls_scatter_kv(ctypes.byref(p), 0, 0, FAKE * 300, FAKE * 400, None) == 0
+    assert lib.ls_scatter_kv(ctypes.byref(p), 0, 16, 0, FAKE * 400, None) == -1
