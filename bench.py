@@ -120,6 +120,74 @@ def run_blockwise(cfg, args):
         "gpu": torch.cuda.get_device_name(0)}), flush=True)
 
 
+def run_sparse(cfg, args):
+    """Sparse latent replay (MLA keys, DSA-style top-k selection + response window):
+    forward and dq backward over all response rows."""
+    import torch
+    from paper_2607_14952_amd import binding as B
+    from paper_2607_14952_amd import inputs
+    from paper_2607_14952_amd.replay import to_device
+    log(f"generating inputs for {cfg.name}")
+    h = inputs.sparse_inputs(cfg)
+    q = to_device(h["q"])
+    lat = to_device(h["latent_pool"])
+    kv = B.PagedKV(lat, lat, to_device(h["page_table"]))
+    idx = to_device(h["idx"])
+    d_out = to_device(h["d_out"])
+    del h
+    kw = dict(prefix_len=cfg.prefix_len, q_pos0=cfg.q_pos0, scale=cfg.scale)
+    ws = B.sparse_workspace(q, kv, cfg.topk, backward=True, prefix_len=cfg.prefix_len,
+                            q_pos0=cfg.q_pos0)
+    out = torch.empty((cfg.resp_len, cfg.n_q_heads, 512), dtype=torch.float32, device="cuda")
+    lse = torch.empty((cfg.n_q_heads, cfg.resp_len), dtype=torch.float32, device="cuda")
+    out_b = torch.empty((cfg.resp_len, cfg.n_q_heads, 512), dtype=torch.bfloat16, device="cuda")
+    dq = torch.empty((cfg.resp_len, cfg.n_q_heads, 576), dtype=torch.float32, device="cuda")
+
+    def step(ev=None):
+        if ev:
+            ev[0].record()
+        B.sparse_attn_fwd(q, kv, idx, out=out, lse=lse, workspace=ws, **kw)
+        if ev:
+            ev[1].record()
+        B.lse_merge(out.view(1, *out.shape), lse.view(1, *lse.shape), out=out_b,
+                    lse=torch.empty_like(lse))
+        B.sparse_attn_bwd(q, kv, idx, d_out, out_b, lse, dq=dq, workspace=ws, **kw)
+        if ev:
+            ev[2].record()
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+    t0 = time.perf_counter()
+    for s in range(args.steps):
+        step(evs[s])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    R, H = cfg.resp_len, cfg.n_q_heads
+    vis = R * cfg.topk + R * (R + 1) // 2
+    fwd_fl = 2 * H * (576 + 512) * vis
+    bwd_fl = 2 * H * (576 + 512 + 576) * vis
+    gathered = vis * 1152
+    fwd_ms = sum(e[0].elapsed_time(e[1]) for e in evs) / args.steps
+    bwd_ms = sum(e[1].elapsed_time(e[2]) for e in evs) / args.steps
+    ms = wall * 1e3 / args.steps
+    print(json.dumps({
+        "metric": "sparse latent replay TFLOP/s (fwd+bwd dq), MLA 576/512 with top-k selection",
+        "value": round((fwd_fl + bwd_fl) / (ms * 1e-3) / 1e12, 2), "unit": "TFLOP/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 3),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": f"{cfg.name}: {H} heads sharing one 576-wide latent row, prefix "
+                               f"{cfg.prefix_len} in {cfg.page_size}-entry pages, {R} tokens x "
+                               f"top-{cfg.topk} + causal window", "parallelism": "single-gpu"},
+        "fwd_ms": round(fwd_ms, 3), "fwd_tflops": round(fwd_fl / (fwd_ms * 1e-3) / 1e12, 2),
+        "fwd_gather_gbs": round(gathered / (fwd_ms * 1e-3) / 1e9, 1),
+        "bwd_ms": round(bwd_ms, 3), "bwd_tflops": round(bwd_fl / (bwd_ms * 1e-3) / 1e12, 2),
+        "flop_per_step": {"fwd": fwd_fl, "bwd": bwd_fl}, "gpu": torch.cuda.get_device_name(0)}),
+        flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -147,6 +215,9 @@ def main():
     cfg = configs.get(args.config)
     if cfg.members > 1:
         run_blockwise(cfg, args)
+        return
+    if cfg.sparse:
+        run_sparse(cfg, args)
         return
     log(f"generating inputs for {cfg.name}")
     t = time.perf_counter()

@@ -191,6 +191,32 @@ ls_status ls_prefix_attn_bwd(const ls_attn_params* p, int64_t kv_begin, int64_t 
                              const float* lse, float* dq, float* dk_resp, float* dv_resp,
                              void* workspace, size_t workspace_bytes, void* stream);
 
+/*
+ * Sparse latent replay (MLA keys with a DSA-style selection; Eq. dsa-attention,
+ * Sec. "Layer Anatomy: MLA/DSA Before Dense or Routed FFNs"): one latent row of
+ * head_dim = 576 bf16 per position (n_kv_heads = 1, v_pool == k_pool); keys are
+ * the whole row and values its first head_dim_v = 512 channels.  Query row t
+ * (position q_pos0 + t) of every head attends to the prefix positions
+ * idx[t][0 .. topk) (distinct, inside [0, prefix_len); int32 device array
+ * [n_q, topk]) and to the response positions prefix_len .. q_pos0 + t.
+ * n_q_heads must be a multiple of 128.  Positions outside the store are
+ * clamped; duplicated or out-of-range indices are the caller's error
+ * (LS_FLAG_CHECKED range-checks them on the host).
+ */
+size_t ls_sparse_attn_workspace_size(const ls_attn_params* p, int32_t topk, int32_t backward);
+
+/* out [n_q, n_q_heads, 512] fp32 (normalized), lse [n_q_heads, n_q] fp32 (natural log). */
+ls_status ls_sparse_attn_fwd(const ls_attn_params* p, const int32_t* idx, int32_t topk,
+                             float* out, float* lse, void* workspace, size_t workspace_bytes,
+                             void* stream);
+
+/* dq [n_q, n_q_heads, 576] fp32 of L = sum(d_out * out) (d_out bf16 [n_q, H, 512]);
+ * the latent rows get no gradient.  LS_FLAG_ACCUMULATE_DQ adds into dq. */
+ls_status ls_sparse_attn_bwd(const ls_attn_params* p, const int32_t* idx, int32_t topk,
+                             const void* d_out, const void* out, int32_t out_dtype,
+                             const float* lse, float* dq, void* workspace,
+                             size_t workspace_bytes, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -22,7 +22,8 @@ STATUS = {0: "LS_OK", -1: "LS_ERR_INVALID_ARG", -2: "LS_ERR_UNSUPPORTED", -3: "L
           -4: "LS_ERR_ALIAS", -5: "LS_ERR_STALE", -6: "LS_ERR_PAGE_OOB", -7: "LS_ERR_HIP"}
 EXPORTS = ["ls_abi_version", "ls_status_string", "ls_last_error", "ls_gather_kv", "ls_scatter_kv",
            "ls_prefix_attn_fwd", "ls_lse_merge", "ls_prefix_attn_bwd_workspace_size",
-           "ls_prefix_attn_bwd"]
+           "ls_prefix_attn_bwd", "ls_sparse_attn_workspace_size", "ls_sparse_attn_fwd",
+           "ls_sparse_attn_bwd"]
 
 
 class AttnParams(ctypes.Structure):
@@ -77,6 +78,14 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.ls_prefix_attn_bwd.restype = c_int32
     lib.ls_prefix_attn_bwd.argtypes = [P, c_int64, c_int64, c_void_p, c_void_p, c_int32, c_void_p,
                                        c_void_p, c_void_p, c_void_p, c_void_p, c_size_t, c_void_p]
+    lib.ls_sparse_attn_workspace_size.restype = c_size_t
+    lib.ls_sparse_attn_workspace_size.argtypes = [P, c_int32, c_int32]
+    lib.ls_sparse_attn_fwd.restype = c_int32
+    lib.ls_sparse_attn_fwd.argtypes = [P, c_void_p, c_int32, c_void_p, c_void_p, c_void_p,
+                                       c_size_t, c_void_p]
+    lib.ls_sparse_attn_bwd.restype = c_int32
+    lib.ls_sparse_attn_bwd.argtypes = [P, c_void_p, c_int32, c_void_p, c_void_p, c_int32, c_void_p,
+                                       c_void_p, c_void_p, c_size_t, c_void_p]
     if lib.ls_abi_version() != ABI_VERSION:
         raise RuntimeError("liblongstraw ABI version mismatch")
     _lib = lib
@@ -253,3 +262,57 @@ def prefix_attn_bwd(q, kv: PagedKV, d_out, out, lse, *, prefix_len: int, q_pos0:
         _ptr(dq), _ptr(dk_resp), _ptr(dv_resp), _ptr(workspace), workspace.numel(),
         _stream(stream)))
     return dq, dk_resp, dv_resp
+
+
+# ----------------------------------------------------------------- sparse latent replay
+def _sparse_params(q, latent: PagedKV, *, prefix_len, q_pos0, scale, flags=0):
+    p = make_params(q, latent, prefix_len=prefix_len, q_pos0=q_pos0, scale=scale, flags=flags)
+    p.head_dim_v = 512
+    return p
+
+
+def sparse_workspace(q, latent: PagedKV, topk: int, *, prefix_len: int, q_pos0: int,
+                     backward: bool):
+    torch = _torch()
+    p = _sparse_params(q, latent, prefix_len=prefix_len, q_pos0=q_pos0, scale=1.0)
+    n = load_library().ls_sparse_attn_workspace_size(ctypes.byref(p), topk, int(backward))
+    return torch.empty(max(n, 16), dtype=torch.uint8, device=q.device)
+
+
+def sparse_attn_fwd(q, latent: PagedKV, idx, *, prefix_len: int, q_pos0: int, scale: float,
+                    flags: int = 0, out=None, lse=None, workspace=None, stream=None):
+    """ls_sparse_attn_fwd: out [R, H, 512] fp32, lse [H, R] fp32.  `latent` holds the
+    latent pool as both k_pool and v_pool."""
+    torch = _torch()
+    R, H = q.shape[0], q.shape[1]
+    topk = 0 if idx is None else idx.shape[1]
+    if out is None:
+        out = torch.empty((R, H, 512), dtype=torch.float32, device=q.device)
+    if lse is None:
+        lse = torch.empty((H, R), dtype=torch.float32, device=q.device)
+    if workspace is None:
+        workspace = sparse_workspace(q, latent, topk, prefix_len=prefix_len, q_pos0=q_pos0,
+                                     backward=False)
+    p = _sparse_params(q, latent, prefix_len=prefix_len, q_pos0=q_pos0, scale=scale, flags=flags)
+    check(load_library().ls_sparse_attn_fwd(ctypes.byref(p), _ptr(idx), topk, _ptr(out),
+                                            _ptr(lse), _ptr(workspace), workspace.numel(),
+                                            _stream(stream)))
+    return out, lse
+
+
+def sparse_attn_bwd(q, latent: PagedKV, idx, d_out, out, lse, *, prefix_len: int, q_pos0: int,
+                    scale: float, flags: int = 0, dq=None, workspace=None, stream=None):
+    """ls_sparse_attn_bwd: dq [R, H, 576] fp32."""
+    torch = _torch()
+    R, H = q.shape[0], q.shape[1]
+    topk = 0 if idx is None else idx.shape[1]
+    if dq is None:
+        dq = torch.empty((R, H, 576), dtype=torch.float32, device=q.device)
+    if workspace is None:
+        workspace = sparse_workspace(q, latent, topk, prefix_len=prefix_len, q_pos0=q_pos0,
+                                     backward=True)
+    p = _sparse_params(q, latent, prefix_len=prefix_len, q_pos0=q_pos0, scale=scale, flags=flags)
+    check(load_library().ls_sparse_attn_bwd(ctypes.byref(p), _ptr(idx), topk, _ptr(d_out),
+                                            _ptr(out), _dtype_code(out), _ptr(lse), _ptr(dq),
+                                            _ptr(workspace), workspace.numel(), _stream(stream)))
+    return dq

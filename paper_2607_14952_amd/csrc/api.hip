@@ -421,3 +421,164 @@ LS_API ls_status ls_prefix_attn_bwd(const ls_attn_params* p, int64_t kv_begin, i
                           : ls::launch_bwd_f32(a, true, has_resp, s);
   return e == hipSuccess ? LS_OK : hip_fail(e, "backward launch");
 }
+
+// ---------------------------------------------------------------- sparse latent replay
+namespace {
+
+struct SparseLayout {
+  int64_t n_max;      // key-list length padded to a whole 32-key tile
+  size_t phys_bytes, stat_bytes, ds_bytes;
+  size_t fwd_bytes() const { return phys_bytes; }
+  size_t bwd_bytes() const { return phys_bytes + 2 * stat_bytes + ds_bytes; }
+};
+
+size_t pad256(size_t x) { return (x + 255) / 256 * 256; }
+
+SparseLayout sparse_layout(const ls_attn_params* p, int32_t topk) {
+  SparseLayout L;
+  const int64_t n = (int64_t)topk + (p->q_pos0 - p->prefix_len) + p->n_q;
+  L.n_max = (n + 31) / 32 * 32;
+  L.phys_bytes = pad256((size_t)p->n_q * L.n_max * 4);
+  L.stat_bytes = pad256((size_t)p->n_q * p->n_q_heads * 4);
+  L.ds_bytes = pad256((size_t)p->n_q * p->n_q_heads * L.n_max * 2);
+  return L;
+}
+
+ls_status check_sparse(const ls_attn_params* p, const int32_t* idx, int32_t topk) {
+  ls_status st = check_params(p, true);
+  if (st != LS_OK) return st;
+  if (p->dtype != LS_BF16 || p->head_dim != 576 || p->head_dim_v != 512 || p->n_kv_heads != 1)
+    return fail(LS_ERR_UNSUPPORTED,
+                "sparse replay supports bf16, one latent row of 576 (values: first 512)");
+  if (p->n_q_heads % 128 != 0)
+    return fail(LS_ERR_UNSUPPORTED, "sparse replay needs a multiple of 128 query heads");
+  if (p->k_pool != p->v_pool)
+    return fail(LS_ERR_INVALID_ARG, "sparse replay reads values from the latent rows: v_pool == k_pool");
+  if (!is_pow2(p->page_size))
+    return fail(LS_ERR_UNSUPPORTED, "page_size %d is not a power of two", p->page_size);
+  if (topk < 0 || topk > p->prefix_len)
+    return fail(LS_ERR_INVALID_ARG, "topk %d outside [0, prefix_len]", topk);
+  if (topk > 0 && (!idx || !aligned16(idx)))
+    return fail(LS_ERR_INVALID_ARG, "idx must be non-NULL and 16-byte aligned");
+  if (sparse_layout(p, topk).n_max > (int64_t)1 << 30)
+    return fail(LS_ERR_UNSUPPORTED, "key list too long");
+  return LS_OK;
+}
+
+void fill_sparse(const ls_attn_params* p, const int32_t* idx, int32_t topk, const SparseLayout& L,
+                 void* ws, ls::SparseArgs& a) {
+  a.q = p->q;
+  a.latent = p->k_pool;
+  a.page_table = p->page_table;
+  a.idx = idx;
+  a.phys = (int32_t*)ws;
+  a.prefix_len = p->prefix_len;
+  a.kv_len = kv_len_of(p);
+  a.window0 = p->q_pos0 - p->prefix_len;
+  a.n_q = p->n_q;
+  a.n_heads = p->n_q_heads;
+  a.topk = topk;
+  a.n_max = (int32_t)L.n_max;
+  a.log2_page = ilog2(p->page_size);
+  a.scale = p->softmax_scale;
+  a.scale_log2 = p->softmax_scale * ls::kLog2e;
+  a.accumulate_dq = (p->flags & LS_FLAG_ACCUMULATE_DQ) ? 1 : 0;
+}
+
+// Checked mode for the index lists: every selected position inside the prefix.
+ls_status check_idx(const ls_attn_params* p, const int32_t* idx, int32_t topk, hipStream_t s) {
+  if (!(p->flags & LS_FLAG_CHECKED) || topk == 0) return LS_OK;
+  std::vector<int32_t> host((size_t)p->n_q * topk);
+  hipError_t e = hipMemcpyAsync(host.data(), idx, host.size() * 4, hipMemcpyDeviceToHost, s);
+  if (e == hipSuccess) e = hipStreamSynchronize(s);
+  if (e != hipSuccess) return hip_fail(e, "checked mode: idx copy");
+  for (size_t i = 0; i < host.size(); ++i)
+    if (host[i] < 0 || host[i] >= p->prefix_len)
+      return fail(LS_ERR_INVALID_ARG, "idx[%zu] = %d outside [0, prefix_len)", i, host[i]);
+  return LS_OK;
+}
+
+}  // namespace
+
+LS_API size_t ls_sparse_attn_workspace_size(const ls_attn_params* p, int32_t topk,
+                                            int32_t backward) {
+  if (!p || p->n_q <= 0 || p->n_q_heads <= 0 || topk < 0) return 0;
+  const SparseLayout L = sparse_layout(p, topk);
+  return backward ? L.bwd_bytes() : L.fwd_bytes();
+}
+
+LS_API ls_status ls_sparse_attn_fwd(const ls_attn_params* p, const int32_t* idx, int32_t topk,
+                                    float* out, float* lse, void* workspace,
+                                    size_t workspace_bytes, void* stream) {
+  ls_status st = check_sparse(p, idx, topk);
+  if (st != LS_OK) return st;
+  if (p->n_q == 0) return LS_OK;
+  if (!out || !lse || !aligned16(out) || !aligned16(lse))
+    return fail(LS_ERR_INVALID_ARG, "out/lse must be non-NULL and 16-byte aligned");
+  const SparseLayout L = sparse_layout(p, topk);
+  if (!workspace || !aligned16(workspace) || workspace_bytes < L.fwd_bytes())
+    return fail(LS_ERR_WORKSPACE, "workspace of %zu bytes needed", L.fwd_bytes());
+  std::vector<Range> ins, outs;
+  pool_ranges(p, ins);
+  if (topk > 0) ins.push_back(rng("idx", idx, (size_t)p->n_q * topk * 4));
+  outs.push_back(rng("out", out, (size_t)p->n_q * p->n_q_heads * 512 * 4));
+  outs.push_back(rng("lse", lse, (size_t)p->n_q * p->n_q_heads * 4));
+  outs.push_back(rng("workspace", workspace, L.fwd_bytes()));
+  if ((st = check_alias(outs, ins)) != LS_OK) return st;
+  hipStream_t s = (hipStream_t)stream;
+  if ((st = check_pages(p, kv_len_of(p), s)) != LS_OK) return st;
+  if ((st = check_idx(p, idx, topk, s)) != LS_OK) return st;
+  ls::SparseArgs a = {};
+  fill_sparse(p, idx, topk, L, workspace, a);
+  a.out = out;
+  a.lse = lse;
+  hipError_t e = ls::launch_sparse_phys(a, s);
+  if (e == hipSuccess) e = ls::launch_sparse_fwd(a, s);
+  return e == hipSuccess ? LS_OK : hip_fail(e, "sparse forward launch");
+}
+
+LS_API ls_status ls_sparse_attn_bwd(const ls_attn_params* p, const int32_t* idx, int32_t topk,
+                                    const void* d_out, const void* out, int32_t out_dtype,
+                                    const float* lse, float* dq, void* workspace,
+                                    size_t workspace_bytes, void* stream) {
+  ls_status st = check_sparse(p, idx, topk);
+  if (st != LS_OK) return st;
+  if (out_dtype != LS_BF16 && out_dtype != LS_F32)
+    return fail(LS_ERR_UNSUPPORTED, "out_dtype %d", out_dtype);
+  if (p->n_q == 0) return LS_OK;
+  for (const void* ptr : {d_out, out, (const void*)lse, (const void*)dq})
+    if (!ptr || !aligned16(ptr))
+      return fail(LS_ERR_INVALID_ARG, "d_out/out/lse/dq must be non-NULL and 16-byte aligned");
+  const SparseLayout L = sparse_layout(p, topk);
+  if (!workspace || !aligned16(workspace) || workspace_bytes < L.bwd_bytes())
+    return fail(LS_ERR_WORKSPACE, "workspace of %zu bytes needed", L.bwd_bytes());
+  const size_t rows = (size_t)p->n_q * p->n_q_heads;
+  std::vector<Range> ins, outs;
+  pool_ranges(p, ins);
+  if (topk > 0) ins.push_back(rng("idx", idx, (size_t)p->n_q * topk * 4));
+  ins.push_back(rng("d_out", d_out, rows * 512 * 2));
+  ins.push_back(rng("out", out, rows * 512 * (out_dtype == LS_BF16 ? 2 : 4)));
+  ins.push_back(rng("lse", lse, rows * 4));
+  outs.push_back(rng("dq", dq, rows * 576 * 4));
+  outs.push_back(rng("workspace", workspace, L.bwd_bytes()));
+  if ((st = check_alias(outs, ins)) != LS_OK) return st;
+  hipStream_t s = (hipStream_t)stream;
+  if ((st = check_pages(p, kv_len_of(p), s)) != LS_OK) return st;
+  if ((st = check_idx(p, idx, topk, s)) != LS_OK) return st;
+  ls::SparseArgs a = {};
+  fill_sparse(p, idx, topk, L, workspace, a);
+  char* w = (char*)workspace + L.phys_bytes;
+  float* delta = (float*)w;
+  float* lse2 = (float*)(w + L.stat_bytes);
+  a.delta = delta;
+  a.lse2 = lse2;
+  a.ds = (__bf16*)(w + 2 * L.stat_bytes);
+  a.d_out = d_out;
+  a.dq = dq;
+  hipError_t e = ls::launch_sparse_phys(a, s);
+  if (e == hipSuccess)
+    e = ls::launch_bwd_prep(d_out, out, true, out_dtype == LS_BF16, lse, p->n_q, p->n_q_heads,
+                            512, delta, lse2, s);
+  if (e == hipSuccess) e = ls::launch_sparse_bwd(a, s);
+  return e == hipSuccess ? LS_OK : hip_fail(e, "sparse backward launch");
+}

@@ -1,0 +1,189 @@
+// Sparse latent replay, backward (dq only) and the key-list resolution; the
+// shared tile helpers and the layout are described in sparse_common.h.
+#include "sparse_common.h"
+
+namespace ls {
+namespace {
+using namespace sparse;
+
+// ---------------------------------------------------------------- key lists
+// phys[t][k] for k < n_max: the physical latent row of key k of token t
+// (selected prefix positions, then the response window); keys past the
+// token's list repeat its last key so tile loads stay inside the pool.
+__global__ __launch_bounds__(256) void sparse_phys_kernel(SparseArgs a) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= (int64_t)a.n_q * a.n_max) return;
+  const int t = (int)(i / a.n_max);
+  int k = (int)(i - (int64_t)t * a.n_max);
+  const int n_t = a.topk + (int)a.window0 + t + 1;
+  if (k >= n_t) k = n_t - 1;
+  int64_t pos = k < a.topk ? (int64_t)a.idx[(int64_t)t * a.topk + k]
+                           : a.prefix_len + (k - a.topk);
+  if (pos < 0) pos = 0;
+  if (pos >= a.kv_len) pos = a.kv_len - 1;
+  a.phys[i] = (int32_t)phys_pos(a.page_table, pos, a.log2_page);
+}
+
+// ---------------------------------------------------------------- backward, phase 1
+// dS[t][head][k] = P (dP - Delta) in bf16, P = exp2(s*c - lse2), dP = dO . v_k.
+__global__ __launch_bounds__(256, 1) void sparse_ds_kernel(SparseArgs a) {
+  __shared__ __attribute__((aligned(1024))) char smem[kSlots * kTile];
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int l32 = lane & 31, hh = lane >> 5;
+  const int t = blockIdx.x;
+  const int head = blockIdx.y * 128 + w * 32 + l32;
+  const int n_t = a.topk + (int)a.window0 + t + 1;
+  const int n_tiles = (n_t + kKeys - 1) / kKeys;
+  const int32_t* phys_t = a.phys + (int64_t)t * a.n_max;
+  const char* pool = static_cast<const char*>(a.latent);
+
+  SFetch f;
+  f.init(lane, w);
+  const SOffsets so = s_offsets(lane);
+  int32_t pr[9];
+  f.rows_of(phys_t, 0, pr);
+  f.issue(smem, pool, pr, w);
+  f.rows_of(phys_t, n_tiles > 1 ? 1 : 0, pr);
+
+  bf16x8 qreg[36], dreg[32];
+  {
+    const int64_t rh = (int64_t)t * a.n_heads + head;
+    const __bf16* qrow = static_cast<const __bf16*>(a.q) + rh * kDk + hh * 8;
+    const __bf16* drow = static_cast<const __bf16*>(a.d_out) + rh * kDv + hh * 8;
+#pragma unroll
+    for (int ks = 0; ks < 36; ++ks) qreg[ks] = *reinterpret_cast<const bf16x8*>(qrow + ks * 16);
+#pragma unroll
+    for (int ks = 0; ks < 32; ++ks) dreg[ks] = *reinterpret_cast<const bf16x8*>(drow + ks * 16);
+  }
+  const int64_t stat = (int64_t)head * a.n_q + t;
+  const float lse2 = a.lse2[stat], delta = a.delta[stat];
+  __bf16* ds_row = a.ds + ((int64_t)t * a.n_heads + head) * a.n_max;
+  wait_fetch();
+  __syncthreads();
+
+  for (int T = 0; T < n_tiles; ++T) {
+    const int tn = T + 1 < n_tiles ? T + 1 : T;
+    f.issue(smem + ((T + 1) % kSlots) * kTile, pool, pr, w);
+    f.rows_of(phys_t, tn + 1 < n_tiles ? tn + 1 : tn, pr);
+    const char* tile = smem + (T % kSlots) * kTile;
+    f32x16 s = zero16(), dp = zero16();
+#pragma unroll
+    for (int ks = 0; ks < 36; ++ks) {
+      const bf16x8 kv = s_row16(tile, so, ks);
+      s = mfma32(kv, qreg[ks], s);
+      if (ks < 32) dp = mfma32(kv, dreg[ks], dp);
+      if (ks % 6 == 5) __builtin_amdgcn_sched_barrier(0);
+    }
+#pragma unroll
+    for (int q4 = 0; q4 < 4; ++q4) {
+      __bf16 v[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int r = 4 * q4 + e;
+        float p = __builtin_amdgcn_exp2f(fmaf(s[r], a.scale_log2, -lse2));
+        if (T * kKeys + acc_key(r, hh) >= n_t) p = 0.f;
+        v[e] = (__bf16)(p * (dp[r] - delta));
+      }
+      // keys 8*q4 + 4h + {0..3} of this tile: four consecutive bf16
+      u32x2 packed;
+      packed[0] = __builtin_bit_cast(uint16_t, v[0]) | ((uint32_t)__builtin_bit_cast(uint16_t, v[1]) << 16);
+      packed[1] = __builtin_bit_cast(uint16_t, v[2]) | ((uint32_t)__builtin_bit_cast(uint16_t, v[3]) << 16);
+      *reinterpret_cast<u32x2*>(ds_row + T * kKeys + 8 * q4 + 4 * hh) = packed;
+    }
+    wait_fetch();
+    __syncthreads();
+  }
+}
+
+// ---------------------------------------------------------------- backward, phase 2
+// dq[t][head][d] (+)= scale * sum_k dS[t][head][k] c_k[d]; wave w owns heads
+// 32*(w & 3) .. +31 and columns 288*(w >> 2) .. +287.
+__global__ __launch_bounds__(512, 1) void sparse_dq_kernel(SparseArgs a) {
+  __shared__ __attribute__((aligned(1024))) char smem[kSlots * kTile];
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int l32 = lane & 31, hh = lane >> 5;
+  const int t = blockIdx.x;
+  const int head = blockIdx.y * 128 + (w & 3) * 32 + l32;
+  const int half = w >> 2;
+  const bool fetcher = w < 4;
+  const int n_t = a.topk + (int)a.window0 + t + 1;
+  const int n_tiles = (n_t + kKeys - 1) / kKeys;
+  const int32_t* phys_t = a.phys + (int64_t)t * a.n_max;
+  const char* pool = static_cast<const char*>(a.latent);
+  const __bf16* ds_row = a.ds + ((int64_t)t * a.n_heads + head) * a.n_max;
+
+  SFetch f;
+  f.init(lane, w & 3);
+  const SOffsets so = s_offsets(lane);
+  int32_t pr[9];
+  if (fetcher) {
+    f.rows_of(phys_t, 0, pr);
+    f.issue(smem, pool, pr, w);
+    f.rows_of(phys_t, n_tiles > 1 ? 1 : 0, pr);
+  }
+  f32x16 acc[9];
+#pragma unroll
+  for (int i = 0; i < 9; ++i) acc[i] = zero16();
+  wait_fetch();
+  __syncthreads();
+
+  for (int T = 0; T < n_tiles; ++T) {
+    const int tn = T + 1 < n_tiles ? T + 1 : T;
+    if (fetcher) {
+      f.issue(smem + ((T + 1) % kSlots) * kTile, pool, pr, w);
+      f.rows_of(phys_t, tn + 1 < n_tiles ? tn + 1 : tn, pr);
+    }
+    const char* tile = smem + (T % kSlots) * kTile;
+    // dS operand: keys 16kk + {4h..4h+3, 8+4h..8+4h+3}
+    bf16x8 d[2];
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk) {
+      const u32x2 lo = *reinterpret_cast<const u32x2*>(ds_row + T * kKeys + 16 * kk + 4 * hh);
+      const u32x2 hi = *reinterpret_cast<const u32x2*>(ds_row + T * kKeys + 16 * kk + 8 + 4 * hh);
+      u32x4 both;
+      both[0] = lo[0]; both[1] = lo[1]; both[2] = hi[0]; both[3] = hi[1];
+      d[kk] = __builtin_bit_cast(bf16x8, both);
+    }
+#pragma unroll
+    for (int db = 0; db < 9; ++db) {
+      acc[db] = mfma32(s_col8(tile, so, 9 * half + db, 0, 8), d[0], acc[db]);
+      acc[db] = mfma32(s_col8(tile, so, 9 * half + db, 16, 24), d[1], acc[db]);
+    }
+    wait_fetch();
+    __syncthreads();
+  }
+
+  float* dq = a.dq + ((int64_t)t * a.n_heads + head) * kDk + 288 * half;
+#pragma unroll
+  for (int db = 0; db < 9; ++db) {
+#pragma unroll
+    for (int q4 = 0; q4 < 4; ++q4) {
+      f32x4* dst = reinterpret_cast<f32x4*>(dq + 32 * db + 8 * q4 + 4 * hh);
+      f32x4 v;
+      v[0] = acc[db][4 * q4 + 0] * a.scale;
+      v[1] = acc[db][4 * q4 + 1] * a.scale;
+      v[2] = acc[db][4 * q4 + 2] * a.scale;
+      v[3] = acc[db][4 * q4 + 3] * a.scale;
+      if (a.accumulate_dq) v += *dst;
+      *dst = v;
+    }
+  }
+}
+
+}  // namespace
+
+hipError_t launch_sparse_phys(const SparseArgs& a, hipStream_t stream) {
+  const int64_t n = (int64_t)a.n_q * a.n_max;
+  hipLaunchKernelGGL(sparse_phys_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, stream, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_sparse_bwd(const SparseArgs& a, hipStream_t stream) {
+  hipLaunchKernelGGL(sparse_ds_kernel, dim3(a.n_q, a.n_heads / 128), dim3(256), 0, stream, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(sparse_dq_kernel, dim3(a.n_q, a.n_heads / 128), dim3(512), 0, stream, a);
+  return hipGetLastError();
+}
+
+}  // namespace ls

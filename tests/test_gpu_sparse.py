@@ -1,0 +1,76 @@
+"""Sparse latent replay (MLA/DSA): HIP path vs the fp64 oracle (needs an MI355X).
+
+Bars: out rel-L2 <= 5e-3, lse max-abs <= 1e-3, dq rel-L2 <= 1e-2 (bf16 inputs)."""
+from __future__ import annotations
+
+import numpy as np
+import pytest
+
+import oracle as O
+from paper_2607_14952_amd import binding as B
+from paper_2607_14952_amd import configs, inputs
+from paper_2607_14952_amd.replay import to_device
+from tests._gpu import announce, host, lse_err, rel_l2
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu_ready():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    B.load_library()
+
+
+def run(cfg, h, *, q_pos0=None, rows=None, backward=True):
+    import torch
+    q_pos0 = cfg.prefix_len if q_pos0 is None else q_pos0
+    q = to_device(h["q"])
+    lat = to_device(h["latent_pool"])
+    kv = B.PagedKV(lat, lat, to_device(h["page_table"]))
+    idx = to_device(h["idx"]) if h["idx"].shape[1] else None
+    announce(f"sparse {cfg.name} R={h['q'].shape[0]} topk={h['idx'].shape[1]} q_pos0={q_pos0}")
+    out, lse = B.sparse_attn_fwd(q, kv, idx, prefix_len=cfg.prefix_len, q_pos0=q_pos0,
+                                 scale=cfg.scale)
+    dq = None
+    if backward:
+        out_b = out.to(torch.bfloat16)
+        dq = B.sparse_attn_bwd(q, kv, idx, to_device(h["d_out"]), out_b, lse,
+                               prefix_len=cfg.prefix_len, q_pos0=q_pos0, scale=cfg.scale)
+    torch.cuda.synchronize()
+    kw = dict(page_size=cfg.page_size, prefix_len=cfg.prefix_len, q_pos0=q_pos0,
+              scale=cfg.scale, head_dim_v=512)
+    r = np.arange(h["q"].shape[0]) if rows is None else np.asarray(rows)
+    o_ref, l_ref = O.sparse_fwd(h["q"], h["latent_pool"], h["page_table"], h["idx"], rows=r, **kw)
+    assert rel_l2(host(out)[r], o_ref) <= 5e-3, "sparse out"
+    assert lse_err(host(lse)[:, r], l_ref) <= 1e-3, "sparse lse"
+    if backward:
+        dq_ref = O.sparse_bwd(h["q"], h["latent_pool"], h["page_table"], h["idx"], h["d_out"],
+                              rows=r, **kw)
+        assert rel_l2(host(dq)[r], dq_ref) <= 1e-2, f"sparse dq {rel_l2(host(dq)[r], dq_ref):.2e}"
+
+
+SMALL = configs.C5.scaled(name="c5_small", prefix_len=8192, resp_len=70, topk=300)
+
+
+def test_sparse_small():
+    run(SMALL, inputs.sparse_inputs(SMALL))
+
+
+def test_sparse_window_only_and_offset_rows():
+    """topk = 0 (only the response window), and rows that start after earlier
+    response positions (q_pos0 > prefix_len: the window reaches back to prefix_len)."""
+    cfg = SMALL.scaled(name="c5_win", topk=0, resp_len=40)
+    h = inputs.sparse_inputs(cfg)
+    run(cfg, h)
+    cfg2 = SMALL.scaled(name="c5_off", resp_len=33, topk=64)
+    h2 = inputs.sparse_inputs(cfg2.scaled(resp_len=33 + 50))   # pool holds 50 earlier response rows
+    h2 = dict(h2, q=h2["q"][50:], d_out=h2["d_out"][50:], idx=h2["idx"][50:])
+    run(cfg2, h2, q_pos0=cfg2.prefix_len + 50)
+
+
+@pytest.mark.timeout(900)
+def test_c5_full_size_sampled():
+    cfg = configs.C5
+    run(cfg, inputs.sparse_inputs(cfg), rows=[0, 1, 1023, 2047])
