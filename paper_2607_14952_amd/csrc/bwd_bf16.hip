@@ -5,7 +5,8 @@
 // l owns row l % 32.  Per 32-key tile it recomputes S^T = K Q^T, forms
 // P = exp2(s*scale*log2e - lse2) with the merged log-normalizer, dP^T = V dO^T,
 // dS = P (dP - Delta) and accumulates dq^T += K^T dS^T.  K and V tiles arrive
-// by direct global->LDS loads into a three-slot ring (row-major, swizzled);
+// by direct global->LDS loads into a four-slot ring, two tiles ahead
+// (row-major, swizzled);
 // the K^T operand of the third product comes from transposing LDS reads of
 // the same K tile.  The dq product of tile t-1 is issued in the same block as
 // the exponentials of tile t.
@@ -30,49 +31,73 @@ constexpr int kQBM = 128;
 constexpr int kQBN = kTileKeys;                   // 32
 constexpr int kRowBytes = kD * 2;                 // 512 B: one key row
 constexpr int kQStage = 2 * kTileBytes;           // K tile + V tile (row-major, swizzled)
-constexpr int kQSlots = 3;
+constexpr int kQAhead = 2;                        // tiles in flight beyond the one consumed
+constexpr int kQSlots = kQAhead + 2;
 
-// S^T = K Q^T and dP^T = V dO^T for one 32-key tile (operand reads issued ahead).
+// Operand reads run a fixed number of MFMAs ahead of their use (see mfma_fence).
+constexpr int kSDAhead = 3;   // steps of (K row, V row) reads in flight
+constexpr int kKTAhead = 4;   // transposed K operands in flight (two reads each)
+
+// S^T = K Q^T and dP^T = V dO^T for one 32-key tile.
 __device__ __forceinline__ void scores_dp(const char* Ks, const char* Vs, const bf16x8* qreg,
                                           const bf16x8* dreg, const TileOffsets& o, f32x16& s,
                                           f32x16& dp) {
+  bf16x8 kr[16], vr[16];
+#pragma unroll
+  for (int i = 0; i < kSDAhead; ++i) {
+    kr[i] = tile_row16(Ks, o, i);
+    vr[i] = tile_row16(Vs, o, i);
+  }
   s = zero16();
   dp = zero16();
 #pragma unroll
   for (int ks = 0; ks < 16; ++ks) {
-    s = mfma32(tile_row16(Ks, o, ks), qreg[ks], s);
-    dp = mfma32(tile_row16(Vs, o, ks), dreg[ks], dp);
+    if (ks + kSDAhead < 16) {
+      kr[ks + kSDAhead] = tile_row16(Ks, o, ks + kSDAhead);
+      vr[ks + kSDAhead] = tile_row16(Vs, o, ks + kSDAhead);
+    }
+    s = mfma32(kr[ks], qreg[ks], s);
+    dp = mfma32(vr[ks], dreg[ks], dp);
+    mfma_fence();
   }
 }
 
 // dq^T += K^T dS^T for one 32-key tile; dS register block kk holds keys
 // 16kk + {4h..4h+3, 8+4h..8+4h+3}, matched by the transposed K reads.
+// Operand i is dims block i/2, key half i%2.
 __device__ __forceinline__ void dq_update(const char* Ks, const bf16x8& d0, const bf16x8& d1,
                                           f32x16* acc, const TileOffsets& o) {
+  bf16x8 kt[16];
+  auto read = [&](int i) {
+    return (i & 1) ? tile_col8(Ks, o, i >> 1, 16, 24) : tile_col8(Ks, o, i >> 1, 0, 8);
+  };
 #pragma unroll
-  for (int db = 0; db < 8; ++db) {
-    acc[db] = mfma32(tile_col8(Ks, o, db, 0, 8), d0, acc[db]);
-    acc[db] = mfma32(tile_col8(Ks, o, db, 16, 24), d1, acc[db]);
+  for (int i = 0; i < kKTAhead; ++i) kt[i] = read(i);
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    if (i + kKTAhead < 16) kt[i + kKTAhead] = read(i + kKTAhead);
+    acc[i >> 1] = mfma32(kt[i], (i & 1) ? d1 : d0, acc[i >> 1]);
+    mfma_fence();
   }
 }
 
-// One pipelined step (ring slots are distinct; see the forward kernel).
+// One pipelined step (ring slots are distinct; see the forward kernel).  `pe`
+// holds the page-table entry of t0_next on entry and that of t0_after on return.
 template <bool kPerKey, bool kFirst>
 __device__ __forceinline__ void dq_step(const BwdArgs& a, char* __restrict__ next,
                                         const char* __restrict__ cur,
                                         const char* __restrict__ prev_k, const TileFetch& kf,
-                                        const TileFetch& vf, int64_t t0_next, int64_t prow_next,
-                                        int64_t k_hi, int64_t t0, int64_t kb, int64_t k_all,
-                                        int64_t my_lim, const bf16x8* qreg, const bf16x8* dreg,
+                                        const TileFetch& vf, const PageLookup& pl, int32_t& pe,
+                                        int64_t t0_next, int64_t t0_after, int64_t k_hi,
+                                        int64_t t0, int64_t kb, int64_t k_all, int64_t my_lim,
+                                        const bf16x8* qreg, const bf16x8* dreg,
                                         const TileOffsets& to, int hh, float lse2, float delta,
                                         f32x16* acc, bf16x8& d0, bf16x8& d1) {
-  if (!kPerKey && t0_next + kQBN <= k_hi) {
-    kf.issue_page(next, prow_next);
-    vf.issue_page(next + kTileBytes, prow_next);
-  } else {
-    kf.issue_rows(next, a.page_table, a.log2_page, t0_next, k_hi);
-    vf.issue_rows(next + kTileBytes, a.page_table, a.log2_page, t0_next, k_hi);
-  }
+  const int64_t prow_next = kPerKey ? 0 : pl.row(pe, t0_next);
+  if (!kPerKey) pe = pl.load(t0_after);
+  __builtin_amdgcn_sched_barrier(0);   // the entry load stays ahead of the stage's loads
+  kf.issue<kPerKey>(next, a.page_table, a.log2_page, t0_next, k_hi, prow_next);
+  vf.issue<kPerKey>(next + kTileBytes, a.page_table, a.log2_page, t0_next, k_hi, prow_next);
   f32x16 s, dp;
   scores_dp(cur, cur + kTileBytes, qreg, dreg, to, s, dp);
   const bool edge = t0 < kb || t0 + kQBN > k_all;
@@ -129,18 +154,22 @@ __global__ __launch_bounds__(256, 1) void bwd_dq_bf16_d256_kernel(BwdArgs a) {
   auto page_row = [&](int t) -> int64_t {
     return kPerKey ? 0 : phys_pos_uniform(a.page_table, k_lo + (int64_t)t * kQBN, a.log2_page);
   };
+  PageLookup pl;
+  pl.init(a.page_table, a.log2_page);
   const TileOffsets to = tile_offsets(lane);
-  {
-    const int64_t pr0 = page_row(0);
-    if (!kPerKey && k_lo + kQBN <= k_hi) {
-      kf.issue_page(smem, pr0);
-      vf.issue_page(smem + kTileBytes, pr0);
-    } else {
-      kf.issue_rows(smem, a.page_table, a.log2_page, k_lo, k_hi);
-      vf.issue_rows(smem + kTileBytes, a.page_table, a.log2_page, k_lo, k_hi);
-    }
+  // tiles past the last one are clamped to it (refetched into an unread slot),
+  // so every iteration issues exactly one stage of direct loads
+  auto clamp = [&](int t) { return t < n_tiles ? t : n_tiles - 1; };
+#pragma unroll
+  for (int i = 0; i < kQAhead; ++i) {
+    const int64_t t0 = k_lo + (int64_t)clamp(i) * kQBN;
+    char* st = smem + i * kQStage;
+    const int64_t pr = page_row(clamp(i));
+    kf.issue<kPerKey>(st, a.page_table, a.log2_page, t0, k_hi, pr);
+    vf.issue<kPerKey>(st + kTileBytes, a.page_table, a.log2_page, t0, k_hi, pr);
   }
-  int64_t prow_next = page_row(n_tiles > 1 ? 1 : 0);
+  auto tile0 = [&](int t) { return k_lo + (int64_t)clamp(t) * kQBN; };
+  int32_t pe = kPerKey ? 0 : pl.load(tile0(kQAhead));
 
   bf16x8 qreg[16], dreg[16];
   {
@@ -167,31 +196,29 @@ __global__ __launch_bounds__(256, 1) void bwd_dq_bf16_d256_kernel(BwdArgs a) {
   for (int i = 0; i < 8; ++i) acc[i] = zero16();
   bf16x8 d0, d1;
 
+  // (a full wait here: the Q/dO loads may have been scheduled after the stages)
   wait_fetch();
-  __syncthreads();
+  tile_barrier();
+  // Iteration t fetches tile t + kQAhead and, before its barrier, waits for
+  // the loads of tile t + 1.
   {
-    const int tn = n_tiles > 1 ? 1 : 0;
-    const int64_t prow_after = page_row(n_tiles > 2 ? 2 : n_tiles - 1);
-    dq_step<kPerKey, true>(a, smem + kQStage, smem, smem, kf, vf, k_lo + (int64_t)tn * kQBN,
-                           prow_next, k_hi, k_lo, kb, k_all, my_lim, qreg, dreg, to, hh, lse2,
-                           delta, acc, d0, d1);
-    prow_next = prow_after;
-    wait_fetch();
-    __syncthreads();
+    dq_step<kPerKey, true>(a, smem + kQAhead * kQStage, smem, smem, kf, vf, pl, pe, tile0(kQAhead),
+                           tile0(kQAhead + 1), k_hi, k_lo, kb, k_all, my_lim, qreg, dreg, to, hh,
+                           lse2, delta, acc, d0, d1);
+    wait_fetch_but_newest_stage();
+    tile_barrier();
   }
   for (int t = 1; t < n_tiles; ++t) {
     const int64_t t0 = k_lo + (int64_t)t * kQBN;
-    const int tn = t + 1 < n_tiles ? t + 1 : t;
-    const int64_t prow_after = page_row(tn + 1 < n_tiles ? tn + 1 : tn);
-    dq_step<kPerKey, false>(a, smem + ((t + 1) % kQSlots) * kQStage,
+    dq_step<kPerKey, false>(a, smem + ((t + kQAhead) % kQSlots) * kQStage,
                             smem + (t % kQSlots) * kQStage, smem + ((t - 1) % kQSlots) * kQStage,
-                            kf, vf, k_lo + (int64_t)tn * kQBN, prow_next, k_hi, t0, kb, k_all,
-                            my_lim, qreg, dreg, to, hh, lse2, delta, acc, d0, d1);
-    prow_next = prow_after;
-    wait_fetch();
-    __syncthreads();
+                            kf, vf, pl, pe, tile0(t + kQAhead), tile0(t + kQAhead + 1), k_hi, t0,
+                            kb, k_all, my_lim, qreg, dreg, to, hh, lse2, delta, acc, d0, d1);
+    wait_fetch_but_newest_stage();
+    tile_barrier();
   }
   dq_update(smem + ((n_tiles - 1) % kQSlots) * kQStage, d0, d1, acc, to);
+  wait_fetch();   // no direct load is left in flight when the waves end
 
   if (row_ok) {
 #pragma unroll

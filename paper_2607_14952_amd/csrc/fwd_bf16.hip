@@ -8,8 +8,9 @@
 //
 // Keys are processed in 32-key tiles aligned to multiples of 32 (one page-table
 // entry per tile when pages hold >= 32 positions).  K and V rows are fetched
-// with direct global->LDS loads into a three-slot ring, one tile ahead; no
-// VGPRs stage them.  The K^T operand is one 16-byte LDS read per lane; the V^T
+// with direct global->LDS loads into a four-slot ring, two tiles ahead (each
+// wave waits only for the older of the two stages in flight); no VGPRs stage
+// them.  The K^T operand is one 16-byte LDS read per lane; the V^T
 // operand comes from transposing LDS reads of the row-major V tile.
 //
 // The loop is software-pipelined across tiles: iteration t issues the score
@@ -30,40 +31,44 @@ constexpr int kD = 256;
 constexpr int kBM = 128;
 constexpr int kBN = kTileKeys;              // 32
 constexpr int kStage = 2 * kTileBytes;      // K tile + V tile
-constexpr int kSlots = 3;
+constexpr int kAhead = 2;                   // tiles in flight beyond the one consumed
+constexpr int kSlots = kAhead + 2;          // + the tile being scored + the V of the previous one
+
+// Operand reads run a fixed number of MFMAs ahead of their use (see mfma_fence).
+constexpr int kKAhead = 6;   // K operand reads in flight (16-byte reads)
+constexpr int kVAhead = 4;   // V operands in flight (two transposing reads each)
 
 // S^T (32 keys x this lane's row) = K Q^T over the 256-wide head.
-// The K operand reads run two steps ahead of the MFMA chain.
 __device__ __forceinline__ f32x16 scores(const char* Ks, const bf16x8* qreg, const TileOffsets& o) {
+  bf16x8 kreg[16];
+#pragma unroll
+  for (int i = 0; i < kKAhead; ++i) kreg[i] = tile_row16(Ks, o, i);
   f32x16 s = zero16();
-  bf16x8 k0 = tile_row16(Ks, o, 0), k1 = tile_row16(Ks, o, 1);
 #pragma unroll
   for (int ks = 0; ks < 16; ++ks) {
-    const bf16x8 kn = tile_row16(Ks, o, ks + 2 < 16 ? ks + 2 : 15);
-    s = mfma32(k0, qreg[ks], s);
-    k0 = k1;
-    k1 = kn;
+    if (ks + kKAhead < 16) kreg[ks + kKAhead] = tile_row16(Ks, o, ks + kKAhead);
+    s = mfma32(kreg[ks], qreg[ks], s);
+    mfma_fence();
   }
-  __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
-#pragma unroll
-  for (int ks = 0; ks < 14; ++ks) {
-    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-    __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-  }
-  __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
   return s;
 }
 
 // O^T += V^T P^T for one 32-key tile.  P's register block kk holds keys
 // 16kk + {4h..4h+3, 8+4h..8+4h+3}; the V^T operand reads the same keys.
+// Operand i is dims block i/2, key half i%2.
 __device__ __forceinline__ void pv(const char* Vs, const bf16x8& p0, const bf16x8& p1,
                                    f32x16* oacc, const TileOffsets& o) {
+  bf16x8 vreg[16];
+  auto read = [&](int i) {
+    return (i & 1) ? tile_col8(Vs, o, i >> 1, 16, 24) : tile_col8(Vs, o, i >> 1, 0, 8);
+  };
 #pragma unroll
-  for (int db = 0; db < 8; ++db) {
-    const bf16x8 v0 = tile_col8(Vs, o, db, 0, 8);
-    const bf16x8 v1 = tile_col8(Vs, o, db, 16, 24);
-    oacc[db] = mfma32(v0, p0, oacc[db]);
-    oacc[db] = mfma32(v1, p1, oacc[db]);
+  for (int i = 0; i < kVAhead; ++i) vreg[i] = read(i);
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    if (i + kVAhead < 16) vreg[i + kVAhead] = read(i + kVAhead);
+    oacc[i >> 1] = mfma32(vreg[i], (i & 1) ? p1 : p0, oacc[i >> 1]);
+    mfma_fence();
   }
 }
 
@@ -100,26 +105,26 @@ __device__ __forceinline__ float softmax_tile(f32x16& s, float c, float& m_run, 
 }
 
 // One pipelined step: scores of the tile in `ks_cur`, the PV product of the
-// previous tile (V in `vs_prev`, P in p0/p1), while the next tile streams into
-// `next`.  The three LDS regions are distinct ring slots; the restrict
+// previous tile (V in `vs_prev`, P in p0/p1), while the tile at t0_next streams
+// into `next`.  The three LDS regions are distinct ring slots; the restrict
 // qualifiers tell the compiler so, which lets it keep LDS reads running while
-// the direct loads into `next` are in flight.
+// the direct loads into `next` are in flight.  `pe` holds the page-table entry
+// of t0_next on entry and that of t0_after on return.
 template <bool kPerKey, bool kFirst>
 __device__ __forceinline__ float step(const FwdArgs& a, char* __restrict__ next,
                                       const char* __restrict__ ks_cur,
                                       const char* __restrict__ vs_prev, const TileFetch& kf,
-                                      const TileFetch& vf, int64_t t0_next, int64_t prow_next,
-                                      int64_t k_hi, int64_t t0, int64_t kb, int64_t k_all,
-                                      int64_t my_lim, const bf16x8* qreg, const TileOffsets& to,
-                                      int hh, f32x16* oacc, bf16x8& p0, bf16x8& p1, float& m_run,
+                                      const TileFetch& vf, const PageLookup& pl, int32_t& pe,
+                                      int64_t t0_next, int64_t t0_after, int64_t k_hi, int64_t t0,
+                                      int64_t kb, int64_t k_all, int64_t my_lim,
+                                      const bf16x8* qreg, const TileOffsets& to, int hh,
+                                      f32x16* oacc, bf16x8& p0, bf16x8& p1, float& m_run,
                                       float& l_run) {
-  if (!kPerKey && t0_next + kBN <= k_hi) {
-    kf.issue_page(next, prow_next);
-    vf.issue_page(next + kTileBytes, prow_next);
-  } else {
-    kf.issue_rows(next, a.page_table, a.log2_page, t0_next, k_hi);
-    vf.issue_rows(next + kTileBytes, a.page_table, a.log2_page, t0_next, k_hi);
-  }
+  const int64_t prow_next = kPerKey ? 0 : pl.row(pe, t0_next);
+  if (!kPerKey) pe = pl.load(t0_after);
+  __builtin_amdgcn_sched_barrier(0);   // the entry load stays ahead of the stage's loads
+  kf.issue<kPerKey>(next, a.page_table, a.log2_page, t0_next, k_hi, prow_next);
+  vf.issue<kPerKey>(next + kTileBytes, a.page_table, a.log2_page, t0_next, k_hi, prow_next);
   f32x16 s = scores(ks_cur, qreg, to);
   if (t0 < kb || t0 + kBN > k_all) mask_tile(s, t0, kb, my_lim, hh);
   const float alpha = softmax_tile(s, a.scale_log2, m_run, l_run);
@@ -167,26 +172,29 @@ __global__ __launch_bounds__(256, 1) void fwd_bf16_d256_kernel(FwdArgs a) {
   TileFetch kf, vf;
   kf.init(static_cast<const __bf16*>(a.k_pool) + (int64_t)g * kD, a.k_pos_stride, lane, w);
   vf.init(static_cast<const __bf16*>(a.v_pool) + (int64_t)g * kD, a.v_pos_stride, lane, w);
-  // Tile t lies in one page unless pages are shorter than a tile; its page row
-  // is looked up one iteration before the fetch, so consuming it never waits
-  // on the DMA loads in flight.  The tile that reaches k_hi takes per-row lookups.
+  // Tile t lies in one page unless pages are shorter than a tile; in the loop
+  // its page-table entry is loaded one iteration before the fetch, so
+  // consuming it never waits on the direct loads in flight.  The tile that
+  // reaches k_hi takes per-row lookups.
+  PageLookup pl;
+  pl.init(a.page_table, a.log2_page);
   auto page_row = [&](int t) -> int64_t {
     return kPerKey ? 0 : phys_pos_uniform(a.page_table, k_lo + (int64_t)t * kBN, a.log2_page);
   };
   auto fetch = [&](int t, int slot, int64_t prow) {
     const int64_t t0 = k_lo + (int64_t)t * kBN;
     char* st = smem + slot * kStage;
-    if (!kPerKey && t0 + kBN <= k_hi) {
-      kf.issue_page(st, prow);
-      vf.issue_page(st + kTileBytes, prow);
-    } else {
-      kf.issue_rows(st, a.page_table, a.log2_page, t0, k_hi);
-      vf.issue_rows(st + kTileBytes, a.page_table, a.log2_page, t0, k_hi);
-    }
+    kf.issue<kPerKey>(st, a.page_table, a.log2_page, t0, k_hi, prow);
+    vf.issue<kPerKey>(st + kTileBytes, a.page_table, a.log2_page, t0, k_hi, prow);
   };
   const TileOffsets to = tile_offsets(lane);
-  fetch(0, 0, page_row(0));
-  int64_t prow_next = page_row(n_tiles > 1 ? 1 : 0);
+  // tiles past the last one are clamped to it (refetched into an unread slot),
+  // so every iteration issues exactly one stage of direct loads
+  auto clamp = [&](int t) { return t < n_tiles ? t : n_tiles - 1; };
+#pragma unroll
+  for (int i = 0; i < kAhead; ++i) fetch(clamp(i), i, page_row(clamp(i)));
+  auto tile0 = [&](int t) { return k_lo + (int64_t)clamp(t) * kBN; };
+  int32_t pe = kPerKey ? 0 : pl.load(tile0(kAhead));
 
   // Q^T operand: lane holds q[row][16*ks + 8*hh .. +7]
   bf16x8 qreg[16];
@@ -209,38 +217,36 @@ __global__ __launch_bounds__(256, 1) void fwd_bf16_d256_kernel(FwdArgs a) {
   float m_run = -INFINITY, l_run = 0.f;
   bf16x8 p0, p1;   // packed P of the previous tile
 
+  // (a full wait here: the Q loads may have been scheduled after the stages)
   wait_fetch();
-  __syncthreads();
+  tile_barrier();
 
-  // tile 0 (peeled: no previous P to multiply)
+  // tile 0 (peeled: no previous P to multiply).  Iteration t fetches tile
+  // t + kAhead and, before its barrier, waits for the loads of tile t + 1.
   {
-    const int tn = n_tiles > 1 ? 1 : 0;
-    const int64_t prow_after = page_row(n_tiles > 2 ? 2 : n_tiles - 1);
-    step<kPerKey, true>(a, smem + kStage, smem, smem + kTileBytes, kf, vf, k_lo + (int64_t)tn * kBN,
-                        prow_next, k_hi, k_lo, kb, k_all, my_lim, qreg, to, hh, oacc, p0, p1,
-                        m_run, l_run);
-    prow_next = prow_after;
-    wait_fetch();
-    __syncthreads();
+    step<kPerKey, true>(a, smem + kAhead * kStage, smem, smem + kTileBytes, kf, vf, pl, pe,
+                        tile0(kAhead), tile0(kAhead + 1), k_hi, k_lo, kb, k_all, my_lim, qreg, to,
+                        hh, oacc, p0, p1, m_run, l_run);
+    wait_fetch_but_newest_stage();
+    tile_barrier();
   }
   for (int t = 1; t < n_tiles; ++t) {
     const int64_t t0 = k_lo + (int64_t)t * kBN;
-    const int tn = t + 1 < n_tiles ? t + 1 : t;   // the last iteration refetches its own tile
-    const int64_t prow_after = page_row(tn + 1 < n_tiles ? tn + 1 : tn);
     const float alpha = step<kPerKey, false>(
-        a, smem + ((t + 1) % kSlots) * kStage, smem + (t % kSlots) * kStage,
-        smem + ((t - 1) % kSlots) * kStage + kTileBytes, kf, vf, k_lo + (int64_t)tn * kBN,
-        prow_next, k_hi, t0, kb, k_all, my_lim, qreg, to, hh, oacc, p0, p1, m_run, l_run);
-    prow_next = prow_after;
+        a, smem + ((t + kAhead) % kSlots) * kStage, smem + (t % kSlots) * kStage,
+        smem + ((t - 1) % kSlots) * kStage + kTileBytes, kf, vf, pl, pe, tile0(t + kAhead),
+        tile0(t + kAhead + 1), k_hi, t0, kb, k_all, my_lim, qreg, to, hh, oacc, p0, p1, m_run,
+        l_run);
     // (l_run < 0 never holds; it keeps the exponentials ahead of this branch)
     if (__any(alpha != 1.f || l_run < 0.f)) {
 #pragma unroll
       for (int i = 0; i < 8; ++i) oacc[i] *= alpha;
     }
-    wait_fetch();
-    __syncthreads();
+    wait_fetch_but_newest_stage();
+    tile_barrier();
   }
   pv(smem + ((n_tiles - 1) % kSlots) * kStage + kTileBytes, p0, p1, oacc, to);
+  wait_fetch();   // no direct load is left in flight when the waves end
 
   const float l_tot = half_sum(l_run);
   if (row_ok) {

@@ -74,47 +74,56 @@ typedef __attribute__((__vector_size__(4 * sizeof(short)))) short i16x4;
 
 // ---------------------------------------------------------------- key tiles in LDS
 // A tile holds 32 key rows of 256 bf16 (512 bytes each), row-major.  The
-// 16-byte chunk c of row k is stored at chunk c ^ tile_swz(k).  The swizzle is
-// a permutation of the 8 chunks of every 128-byte group; it spreads over all
-// 32 banks both (a) eight consecutive rows read at one chunk (16-byte operand
-// reads) and (b) four consecutive rows read as 32-byte halves of a 16-lane
-// transposed read.
+// 16-byte chunk c of row k is stored at chunk c ^ tile_swz(k).
+//
+// gfx950 LDS has 64 four-byte banks (256 bytes per clock).  A 16-byte read
+// is served 16 lanes at a time and an 8-byte transposing read 32 lanes at a
+// time, so a read is conflict free when the lanes of each phase touch distinct
+// 16-byte bank groups (chunk index mod 16; a 512-byte row spans two bank
+// cycles).  The swizzle XORs the low four chunk bits with a per-row value that
+// is (a) a bijection on any 16 consecutive aligned rows, so the row-per-lane
+// operand (16 rows at one logical chunk per phase) is conflict free, and
+// (b) distinct in bits 2-3 on any 4 consecutive aligned rows, so a transposed
+// read (4 rows x 4 consecutive chunks per 16-lane group) covers all 16 groups.
 constexpr int kTileKeys = 32;
 constexpr int kTileRow = 512;
 constexpr int kTileBytes = kTileKeys * kTileRow;   // 16 KiB
 
-__device__ __forceinline__ int tile_swz(int k) { return ((k & 3) << 1) | ((k >> 2) & 1); }
+__host__ __device__ inline int tile_swz(int k) { return ((k & 3) << 2) | ((k >> 2) & 3); }
 
-// Lane-constant byte offsets for reading a tile.  For the row-per-lane
-// operand (lane supplies row l32, 16-byte chunk 2*ks + h) the swizzle only
-// touches the low three chunk bits, so the offset is row_off[ks & 3] +
-// 128 * (ks >> 2).  For the transposed operand (tile_col8) every row a lane
-// names is congruent to 4h + s/4 modulo 8, so its swizzle is also constant;
-// the offset is col_off[db & 1] + 128 * (db >> 1) + 512 * (row group start).
+// Lane-constant byte offsets for reading a tile.  Row-per-lane operand (lane
+// supplies row l32, 16-byte chunk 2*ks + h): the swizzle touches the low four
+// chunk bits only, so the offset is row_off[ks & 7] + 256 * (ks >> 3).
+// Transposed operand (tile_col8, rows r + 4h + s/4 for a row-group start r,
+// a multiple of 8): the row's swizzle depends on the lane and on bit 3 of r,
+// so the offset is col_off[(r >> 3) & 1][db & 3] + 256 * (db >> 2) + 512 * r.
 struct TileOffsets {
-  int row_off[4];
-  int col_off[2];
+  int row_off[8];
+  int col_off[2][4];
 };
 
-__device__ __forceinline__ TileOffsets tile_offsets(int lane) {
+__host__ __device__ inline TileOffsets tile_offsets(int lane) {
   TileOffsets o;
   const int l32 = lane & 31, h = lane >> 5;
   const int sw = tile_swz(l32);
 #pragma unroll
-  for (int q = 0; q < 4; ++q) o.row_off[q] = l32 * kTileRow + (((2 * q + h) ^ sw) << 4);
+  for (int q = 0; q < 8; ++q) o.row_off[q] = l32 * kTileRow + (((2 * q + h) ^ sw) << 4);
   const int s = lane & 15;
   const int x = 2 * ((lane >> 4) & 1) + ((s & 3) >> 1);   // chunk of the 4 columns, mod 4
   const int row = 4 * h + (s >> 2);
-  const int swc = tile_swz(row);
-  const int base = row * kTileRow + ((s & 1) << 3);
-  o.col_off[0] = base + ((x ^ swc) << 4);
-  o.col_off[1] = base + (((4 + x) ^ swc) << 4);
+#pragma unroll
+  for (int par = 0; par < 2; ++par) {
+    const int swc = tile_swz(row + 8 * par);
+#pragma unroll
+    for (int d = 0; d < 4; ++d)
+      o.col_off[par][d] = row * kTileRow + ((s & 1) << 3) + (((4 * d + x) ^ swc) << 4);
+  }
   return o;
 }
 
 // Operand with one key row per lane: row l32, chunk 2*ks + h.
 __device__ __forceinline__ bf16x8 tile_row16(const char* tile, const TileOffsets& o, int ks) {
-  return *reinterpret_cast<const bf16x8*>(tile + o.row_off[ks & 3] + 128 * (ks >> 2));
+  return *reinterpret_cast<const bf16x8*>(tile + o.row_off[ks & 7] + 256 * (ks >> 3));
 }
 
 // Operand with one column per lane and eight keys along k (transposed read):
@@ -125,11 +134,19 @@ __device__ __forceinline__ bf16x8 tile_row16(const char* tile, const TileOffsets
 // columns, and lane i of the group receives column i of the four rows.
 __device__ __forceinline__ bf16x8 tile_col8(const char* tile, const TileOffsets& o, int db, int r0,
                                             int r1) {
-  const char* p = tile + o.col_off[db & 1] + 128 * (db >> 1);
-  const i16x4 a = __builtin_amdgcn_ds_read_tr16_b64_v4i16(LS_LDS4(p + r0 * kTileRow));
-  const i16x4 b = __builtin_amdgcn_ds_read_tr16_b64_v4i16(LS_LDS4(p + r1 * kTileRow));
+  const char* p = tile + 256 * (db >> 2);
+  const i16x4 a = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      LS_LDS4(p + o.col_off[(r0 >> 3) & 1][db & 3] + r0 * kTileRow));
+  const i16x4 b = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      LS_LDS4(p + o.col_off[(r1 >> 3) & 1][db & 3] + r1 * kTileRow));
   return __builtin_bit_cast(bf16x8, __builtin_shufflevector(a, b, 0, 1, 2, 3, 4, 5, 6, 7));
 }
+
+// Scheduling fence placed after every MFMA of an operand pipeline: LDS reads
+// and MFMAs keep their source order (VALU and SALU work may still move across),
+// so operand reads issued a fixed number of MFMAs ahead stay ahead and each
+// MFMA waits only for its own operand (a partial LDS wait).
+__device__ __forceinline__ void mfma_fence() { __builtin_amdgcn_sched_barrier(0x0006); }
 
 // Max of x over the two lane halves (lane l and l ^ 32) without LDS traffic.
 __device__ __forceinline__ float half_max(float x) {
@@ -158,20 +175,50 @@ __device__ __forceinline__ int64_t phys_pos_uniform(const int32_t* table, int64_
   return ((int64_t)t[j >> log2_page] << log2_page) | (j & ((int64_t(1) << log2_page) - 1));
 }
 
+// Page-table entries for the tile loops, read one iteration ahead of use.  A
+// scalar load shares the LDS wait counter and may return out of order, so
+// while one is in flight every LDS wait becomes a wait for all LDS reads; a
+// buffer load is vector memory and leaves LDS waits partial.  Its result is
+// made wave-uniform with readfirstlane (all lanes load the same entry).
+struct PageLookup {
+  __amdgpu_buffer_rsrc_t rsrc;
+  int log2_page;
+  __device__ __forceinline__ void init(const int32_t* table, int lp) {
+    rsrc = __builtin_amdgcn_make_buffer_rsrc(const_cast<int32_t*>(table), (short)0, 0x7FFFFFFF,
+                                             0x00020000);
+    log2_page = lp;
+  }
+  // raw entry for logical position j (a VGPR; consume with row())
+  __device__ __forceinline__ int32_t load(int64_t j) const {
+    return __builtin_amdgcn_raw_buffer_load_b32(rsrc, (int)(j >> log2_page) * 4, 0, 0);
+  }
+  __device__ __forceinline__ int64_t row(int32_t entry, int64_t j) const {
+    return ((int64_t)__builtin_amdgcn_readfirstlane(entry) << log2_page) |
+           (j & ((int64_t(1) << log2_page) - 1));
+  }
+};
+
 // Direct global->LDS loads of the key rows [t0, t0 + 32) of one KV head into
 // a tile (swizzled layout above).  Each wave writes rows 8w .. 8w+7 with four
 // 1 KiB instructions: lane l of instruction i carries row 8w + 2i + l/32,
-// physical chunk l % 32 (logical chunk (l % 32) ^ tile_swz(row)).  Rows at or
-// beyond k_hi repeat row k_hi - 1.  Completion is tracked by vmcnt.
+// physical chunk l % 32 (logical chunk (l % 32) ^ tile_swz(row)).  Completion
+// is tracked by vmcnt.
+//
+// Tiles inside one page use buffer loads (MUBUF) with the page's first row as
+// the resource base and 32-bit lane offsets.  Unlike the FLAT-encoded
+// global_load_lds, these do not count as possible out-of-order LDS accesses
+// for the compiler's wait insertion, so LDS reads issued while they are in
+// flight keep partial waits.  Pages shorter than a tile use the per-row FLAT
+// form.
 struct TileFetch {
   const char* pool;    // pool base + KV head offset (bytes)
   int64_t row_bytes;   // bytes between positions
-  int64_t lane_off[4]; // row * row_bytes + chunk * 16 for the lane's 4 rows
+  int lane_off[4];     // byte offset (logical chunk * 16) of the lane's source in its row
   int lds_row[4];      // first LDS row written by instruction i
   int lane_row[4];     // row carried by this lane in instruction i
 
-  __device__ __forceinline__ void init(const void* pool_head, int64_t pos_stride_elems, int lane,
-                                       int w) {
+  __host__ __device__ inline void init(const void* pool_head, int64_t pos_stride_elems, int lane,
+                                        int w) {
     pool = static_cast<const char*>(pool_head);
     row_bytes = pos_stride_elems * 2;
 #pragma unroll
@@ -182,13 +229,20 @@ struct TileFetch {
     }
   }
 
-  // Whole tile inside one page, whose physical row for t0 is `prow` (wave-uniform).
-  __device__ __forceinline__ void issue_page(char* tile, int64_t prow) const {
-    const char* src = pool + prow * row_bytes;
+  // Tile inside one page, whose physical row for t0 is `prow` (wave-uniform);
+  // rows at or beyond n_valid (1 <= n_valid <= 32) repeat row n_valid - 1.
+  // Straight-line code: every call issues exactly four loads, which the
+  // compiler's wait insertion relies on to keep the waits of later loads of
+  // the same wave partial.
+  __device__ __forceinline__ void issue_page(char* tile, int64_t prow, int n_valid) const {
+    const __amdgpu_buffer_rsrc_t r = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<char*>(pool + prow * row_bytes), (short)0, 0x7FFFFFFF, 0x00020000);
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
-      __builtin_amdgcn_global_load_lds(src + lane_row[i] * row_bytes + lane_off[i],
-                                       LS_LDS(tile + lds_row[i] * kTileRow), 16, 0, 0);
+    for (int i = 0; i < 4; ++i) {
+      const int off = (int)(min(lane_row[i], n_valid - 1) * row_bytes) + lane_off[i];
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(r, LS_LDS(tile + lds_row[i] * kTileRow), 16, off, 0,
+                                               0, 0);
+    }
   }
 
   // Any tile: one page-table lookup per row; rows at or beyond k_hi repeat k_hi - 1.
@@ -202,9 +256,36 @@ struct TileFetch {
                                        LS_LDS(tile + lds_row[i] * kTileRow), 16, 0, 0);
     }
   }
+
+  // Tile [t0, t0 + 32) with k_hi > t0: page path unless pages are shorter than a tile.
+  template <bool kPerKey>
+  __device__ __forceinline__ void issue(char* tile, const int32_t* table, int log2_page, int64_t t0,
+                                        int64_t k_hi, int64_t prow) const {
+    if (kPerKey) {
+      issue_rows(tile, table, log2_page, t0, k_hi);
+    } else {
+      issue_page(tile, prow, (int)min(k_hi - t0, (int64_t)kTileKeys));
+    }
+  }
 };
 
 // Wait for this wave's direct loads (vmcnt = 0).
 __device__ __forceinline__ void wait_fetch() { __builtin_amdgcn_s_waitcnt(0x0F70); }
+
+// Wait until at most one K+V stage of this wave's direct loads is in flight
+// (vmcnt = 8: a stage is 4 K and 4 V instructions per wave, and they are the
+// newest vector-memory operations when this is reached).
+__device__ __forceinline__ void wait_fetch_but_newest_stage() { __builtin_amdgcn_s_waitcnt(0x0F78); }
+
+// Workgroup barrier without the release/acquire fence of __syncthreads: that
+// fence counts the direct loads as LDS writes and would wait for every one in
+// flight.  The empty asm statements keep the compiler from moving memory
+// operations across the barrier; each wave's own waitcnt before it decides
+// which loads have landed.
+__device__ __forceinline__ void tile_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
 
 }  // namespace ls

@@ -8,8 +8,8 @@
 // Key lists are resolved to physical latent rows once per call.  A workgroup
 // owns one token, lanes own heads (scores computed transposed, S^T = K Q^T).
 // Gathered rows (1152 bytes) stream by direct global->LDS loads into a
-// three-slot ring; 16-byte chunks are XOR-swizzled inside aligned 8-chunk
-// groups so row reads and transposing column reads are bank-conflict free.
+// three-slot ring; 16-byte chunks are permuted inside aligned 8-chunk groups
+// so row reads and transposing column reads are bank-conflict free.
 // The forward kernel is in sparse_fwd.hip, the dq backward in sparse_bwd.hip.
 #pragma once
 #include <math.h>
@@ -28,26 +28,42 @@ constexpr int kTile = kKeys * kRow;           // 36 KiB
 constexpr int kSlots = 3;
 constexpr int kChunks = kRow / 16;            // 72
 
-// Lane-constant LDS offsets for a 1152-byte-row tile (see mfma_common.h for
-// the 512-byte version: the swizzle acts inside aligned 8-chunk groups).
+// Chunk swizzle of a 1152-byte-row tile: chunk c of row k is stored at
+// (c & ~7) | ((c & 7) ^ s_swz(k)), a permutation inside each aligned 8-chunk
+// group (72 chunks = 9 groups, so no chunk leaves its row).  With 64 four-byte
+// banks an odd row starts 128 bytes (8 chunks) into the bank cycle, so a
+// chunk's bank group (16 bytes, mod 16) is its in-group position plus 8 for odd
+// rows.  s_swz is a bijection on the even and on the odd rows of any 16
+// consecutive aligned rows (row-per-lane reads, 16 lanes per phase, are
+// conflict free) and its bit 2 differs between the two even and between the
+// two odd rows of any 4 consecutive aligned rows (a transposed read's 4 rows x
+// 4 chunks cover all 16 bank groups).
+__host__ __device__ inline int s_swz(int k) { return (((k >> 1) & 1) << 2) | ((k >> 2) & 3); }
+
+// Lane-constant LDS offsets: row operand row_off[ks & 3] + 128 * (ks >> 2);
+// transposed operand col_off[(r >> 3) & 1][db & 1] + 128 * (db >> 1) + kRow * r
+// for a row-group start r (a multiple of 8).
 struct SOffsets {
   int row_off[4];
-  int col_off[2];
+  int col_off[2][2];
 };
 
-__device__ __forceinline__ SOffsets s_offsets(int lane) {
+__host__ __device__ inline SOffsets s_offsets(int lane) {
   SOffsets o;
   const int l32 = lane & 31, h = lane >> 5;
-  const int sw = tile_swz(l32);
+  const int sw = s_swz(l32);
 #pragma unroll
   for (int q = 0; q < 4; ++q) o.row_off[q] = l32 * kRow + (((2 * q + h) ^ sw) << 4);
   const int s = lane & 15;
   const int x = 2 * ((lane >> 4) & 1) + ((s & 3) >> 1);
   const int row = 4 * h + (s >> 2);
-  const int swc = tile_swz(row);
   const int base = row * kRow + ((s & 1) << 3);
-  o.col_off[0] = base + ((x ^ swc) << 4);
-  o.col_off[1] = base + (((4 + x) ^ swc) << 4);
+#pragma unroll
+  for (int par = 0; par < 2; ++par) {
+    const int swc = s_swz(row + 8 * par);
+    o.col_off[par][0] = base + ((x ^ swc) << 4);
+    o.col_off[par][1] = base + (((4 + x) ^ swc) << 4);
+  }
   return o;
 }
 
@@ -59,9 +75,11 @@ __device__ __forceinline__ bf16x8 s_row16(const char* tile, const SOffsets& o, i
 // Transposed operand: lane l = 32h + c gets column 32*db + c of rows
 // r0 + 4h + {0..3} and r1 + 4h + {0..3} (r0, r1 multiples of 8).
 __device__ __forceinline__ bf16x8 s_col8(const char* tile, const SOffsets& o, int db, int r0, int r1) {
-  const char* p = tile + o.col_off[db & 1] + 128 * (db >> 1);
-  const i16x4 a = __builtin_amdgcn_ds_read_tr16_b64_v4i16(LS_LDS4(p + r0 * kRow));
-  const i16x4 b = __builtin_amdgcn_ds_read_tr16_b64_v4i16(LS_LDS4(p + r1 * kRow));
+  const char* p = tile + 128 * (db >> 1);
+  const i16x4 a = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      LS_LDS4(p + o.col_off[(r0 >> 3) & 1][db & 1] + r0 * kRow));
+  const i16x4 b = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      LS_LDS4(p + o.col_off[(r1 >> 3) & 1][db & 1] + r1 * kRow));
   return __builtin_bit_cast(bf16x8, __builtin_shufflevector(a, b, 0, 1, 2, 3, 4, 5, 6, 7));
 }
 
@@ -72,11 +90,12 @@ __device__ __forceinline__ bf16x8 s_col8(const char* tile, const SOffsets& o, in
 // rather than kept in registers.
 struct SFetch {
   int q0;   // (9w) * 64 + lane
-  __device__ __forceinline__ void init(int lane, int w) { q0 = 9 * w * 64 + lane; }
-  __device__ __forceinline__ int row(int i) const { return (q0 + 64 * i) / kChunks; }
-  __device__ __forceinline__ int coff(int i) const {
+  __host__ __device__ inline void init(int lane, int w) { q0 = 9 * w * 64 + lane; }
+  __host__ __device__ inline int row(int i) const { return (q0 + 64 * i) / kChunks; }
+  __host__ __device__ inline int coff(int i) const {
     const int q = q0 + 64 * i, r = q / kChunks;
-    return ((q - r * kChunks) ^ tile_swz(r)) * 16;
+    const int c = q - r * kChunks;
+    return ((c & ~7) | ((c & 7) ^ s_swz(r))) * 16;
   }
   // phys rows of this lane's 9 chunks for tile T (from the resolved key list)
   __device__ __forceinline__ void rows_of(const int32_t* __restrict__ phys_t, int T,

@@ -1,0 +1,159 @@
+// Host-side model check of the LDS tile layouts used by the MFMA kernels.
+//
+// The direct global->LDS loads (TileFetch, SFetch) are replayed on the CPU to
+// fill a model tile with the logical (row, column) index of every bf16 slot;
+// then every lane offset the kernels read through (tile_offsets/tile_row16/
+// tile_col8 and s_offsets/s_row16/s_col8) must return the elements the MFMA
+// operand layout asks for, and every read must be bank-conflict free under the
+// gfx950 LDS model: 64 banks of 4 bytes, 16-byte reads served 16 lanes per
+// phase, 8-byte transposing reads 32 lanes per phase.  The transposing read
+// delivers, in each 16-lane group, to lane i the column i of the four rows
+// named by source lanes 4j + i/4 (element i % 4 of each).
+#include <stdio.h>
+#include <stdlib.h>
+
+#include <vector>
+
+#include "mfma_common.h"
+#include "sparse_common.h"
+
+static int failures = 0;
+#define CHECK(cond, ...)                         \
+  do {                                           \
+    if (!(cond)) {                               \
+      if (failures < 20) {                       \
+        printf("FAIL %s:%d: ", __FILE__, __LINE__); \
+        printf(__VA_ARGS__);                     \
+        printf("\n");                            \
+      }                                          \
+      ++failures;                                \
+    }                                            \
+  } while (0)
+
+// distinct 16-byte bank groups within each 16-lane phase
+static void check_b128_phases(const int* off, const char* what) {
+  for (int ph = 0; ph < 4; ++ph) {
+    int seen = 0;
+    for (int l = 16 * ph; l < 16 * ph + 16; ++l) {
+      const int g = (off[l] & 255) >> 4;
+      CHECK(!(seen & (1 << g)), "%s: bank conflict in 16-byte read, phase %d lane %d", what, ph, l);
+      seen |= 1 << g;
+    }
+  }
+}
+
+// distinct 8-byte bank pairs within each 32-lane phase
+static void check_b64_phases(const int* off, const char* what) {
+  for (int ph = 0; ph < 2; ++ph) {
+    unsigned seen = 0;
+    for (int l = 32 * ph; l < 32 * ph + 32; ++l) {
+      const int g = (off[l] & 255) >> 3;
+      CHECK(!(seen & (1u << g)), "%s: bank conflict in transposing read, phase %d lane %d", what, ph, l);
+      seen |= 1u << g;
+    }
+  }
+}
+
+// Transposing read: output element j of lane l from the model tile.
+static int tr_elem(const std::vector<int>& tag, const int* src_off, int l, int j) {
+  const int g = l >> 4, i = l & 15;
+  const int src = 16 * g + 4 * j + (i >> 2);
+  return tag[src_off[src] / 2 + (i & 3)];
+}
+
+static void dense() {
+  using namespace ls;
+  const int cols = kTileRow / 2;
+  std::vector<int> tag(kTileBytes / 2, -1);
+  for (int w = 0; w < 4; ++w)
+    for (int lane = 0; lane < 64; ++lane) {
+      TileFetch f;
+      f.init(nullptr, cols, lane, w);
+      for (int i = 0; i < 4; ++i) {
+        const int dst = f.lds_row[i] * kTileRow + 16 * lane;   // 1 KiB per instruction, linear
+        for (int e = 0; e < 8; ++e) {
+          CHECK(tag[dst / 2 + e] == -1, "dense fetch writes slot %d twice", dst / 2 + e);
+          tag[dst / 2 + e] = f.lane_row[i] * cols + (int)(f.lane_off[i] / 2) + e;
+        }
+      }
+    }
+  for (int v : tag) CHECK(v >= 0, "dense fetch leaves a slot unwritten");
+
+  TileOffsets o[64];
+  for (int l = 0; l < 64; ++l) o[l] = tile_offsets(l);
+  for (int ks = 0; ks < 16; ++ks) {
+    int off[64];
+    for (int l = 0; l < 64; ++l) {
+      off[l] = o[l].row_off[ks & 7] + 256 * (ks >> 3);
+      const int row = l & 31, c0 = 16 * ks + 8 * (l >> 5);
+      for (int e = 0; e < 8; ++e)
+        CHECK(tag[off[l] / 2 + e] == row * cols + c0 + e, "dense row operand ks=%d lane=%d e=%d", ks, l, e);
+    }
+    check_b128_phases(off, "dense row operand");
+  }
+  for (int db = 0; db < 8; ++db)
+    for (int r = 0; r < 32; r += 8) {
+      int off[64];
+      for (int l = 0; l < 64; ++l) off[l] = 256 * (db >> 2) + o[l].col_off[(r >> 3) & 1][db & 3] + r * kTileRow;
+      for (int l = 0; l < 64; ++l)
+        for (int j = 0; j < 4; ++j) {
+          const int want = (r + 4 * (l >> 5) + j) * cols + 32 * db + (l & 31);
+          CHECK(tr_elem(tag, off, l, j) == want, "dense transposed operand db=%d r=%d lane=%d j=%d", db, r, l, j);
+        }
+      check_b64_phases(off, "dense transposed operand");
+    }
+}
+
+static void sparse() {
+  using namespace ls::sparse;
+  const int cols = kRow / 2;
+  std::vector<int> tag(kTile / 2, -1);
+  for (int w = 0; w < 4; ++w)
+    for (int lane = 0; lane < 64; ++lane) {
+      SFetch f;
+      f.init(lane, w);
+      for (int i = 0; i < 9; ++i) {
+        const int dst = (9 * w + i) * 1024 + 16 * lane;
+        for (int e = 0; e < 8; ++e) {
+          CHECK(tag[dst / 2 + e] == -1, "sparse fetch writes slot %d twice", dst / 2 + e);
+          tag[dst / 2 + e] = f.row(i) * cols + f.coff(i) / 2 + e;
+        }
+      }
+    }
+  for (int v : tag) CHECK(v >= 0, "sparse fetch leaves a slot unwritten");
+
+  SOffsets o[64];
+  for (int l = 0; l < 64; ++l) o[l] = s_offsets(l);
+  for (int ks = 0; ks < 36; ++ks) {
+    int off[64];
+    for (int l = 0; l < 64; ++l) {
+      off[l] = o[l].row_off[ks & 3] + 128 * (ks >> 2);
+      const int row = l & 31, c0 = 16 * ks + 8 * (l >> 5);
+      for (int e = 0; e < 8; ++e)
+        CHECK(tag[off[l] / 2 + e] == row * cols + c0 + e, "sparse row operand ks=%d lane=%d e=%d", ks, l, e);
+    }
+    check_b128_phases(off, "sparse row operand");
+  }
+  for (int db = 0; db < 18; ++db)
+    for (int r = 0; r < 32; r += 8) {
+      int off[64];
+      for (int l = 0; l < 64; ++l) off[l] = 128 * (db >> 1) + o[l].col_off[(r >> 3) & 1][db & 1] + r * kRow;
+      for (int l = 0; l < 64; ++l)
+        for (int j = 0; j < 4; ++j) {
+          const int want = (r + 4 * (l >> 5) + j) * cols + 32 * db + (l & 31);
+          CHECK(tr_elem(tag, off, l, j) == want, "sparse transposed operand db=%d r=%d lane=%d j=%d", db, r, l, j);
+        }
+      check_b64_phases(off, "sparse transposed operand");
+    }
+}
+
+int main() {
+  dense();
+  sparse();
+  if (failures) {
+    printf("%d failures\n", failures);
+    return 1;
+  }
+  printf("lds layouts ok\n");
+  return 0;
+}
