@@ -38,16 +38,19 @@ constexpr int kQSlots = kQAhead + 2;
 constexpr int kSDAhead = 3;   // steps of (K row, V row) reads in flight
 constexpr int kKTAhead = 4;   // transposed K operands in flight (two reads each)
 
-// S^T = K Q^T and dP^T = V dO^T for one 32-key tile.
+// S^T = K Q^T and dP^T = V dO^T for one 32-key tile.  After step ks < 8,
+// load(ks) issues one instruction of the next stage's direct loads.
+template <typename Load>
 __device__ __forceinline__ void scores_dp(const char* Ks, const char* Vs, const bf16x8* qreg,
                                           const bf16x8* dreg, const TileOffsets& o, f32x16& s,
-                                          f32x16& dp) {
+                                          f32x16& dp, Load&& load) {
   bf16x8 kr[16], vr[16];
 #pragma unroll
   for (int i = 0; i < kSDAhead; ++i) {
     kr[i] = tile_row16(Ks, o, i);
     vr[i] = tile_row16(Vs, o, i);
   }
+  mfma_fence();
   s = zero16();
   dp = zero16();
 #pragma unroll
@@ -58,6 +61,7 @@ __device__ __forceinline__ void scores_dp(const char* Ks, const char* Vs, const 
     }
     s = mfma32(kr[ks], qreg[ks], s);
     dp = mfma32(vr[ks], dreg[ks], dp);
+    if (ks < 8) load(ks);
     mfma_fence();
   }
 }
@@ -93,13 +97,22 @@ __device__ __forceinline__ void dq_step(const BwdArgs& a, char* __restrict__ nex
                                         const bf16x8* qreg, const bf16x8* dreg,
                                         const TileOffsets& to, int hh, float lse2, float delta,
                                         f32x16* acc, bf16x8& d0, bf16x8& d1) {
-  const int64_t prow_next = kPerKey ? 0 : pl.row(pe, t0_next);
-  if (!kPerKey) pe = pl.load(t0_after);
-  __builtin_amdgcn_sched_barrier(0);   // the entry load stays ahead of the stage's loads
-  kf.issue<kPerKey>(next, a.page_table, a.log2_page, t0_next, k_hi, prow_next);
-  vf.issue<kPerKey>(next + kTileBytes, a.page_table, a.log2_page, t0_next, k_hi, prow_next);
   f32x16 s, dp;
-  scores_dp(cur, cur + kTileBytes, qreg, dreg, to, s, dp);
+  if (kPerKey) {
+    kf.issue_rows(next, a.page_table, a.log2_page, t0_next, k_hi);
+    vf.issue_rows(next + kTileBytes, a.page_table, a.log2_page, t0_next, k_hi);
+    scores_dp(cur, cur + kTileBytes, qreg, dreg, to, s, dp, [](int) {});
+  } else {
+    const int64_t prow_next = pl.row(pe, t0_next);
+    pe = pl.load(t0_after);
+    __builtin_amdgcn_sched_barrier(0);   // the entry load stays ahead of the stage's loads
+    const __amdgpu_buffer_rsrc_t rk = kf.page_rsrc(prow_next), rv = vf.page_rsrc(prow_next);
+    const int nv = (int)min(k_hi - t0_next, (int64_t)kQBN);
+    scores_dp(cur, cur + kTileBytes, qreg, dreg, to, s, dp, [&](int i) {
+      if (i < 4) kf.issue_one(next, rk, i, nv);
+      else vf.issue_one(next + kTileBytes, rv, i - 4, nv);
+    });
+  }
   const bool edge = t0 < kb || t0 + kQBN > k_all;
 #pragma unroll
   for (int r = 0; r < 16; ++r) {
@@ -119,7 +132,8 @@ template <bool kPerKey>
 __global__ __launch_bounds__(256, 1) void bwd_dq_bf16_d256_kernel(BwdArgs a) {
   __shared__ __attribute__((aligned(1024))) char smem[kQSlots * kQStage];
 
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave-uniform (scalar)
   const int l32 = lane & 31, hh = lane >> 5;
   const int g = blockIdx.y;
   const int lg = a.log2_group;

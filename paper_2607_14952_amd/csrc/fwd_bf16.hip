@@ -38,16 +38,22 @@ constexpr int kSlots = kAhead + 2;          // + the tile being scored + the V o
 constexpr int kKAhead = 6;   // K operand reads in flight (16-byte reads)
 constexpr int kVAhead = 4;   // V operands in flight (two transposing reads each)
 
-// S^T (32 keys x this lane's row) = K Q^T over the 256-wide head.
-__device__ __forceinline__ f32x16 scores(const char* Ks, const bf16x8* qreg, const TileOffsets& o) {
+// S^T (32 keys x this lane's row) = K Q^T over the 256-wide head.  After
+// MFMA ks < 8, load(ks) issues one instruction of the next stage's direct
+// loads, so their issue overlaps the MFMA chain.
+template <typename Load>
+__device__ __forceinline__ f32x16 scores(const char* Ks, const bf16x8* qreg, const TileOffsets& o,
+                                         Load&& load) {
   bf16x8 kreg[16];
 #pragma unroll
   for (int i = 0; i < kKAhead; ++i) kreg[i] = tile_row16(Ks, o, i);
+  mfma_fence();
   f32x16 s = zero16();
 #pragma unroll
   for (int ks = 0; ks < 16; ++ks) {
     if (ks + kKAhead < 16) kreg[ks + kKAhead] = tile_row16(Ks, o, ks + kKAhead);
     s = mfma32(kreg[ks], qreg[ks], s);
+    if (ks < 8) load(ks);
     mfma_fence();
   }
   return s;
@@ -120,12 +126,22 @@ __device__ __forceinline__ float step(const FwdArgs& a, char* __restrict__ next,
                                       const bf16x8* qreg, const TileOffsets& to, int hh,
                                       f32x16* oacc, bf16x8& p0, bf16x8& p1, float& m_run,
                                       float& l_run) {
-  const int64_t prow_next = kPerKey ? 0 : pl.row(pe, t0_next);
-  if (!kPerKey) pe = pl.load(t0_after);
-  __builtin_amdgcn_sched_barrier(0);   // the entry load stays ahead of the stage's loads
-  kf.issue<kPerKey>(next, a.page_table, a.log2_page, t0_next, k_hi, prow_next);
-  vf.issue<kPerKey>(next + kTileBytes, a.page_table, a.log2_page, t0_next, k_hi, prow_next);
-  f32x16 s = scores(ks_cur, qreg, to);
+  f32x16 s;
+  if (kPerKey) {
+    kf.issue_rows(next, a.page_table, a.log2_page, t0_next, k_hi);
+    vf.issue_rows(next + kTileBytes, a.page_table, a.log2_page, t0_next, k_hi);
+    s = scores(ks_cur, qreg, to, [](int) {});
+  } else {
+    const int64_t prow_next = pl.row(pe, t0_next);
+    pe = pl.load(t0_after);
+    __builtin_amdgcn_sched_barrier(0);   // the entry load stays ahead of the stage's loads
+    const __amdgpu_buffer_rsrc_t rk = kf.page_rsrc(prow_next), rv = vf.page_rsrc(prow_next);
+    const int nv = (int)min(k_hi - t0_next, (int64_t)kBN);
+    s = scores(ks_cur, qreg, to, [&](int i) {
+      if (i < 4) kf.issue_one(next, rk, i, nv);
+      else vf.issue_one(next + kTileBytes, rv, i - 4, nv);
+    });
+  }
   if (t0 < kb || t0 + kBN > k_all) mask_tile(s, t0, kb, my_lim, hh);
   const float alpha = softmax_tile(s, a.scale_log2, m_run, l_run);
   if (!kFirst) pv(vs_prev, p0, p1, oacc, to);
@@ -138,7 +154,8 @@ template <bool kPerKey>
 __global__ __launch_bounds__(256, 1) void fwd_bf16_d256_kernel(FwdArgs a) {
   __shared__ __attribute__((aligned(1024))) char smem[kSlots * kStage];
 
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave-uniform (scalar)
   const int l32 = lane & 31, hh = lane >> 5;
   const int g = blockIdx.y, sp = blockIdx.z;
   const int lg = a.log2_group;

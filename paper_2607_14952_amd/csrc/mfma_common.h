@@ -229,20 +229,30 @@ struct TileFetch {
     }
   }
 
-  // Tile inside one page, whose physical row for t0 is `prow` (wave-uniform);
-  // rows at or beyond n_valid (1 <= n_valid <= 32) repeat row n_valid - 1.
-  // Straight-line code: every call issues exactly four loads, which the
-  // compiler's wait insertion relies on to keep the waits of later loads of
-  // the same wave partial.
+  // Buffer resource whose base is physical row `prow` (wave-uniform).
+  __device__ __forceinline__ __amdgpu_buffer_rsrc_t page_rsrc(int64_t prow) const {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>(pool + prow * row_bytes), (short)0,
+                                             0x7FFFFFFF, 0x00020000);
+  }
+
+  // Load instruction i (0..3) of a tile inside one page (resource from
+  // page_rsrc of its first row); rows at or beyond n_valid (1 <= n_valid <= 32)
+  // repeat row n_valid - 1.  32 rows of a page span less than 2 GiB, so the
+  // lane offsets are 32-bit.
+  __device__ __forceinline__ void issue_one(char* tile, __amdgpu_buffer_rsrc_t r, int i,
+                                            int n_valid) const {
+    const int off = min(lane_row[i], n_valid - 1) * (int)row_bytes + lane_off[i];
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, LS_LDS(tile + lds_row[i] * kTileRow), 16, off, 0, 0,
+                                             0);
+  }
+
+  // Whole tile inside one page, in straight-line code: every call issues
+  // exactly four loads, which the compiler's wait insertion relies on to keep
+  // the waits of later loads of the same wave partial.
   __device__ __forceinline__ void issue_page(char* tile, int64_t prow, int n_valid) const {
-    const __amdgpu_buffer_rsrc_t r = __builtin_amdgcn_make_buffer_rsrc(
-        const_cast<char*>(pool + prow * row_bytes), (short)0, 0x7FFFFFFF, 0x00020000);
+    const __amdgpu_buffer_rsrc_t r = page_rsrc(prow);
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int off = (int)(min(lane_row[i], n_valid - 1) * row_bytes) + lane_off[i];
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(r, LS_LDS(tile + lds_row[i] * kTileRow), 16, off, 0,
-                                               0, 0);
-    }
+    for (int i = 0; i < 4; ++i) issue_one(tile, r, i, n_valid);
   }
 
   // Any tile: one page-table lookup per row; rows at or beyond k_hi repeat k_hi - 1.
