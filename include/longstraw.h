@@ -44,8 +44,9 @@
  *   undefined behaviour.
  *
  * Supported shapes: dtype LS_F32 with head_dim, head_dim_v <= 256 (any GQA
- * group); dtype LS_BF16 with head_dim = head_dim_v = 256 and n_q_heads /
- * n_kv_heads dividing 32.
+ * group); dtype LS_BF16 with head_dim = head_dim_v = 256, n_q_heads /
+ * n_kv_heads dividing 32, n_q * n_q_heads * 512 < 2^31 bytes of queries and
+ * fewer than 2^29 logical pages (the kernels use 32-bit buffer offsets).
  */
 #ifndef LONGSTRAW_H
 #define LONGSTRAW_H
@@ -184,7 +185,9 @@ size_t ls_prefix_attn_bwd_workspace_size(const ls_attn_params* p);
  *              (Eq. gradient-boundary and the lazy gradient pages).
  * dk_resp/dv_resp may both be NULL when the range holds no response key.
  * LS_FLAG_ACCUMULATE_DQ / LS_FLAG_ACCUMULATE_DKV select += over =.
- * workspace: device memory of ls_prefix_attn_bwd_workspace_size() bytes.
+ * workspace: device memory of ls_prefix_attn_bwd_workspace_size(p) bytes for
+ *   the same p (it grows with the response length q_pos0 + n_q - prefix_len:
+ *   the bf16 path keeps per-row-chunk dK/dV partial sums there).
  */
 ls_status ls_prefix_attn_bwd(const ls_attn_params* p, int64_t kv_begin, int64_t kv_end,
                              const void* d_out, const void* out, int32_t out_dtype,

@@ -227,9 +227,11 @@ def lse_merge(out_part, lse_part, *, out_dtype=None, out=None, lse=None, flags: 
     return out, lse
 
 
-def bwd_workspace(q, kv: PagedKV, **kw):
+def bwd_workspace(q, kv: PagedKV, *, prefix_len: int, q_pos0: int):
+    """Workspace for ls_prefix_attn_bwd calls with these rows, prefix_len and
+    q_pos0 (also large enough for any call with a smaller q_pos0)."""
     torch = _torch()
-    p = make_params(q, kv, prefix_len=0, q_pos0=0, scale=1.0)
+    p = make_params(q, kv, prefix_len=prefix_len, q_pos0=q_pos0, scale=1.0)
     n = load_library().ls_prefix_attn_bwd_workspace_size(ctypes.byref(p))
     return torch.empty(max(n, 16), dtype=torch.uint8, device=q.device)
 
@@ -254,7 +256,7 @@ def prefix_attn_bwd(q, kv: PagedKV, d_out, out, lse, *, prefix_len: int, q_pos0:
         if dv_resp is None:
             dv_resp = torch.zeros((n_resp, Hkv, Dv), dtype=torch.float32, device=q.device)
     if workspace is None:
-        workspace = bwd_workspace(q, kv)
+        workspace = bwd_workspace(q, kv, prefix_len=prefix_len, q_pos0=q_pos0)
     p = make_params(q, kv, prefix_len=prefix_len, q_pos0=q_pos0, scale=scale, flags=flags,
                     expected_epoch=expected_epoch)
     check(load_library().ls_prefix_attn_bwd(

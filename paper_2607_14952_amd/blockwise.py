@@ -108,8 +108,9 @@ class BlockwiseReplay:
         B.lse_merge(op, lp, out=out, lse=lse, stream=self.stream)
         if keep is not None:
             keep[b] = (out.clone(), lse.clone())
-        if self.ws is None:
-            self.ws = B.bwd_workspace(q[:c.rows_per_call], self.prefix.kv)
+        if self.ws is None:   # sized for the block with the most response keys (highest q_pos0)
+            self.ws = B.bwd_workspace(q[:c.rows_per_call], self.prefix.kv, prefix_len=c.prefix_len,
+                                      q_pos0=c.prefix_len + (c.blocks - 1) * c.rows_per_call)
         dq = self.dq[rows]
         for r, (kb, ke) in enumerate(self.prefix_ranges + [(c.prefix_len, kv_end)]):
             B.prefix_attn_bwd(qb, self.prefix.kv, dob, out, lse, prefix_len=c.prefix_len,

@@ -121,6 +121,11 @@ ls_status check_supported(const ls_attn_params* p) {
                 p->head_dim, p->head_dim_v);
   if (!is_pow2(G) || G > 32)
     return fail(LS_ERR_UNSUPPORTED, "bf16 path needs a GQA group dividing 32 (got %d)", G);
+  // the kernels address query-side arrays and the page table with 32-bit offsets
+  if ((int64_t)p->n_q * p->n_q_heads * p->head_dim * 2 >= (int64_t(1) << 31))
+    return fail(LS_ERR_UNSUPPORTED, "bf16 path: n_q * n_q_heads * head_dim * 2 must be < 2^31");
+  if (p->n_logical_pages >= (int64_t(1) << 29))
+    return fail(LS_ERR_UNSUPPORTED, "bf16 path: n_logical_pages must be < 2^29");
   return LS_OK;
 }
 
@@ -329,11 +334,29 @@ LS_API ls_status ls_lse_merge(const float* out_part, const float* lse_part, int3
   return e == hipSuccess ? LS_OK : hip_fail(e, "merge launch");
 }
 
+namespace {
+// Backward workspace: Delta and lse * log2(e), both [Hq, n_q] fp32 and padded
+// to 256 bytes, then (bf16 path) the dk/dv partials of the row chunks,
+// [chunks, 2, Hkv, kv_len - prefix_len, D] fp32.
+struct BwdWorkspace {
+  size_t stat_bytes, part_bytes;
+  size_t total() const { return 2 * stat_bytes + part_bytes; }
+};
+
+BwdWorkspace bwd_workspace_layout(const ls_attn_params* p) {
+  BwdWorkspace w{0, 0};
+  if (!p || p->n_q <= 0 || p->n_q_heads <= 0 || p->n_kv_heads <= 0) return w;
+  w.stat_bytes = ((size_t)p->n_q * p->n_q_heads * 4 + 255) / 256 * 256;
+  const int64_t n_resp = p->q_pos0 + p->n_q - p->prefix_len;
+  if (p->dtype == LS_BF16 && n_resp > 0 && p->n_q_heads % p->n_kv_heads == 0)
+    w.part_bytes = (size_t)ls::dkdv_row_chunks(p->n_q, p->n_q_heads / p->n_kv_heads) * 2 *
+                   p->n_kv_heads * (size_t)n_resp * p->head_dim * 4;
+  return w;
+}
+}  // namespace
+
 LS_API size_t ls_prefix_attn_bwd_workspace_size(const ls_attn_params* p) {
-  if (!p || p->n_q <= 0 || p->n_q_heads <= 0) return 0;
-  // delta and lse * log2(e), both [Hq, n_q] fp32, each padded to 256 bytes
-  size_t one = ((size_t)p->n_q * p->n_q_heads * 4 + 255) / 256 * 256;
-  return 2 * one;
+  return bwd_workspace_layout(p).total();
 }
 
 LS_API ls_status ls_prefix_attn_bwd(const ls_attn_params* p, int64_t kv_begin, int64_t kv_end,
@@ -381,9 +404,9 @@ LS_API ls_status ls_prefix_attn_bwd(const ls_attn_params* p, int64_t kv_begin, i
   hipStream_t s = (hipStream_t)stream;
   if ((st = check_pages(p, kv_end, s)) != LS_OK) return st;
 
-  size_t one = need / 2;
+  const BwdWorkspace wl = bwd_workspace_layout(p);
   float* delta = (float*)workspace;
-  float* lse2 = (float*)((char*)workspace + one);
+  float* lse2 = (float*)((char*)workspace + wl.stat_bytes);
   hipError_t e = ls::launch_bwd_prep(d_out, out, p->dtype == LS_BF16, out_dtype == LS_BF16, lse,
                                      p->n_q, p->n_q_heads, p->head_dim_v, delta, lse2, s);
   if (e != hipSuccess) return hip_fail(e, "backward prep launch");
@@ -399,6 +422,7 @@ LS_API ls_status ls_prefix_attn_bwd(const ls_attn_params* p, int64_t kv_begin, i
   a.dq = dq;
   a.dk_resp = dk_resp;
   a.dv_resp = dv_resp;
+  a.dkdv_part = wl.part_bytes ? (float*)((char*)workspace + 2 * wl.stat_bytes) : nullptr;
   a.q_pos0 = p->q_pos0;
   a.prefix_len = p->prefix_len;
   a.kv_begin = kv_begin;

@@ -11,11 +11,12 @@
 // the same K tile.  The dq product of tile t-1 is issued in the same block as
 // the exponentials of tile t.
 //
-// dk/dv kernel: one wave per 32 response keys of one KV head; lane l owns key
-// l % 32.  Per block of 32 packed query rows it computes S = Q K^T and
-// dP = dO V^T (scores untransposed, rows in registers), then
-// dv^T += dO^T P and dk^T += Q^T dS with Q and dO staged row-major and
-// row-transposed in LDS.  Only keys >= prefix_len ever get a gradient.
+// dk/dv kernel: 128 response keys of one KV head per workgroup (lane l of
+// wave w owns key 32w + l % 32) against one chunk of packed query rows; Q and
+// dO row tiles stream through LDS and are read row-wise for S = Q K^T and
+// dP = dO V^T and transposed for dv^T += dO^T P and dk^T += Q^T dS.  Chunk
+// partials are summed by a reduce kernel.  Only keys >= prefix_len ever get a
+// gradient.
 #include <math.h>
 
 #include "ls_internal.h"
@@ -253,146 +254,181 @@ __global__ __launch_bounds__(256, 1) void bwd_dq_bf16_d256_kernel(BwdArgs a) {
 }
 
 // ============================================================== dk/dv kernel
-constexpr int kKB = 32;                       // response keys per wave
-constexpr int kRB = 32;                       // packed query rows per step
-constexpr int kKVBytes = kKB * kRowBytes;     // 16 KiB each for K, V
-constexpr int kRowTileBytes = kRB * kRowBytes;
+// Workgroup = 4 waves = kKeysPerWG response keys of one KV head (wave w owns
+// keys j0 + 32w .. +31; lane l owns key l % 32 and keeps its K and V rows in
+// registers) x one chunk of kRowChunk packed query rows.  The chunk's 32-row
+// tiles of Q and dO stream into a four-slot LDS ring by direct loads, two
+// tiles ahead, each with the rows' lse * log2(e) and Delta.  Per tile:
+//   S = Q K^T, dP = dO V^T (lane = key, result registers = rows),
+//   P = exp2(S * scale * log2(e) - lse2), dS = P (dP - Delta), zero where the
+//   row does not see the key (causal edge) or lies past the last row,
+//   dv^T += dO^T P, dk^T += Q^T dS (transposed reads of the row tiles).
+// The chunk's partial sums go to the workspace; dkdv_reduce_kernel adds the
+// active chunks in order (deterministic), scales dk and writes or accumulates.
+constexpr int kKeysPerWG = 128;
+constexpr int kRowChunk = kDkdvRowChunk;                   // packed query rows per workgroup
+constexpr int kRStat = 256;                                // per wave: 32 lse2 + 32 Delta floats
+constexpr int kRStage = 2 * kTileBytes + 4 * kRStat;       // Q tile, dO tile, stats
+constexpr int kRAhead = 2;
+constexpr int kRSlots = kRAhead + 2;
 
-__global__ __launch_bounds__(64, 1) void bwd_dkdv_bf16_d256_kernel(BwdArgs a, int64_t key0,
+// First row (a multiple of 32) of `chunk` that can see a key of the block
+// starting at j0 (rows of tokens >= j0 - q_pos0); the chunk is active when it
+// is below the chunk's end.  Shared by the dk/dv and reduce kernels.
+__device__ __forceinline__ int dkdv_row_lo(const BwdArgs& a, int64_t j0, int chunk) {
+  int64_t first_tok = j0 - a.q_pos0;
+  if (first_tok < 0) first_tok = 0;
+  const int64_t rows_total = (int64_t)a.n_q << a.log2_group;
+  const int64_t vis = min(rows_total, first_tok << a.log2_group) & ~int64_t(31);
+  return (int)max((int64_t)chunk * kRowChunk, vis);
+}
+__device__ __forceinline__ int dkdv_row_hi(const BwdArgs& a, int chunk) {
+  return min(a.n_q << a.log2_group, (chunk + 1) * kRowChunk);
+}
+
+// Direct loads of 32 packed query rows (token, head of KV group g) of Q or dO
+// into a row tile (same swizzled layout and lane mapping as the key tiles);
+// rows at or beyond rows_total repeat the last row.
+struct RowFetch {
+  int lane_off[4], lds_row[4], lane_row[4];
+  __device__ __forceinline__ void init(int lane, int w) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      lds_row[i] = 8 * w + 2 * i;
+      lane_row[i] = lds_row[i] + (lane >> 5);
+      lane_off[i] = ((lane & 31) ^ tile_swz(lane_row[i])) * 16;
+    }
+  }
+  // byte offset of instruction i's row for tile row row0 in a [n_q, Hq, 256] bf16 array
+  __device__ __forceinline__ int offset(const BwdArgs& a, int g, int row0, int rows_total,
+                                        int i) const {
+    const int prow = min(row0 + lane_row[i], rows_total - 1);
+    const int head = (g << a.log2_group) + (prow & ((1 << a.log2_group) - 1));
+    return ((prow >> a.log2_group) * a.n_q_heads + head) * kRowBytes + lane_off[i];
+  }
+  __device__ __forceinline__ void issue_one(char* tile, __amdgpu_buffer_rsrc_t r, int off,
+                                            int i) const {
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, LS_LDS(tile + lds_row[i] * kTileRow), 16, off, 0, 0,
+                                             0);
+  }
+};
+
+__global__ __launch_bounds__(256, 1) void bwd_dkdv_bf16_d256_kernel(BwdArgs a, int64_t key0,
                                                                    int64_t key_end) {
-  __shared__ __attribute__((aligned(16))) char smem[2 * kKVBytes + 4 * kRowTileBytes];
-  char* Ks = smem;                              // [32 keys][256] row-major, chunk ^ (key & 7)
-  char* Vs = smem + kKVBytes;
-  char* Qs = smem + 2 * kKVBytes;               // [32 rows][256] row-major, chunk ^ (row & 7)
-  char* Ds = Qs + kRowTileBytes;                // dO, same layout
-  char* Qt = Ds + kRowTileBytes;                // [256 d][32 row slots], chunk ^ ((d >> 1) & 3)
-  char* Dt = Qt + kRowTileBytes;                // dO^T, same layout
+  __shared__ __attribute__((aligned(1024))) char smem[kRSlots * kRStage];
 
-  const int lane = threadIdx.x, l32 = lane & 31, hh = lane >> 5;
-  const int g = blockIdx.y;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int l32 = lane & 31, hh = lane >> 5;
+  const int g = blockIdx.y, chunk = blockIdx.z;
   const int lg = a.log2_group;
   const int rows_total = a.n_q << lg;
-  const int64_t j0 = key0 + (int64_t)blockIdx.x * kKB;
-  const int64_t j_mine = j0 + l32;
-  const u32x4 zero = {0u, 0u, 0u, 0u};
+  const int64_t j0 = key0 + (int64_t)blockIdx.x * kKeysPerWG;
+  const int64_t jw = j0 + 32 * w;          // first key of this wave
+  const int64_t j_mine = jw + l32;
+  const int row_lo = dkdv_row_lo(a, j0, chunk);
+  const int row_hi = dkdv_row_hi(a, chunk);
+  if (row_lo >= row_hi) return;            // no row of the chunk sees a key of the block
+  const int n_tiles = (row_hi - row_lo + 31) / 32;
 
-  // stage the 32 keys' K and V rows (row-major, swizzled)
+  // K and V rows of this lane's key (B operands: lane = key, 8 dims per step)
+  bf16x8 kreg[16], vreg[16];
   {
-    const __bf16* kp = static_cast<const __bf16*>(a.k_pool) + (int64_t)g * kD;
-    const __bf16* vp = static_cast<const __bf16*>(a.v_pool) + (int64_t)g * kD;
-    const int c = lane & 31;
-    for (int key = hh; key < kKB; key += 2) {
-      const int64_t j = j0 + key;
-      u32x4 kv = zero, vv = zero;
-      if (j < key_end) {
-        const int64_t pr = phys_pos(a.page_table, j, a.log2_page);
-        kv = *reinterpret_cast<const u32x4*>(kp + pr * a.k_pos_stride + c * 8);
-        vv = *reinterpret_cast<const u32x4*>(vp + pr * a.v_pos_stride + c * 8);
+    const bool ok = j_mine < key_end;
+    const int64_t pr = ok ? phys_pos(a.page_table, j_mine, a.log2_page) : 0;
+    const __bf16* kr = static_cast<const __bf16*>(a.k_pool) + pr * a.k_pos_stride + g * kD + hh * 8;
+    const __bf16* vr = static_cast<const __bf16*>(a.v_pool) + pr * a.v_pos_stride + g * kD + hh * 8;
+#pragma unroll
+    for (int ks = 0; ks < 16; ++ks) {
+      if (ok) {
+        kreg[ks] = *reinterpret_cast<const bf16x8*>(kr + ks * 16);
+        vreg[ks] = *reinterpret_cast<const bf16x8*>(vr + ks * 16);
+      } else {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) kreg[ks][e] = vreg[ks][e] = (__bf16)0.f;
       }
-      const int off = key * kRowBytes + ((c ^ (key & 7)) << 4);
-      *reinterpret_cast<u32x4*>(Ks + off) = kv;
-      *reinterpret_cast<u32x4*>(Vs + off) = vv;
     }
   }
 
+  const __amdgpu_buffer_rsrc_t rq = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<void*>(a.q), (short)0, 0x7FFFFFFF, 0x00020000);
+  const __amdgpu_buffer_rsrc_t rd = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<void*>(a.d_out), (short)0, 0x7FFFFFFF, 0x00020000);
+  // Delta and lse2 live in one workspace block; lanes 0-31 load lse2 rows, 32-63 Delta rows
+  const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<float*>(a.delta), (short)0, 0x7FFFFFFF, 0x00020000);
+  const int lse2_off = (int)((const char*)a.lse2 - (const char*)a.delta);
+  RowFetch rf;
+  rf.init(lane, w);
+  auto clamp = [&](int t) { return t < n_tiles ? t : n_tiles - 1; };
+  auto stats = [&](char* st, int row0) {
+    const int prow = min(row0 + l32, rows_total - 1);
+    const int head = (g << lg) + (prow & ((1 << lg) - 1));
+    const int off = (hh ? 0 : lse2_off) + (head * a.n_q + (prow >> lg)) * 4;
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, LS_LDS(st + 2 * kTileBytes + kRStat * w), 4, off,
+                                             0, 0, 0);
+  };
+  auto fetch = [&](char* st, int row0, int i) {   // instruction i of a stage's row loads
+    const int off = rf.offset(a, g, row0, rows_total, i & 3);
+    if (i < 4) rf.issue_one(st, rq, off, i);
+    else rf.issue_one(st + kTileBytes, rd, off, i - 4);
+  };
+#pragma unroll
+  for (int i = 0; i < kRAhead; ++i) {
+    char* st = smem + i * kRStage;
+    const int row0 = row_lo + 32 * clamp(i);
+    stats(st, row0);
+#pragma unroll
+    for (int k = 0; k < 8; ++k) fetch(st, row0, k);
+  }
+  const TileOffsets to = tile_offsets(lane);
   f32x16 dk[8], dv[8];
 #pragma unroll
   for (int i = 0; i < 8; ++i) dk[i] = dv[i] = zero16();
+  wait_fetch();
+  tile_barrier();
 
-  // rows (token, head) with token >= j0 - q_pos0 can see some key of the block
-  int64_t first_tok = j0 - a.q_pos0;
-  if (first_tok < 0) first_tok = 0;
-  const int row_begin = (int)((first_tok << lg) / kRB * kRB);
-  const int swz = l32 & 7;
-  const int tswz = (l32 >> 1) & 3;
-
-  for (int rb0 = row_begin; rb0 < rows_total; rb0 += kRB) {
-    __syncthreads();   // previous step's reads of Qs/Ds/Qt/Dt are done
-    // stage Q and dO rows: item (row quad m, chunk c): 8 quads x 32 chunks, 4 per lane
+  for (int t = 0; t < n_tiles; ++t) {
+    char* cur = smem + (t % kRSlots) * kRStage;
+    char* next = smem + ((t + kRAhead) % kRSlots) * kRStage;
+    const int row_next = row_lo + 32 * clamp(t + kRAhead);
+    stats(next, row_next);
+    __builtin_amdgcn_sched_barrier(0);
+    f32x16 s, dp;
+    scores_dp(cur, cur + kTileBytes, kreg, vreg, to, s, dp,
+              [&](int i) { fetch(next, row_next, i); });
+    const float* st = reinterpret_cast<const float*>(cur + 2 * kTileBytes + kRStat * w);
+    const int row0 = row_lo + 32 * t;
+    const bool edge = a.q_pos0 + (row0 >> lg) < jw + 31 || row0 + 32 > rows_total;
 #pragma unroll
-    for (int it = 0; it < 4; ++it) {
-      const int item = lane + 64 * it;
-      const int m = item & 7, c = item >> 3;
-      u32x4 qv[4], dvv[4];
+    for (int m = 0; m < 4; ++m) {
+      const f32x4 l2 = *reinterpret_cast<const f32x4*>(st + 8 * m + 4 * hh);
+      const f32x4 dl = *reinterpret_cast<const f32x4*>(st + 32 + 8 * m + 4 * hh);
 #pragma unroll
-      for (int kk = 0; kk < 4; ++kk) {
-        const int prow = rb0 + 4 * m + kk;
-        if (prow < rows_total) {
-          const int tok = prow >> lg;
-          const int head = (g << lg) + (prow & ((1 << lg) - 1));
-          const int64_t rh = (int64_t)tok * a.n_q_heads + head;
-          qv[kk] = *reinterpret_cast<const u32x4*>(static_cast<const __bf16*>(a.q) + rh * kD + c * 8);
-          dvv[kk] = *reinterpret_cast<const u32x4*>(static_cast<const __bf16*>(a.d_out) + rh * kD + c * 8);
-        } else {
-          qv[kk] = zero;
-          dvv[kk] = zero;
+      for (int e = 0; e < 4; ++e) {
+        const int r = 4 * m + e;
+        float p = __builtin_amdgcn_exp2f(fmaf(s[r], a.scale_log2, -l2[e]));
+        if (edge) {
+          const int row = row0 + acc_key(r, hh);
+          if (row >= rows_total || a.q_pos0 + (row >> lg) < j_mine) p = 0.f;
         }
-        const int row = 4 * m + kk;
-        const int off = row * kRowBytes + ((c ^ (row & 7)) << 4);
-        *reinterpret_cast<u32x4*>(Qs + off) = qv[kk];
-        *reinterpret_cast<u32x4*>(Ds + off) = dvv[kk];
-      }
-      const int slot = swap23(4 * m);
-      const int sc = slot >> 3, sb = (slot & 7) * 2;
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const int d = 8 * c + e;
-        const int dw = e >> 1;
-        const int off = d * (kRB * 2) + ((sc ^ ((d >> 1) & 3)) << 4) + sb;
-        *reinterpret_cast<u32x2*>(Qt + off) = pick4(qv[0][dw], qv[1][dw], qv[2][dw], qv[3][dw], (e & 1) != 0);
-        *reinterpret_cast<u32x2*>(Dt + off) = pick4(dvv[0][dw], dvv[1][dw], dvv[2][dw], dvv[3][dw], (e & 1) != 0);
+        s[r] = p;
+        dp[r] = p * (dp[r] - dl[e]);
       }
     }
-    __syncthreads();
-
-    // S[row][key] = Q K^T and dP[row][key] = dO V^T (lane = key, registers = rows)
-    f32x16 s = zero16(), dp = zero16();
-#pragma unroll
-    for (int ks = 0; ks < 16; ++ks) {
-      const int off = l32 * kRowBytes + (((2 * ks + hh) ^ swz) << 4);
-      const bf16x8 qa = *reinterpret_cast<const bf16x8*>(Qs + off);
-      const bf16x8 da = *reinterpret_cast<const bf16x8*>(Ds + off);
-      const bf16x8 kbv = *reinterpret_cast<const bf16x8*>(Ks + off);
-      const bf16x8 vbv = *reinterpret_cast<const bf16x8*>(Vs + off);
-      s = mfma32(qa, kbv, s);
-      dp = mfma32(da, vbv, dp);
-    }
-#pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int prow = rb0 + acc_key(r, hh);   // register r holds packed row acc_key(r, h)
-      float p = 0.f, dsv = 0.f;
-      if (prow < rows_total) {
-        const int tok = prow >> lg;
-        const int head = (g << lg) + (prow & ((1 << lg) - 1));
-        if (a.q_pos0 + tok >= j_mine) {
-          const int64_t o = (int64_t)head * a.n_q + tok;
-          p = __builtin_amdgcn_exp2f(fmaf(s[r], a.scale_log2, -a.lse2[o]));
-          dsv = p * (dp[r] - a.delta[o]);
-        }
-      }
-      s[r] = p;
-      dp[r] = dsv;
-    }
-    const bf16x8 p0 = pack8(s, 0), p1 = pack8(s, 1);
-    const bf16x8 d0 = pack8(dp, 0), d1 = pack8(dp, 1);
-#pragma unroll
-    for (int db = 0; db < 8; ++db) {
-      const int rowoff = (32 * db + l32) * (kRB * 2);
-      const bf16x8 t0 = *reinterpret_cast<const bf16x8*>(Dt + rowoff + (((0 + hh) ^ tswz) << 4));
-      const bf16x8 t1 = *reinterpret_cast<const bf16x8*>(Dt + rowoff + (((2 + hh) ^ tswz) << 4));
-      dv[db] = mfma32(t0, p0, dv[db]);
-      dv[db] = mfma32(t1, p1, dv[db]);
-      const bf16x8 u0 = *reinterpret_cast<const bf16x8*>(Qt + rowoff + (((0 + hh) ^ tswz) << 4));
-      const bf16x8 u1 = *reinterpret_cast<const bf16x8*>(Qt + rowoff + (((2 + hh) ^ tswz) << 4));
-      dk[db] = mfma32(u0, d0, dk[db]);
-      dk[db] = mfma32(u1, d1, dk[db]);
-    }
+    dq_update(cur + kTileBytes, pack8(s, 0), pack8(s, 1), dv, to);   // dv^T += dO^T P
+    dq_update(cur, pack8(dp, 0), pack8(dp, 1), dk, to);              // dk^T += Q^T dS
+    __builtin_amdgcn_s_waitcnt(0x0F79);   // vmcnt(9): only the newest stage may be in flight
+    tile_barrier();
   }
+  wait_fetch();
 
+  // partial sums of this chunk: part[chunk][0 = dk, 1 = dv][g][key - prefix_len][256]
   if (j_mine < key_end) {
-    const int64_t r = (j_mine - a.prefix_len) * a.n_kv_heads + g;
-    float* dkr = a.dk_resp + r * kD;
-    float* dvr = a.dv_resp + r * kD;
+    const int64_t n_part = a.kv_end - a.prefix_len;
+    const int64_t kidx = j_mine - a.prefix_len;
+    float* pk = a.dkdv_part + (((int64_t)chunk * 2 * a.n_kv_heads + g) * n_part + kidx) * kD;
+    float* pv = pk + (int64_t)a.n_kv_heads * n_part * kD;
 #pragma unroll
     for (int db = 0; db < 8; ++db) {
 #pragma unroll
@@ -401,18 +437,47 @@ __global__ __launch_bounds__(64, 1) void bwd_dkdv_bf16_d256_kernel(BwdArgs a, in
         f32x4 kv, vv;
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          kv[e] = dk[db][4 * q4 + e] * a.scale;
+          kv[e] = dk[db][4 * q4 + e];
           vv[e] = dv[db][4 * q4 + e];
         }
-        if (a.accumulate_dkv) {
-          kv += *reinterpret_cast<const f32x4*>(dkr + d0);
-          vv += *reinterpret_cast<const f32x4*>(dvr + d0);
-        }
-        *reinterpret_cast<f32x4*>(dkr + d0) = kv;
-        *reinterpret_cast<f32x4*>(dvr + d0) = vv;
+        *reinterpret_cast<f32x4*>(pk + d0) = kv;
+        *reinterpret_cast<f32x4*>(pv + d0) = vv;
       }
     }
   }
+}
+
+// dk_resp / dv_resp for keys [key0, key_end): the sum over the active row
+// chunks, in chunk order; dk is scaled by softmax_scale.  Thread = 4 dims of
+// one key of one KV head.
+__global__ __launch_bounds__(256) void dkdv_reduce_kernel(BwdArgs a, int64_t key0, int64_t key_end,
+                                                          int n_chunks) {
+  const int64_t n_keys = key_end - key0;
+  const int64_t item = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;   // (key, g, d4)
+  if (item >= n_keys * a.n_kv_heads * (kD / 4)) return;
+  const int d0 = (int)(item % (kD / 4)) * 4;
+  const int g = (int)((item / (kD / 4)) % a.n_kv_heads);
+  const int64_t j = key0 + item / ((kD / 4) * a.n_kv_heads);
+  const int64_t j0 = key0 + (j - key0) / kKeysPerWG * kKeysPerWG;
+  const int64_t n_part = a.kv_end - a.prefix_len;
+  const int64_t kidx = j - a.prefix_len;
+  f32x4 sk = {0.f, 0.f, 0.f, 0.f}, sv = sk;
+  for (int c = 0; c < n_chunks; ++c) {
+    if (dkdv_row_lo(a, j0, c) >= dkdv_row_hi(a, c)) continue;
+    const float* pk = a.dkdv_part + (((int64_t)c * 2 * a.n_kv_heads + g) * n_part + kidx) * kD + d0;
+    sk += *reinterpret_cast<const f32x4*>(pk);
+    sv += *reinterpret_cast<const f32x4*>(pk + (int64_t)a.n_kv_heads * n_part * kD);
+  }
+  sk *= a.scale;
+  const int64_t r = (kidx * a.n_kv_heads + g) * kD + d0;
+  f32x4* dkr = reinterpret_cast<f32x4*>(a.dk_resp + r);
+  f32x4* dvr = reinterpret_cast<f32x4*>(a.dv_resp + r);
+  if (a.accumulate_dkv) {
+    sk += *dkr;
+    sv += *dvr;
+  }
+  *dkr = sk;
+  *dvr = sv;
 }
 
 }  // namespace
@@ -434,9 +499,15 @@ hipError_t launch_bwd_bf16_d256(const BwdArgs& a, bool need_dq, bool need_dkv,
     const int64_t key0 = a.kv_begin > a.prefix_len ? a.kv_begin : a.prefix_len;
     const int64_t n_keys = a.kv_end - key0;
     if (n_keys > 0) {
-      const unsigned blocks = (unsigned)((n_keys + kKB - 1) / kKB);
-      hipLaunchKernelGGL(bwd_dkdv_bf16_d256_kernel, dim3(blocks, a.n_kv_heads), dim3(64), 0,
-                         stream, a, key0, a.kv_end);
+      const unsigned blocks = (unsigned)((n_keys + kKeysPerWG - 1) / kKeysPerWG);
+      const int n_chunks = dkdv_row_chunks(a.n_q, a.group);
+      hipLaunchKernelGGL(bwd_dkdv_bf16_d256_kernel, dim3(blocks, a.n_kv_heads, n_chunks),
+                         dim3(256), 0, stream, a, key0, a.kv_end);
+      hipError_t e = hipGetLastError();
+      if (e != hipSuccess) return e;
+      const int64_t items = n_keys * a.n_kv_heads * (kD / 4);
+      hipLaunchKernelGGL(dkdv_reduce_kernel, dim3((unsigned)((items + 255) / 256)), dim3(256), 0,
+                         stream, a, key0, a.kv_end, n_chunks);
       return hipGetLastError();
     }
   }

@@ -10,6 +10,13 @@ namespace ls {
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 constexpr int kMaxSplitsPerLaunch = 64;
+constexpr int kDkdvRowChunk = 2048;   // packed query rows per dk/dv workgroup (bf16 path)
+
+// Row chunks of the bf16 dk/dv kernel (partials in the backward workspace).
+inline int dkdv_row_chunks(int n_q, int group) {
+  const int64_t rows = (int64_t)n_q * group;
+  return (int)((rows + kDkdvRowChunk - 1) / kDkdvRowChunk);
+}
 
 // Everything a forward-split kernel needs; passed by value as a kernel argument.
 struct FwdArgs {
@@ -43,6 +50,7 @@ struct BwdArgs {
   float* dq;                // [n_q, Hq, D]
   float* dk_resp;           // [kv_len - prefix_len, Hkv, D]
   float* dv_resp;           // [kv_len - prefix_len, Hkv, Dv]
+  float* dkdv_part;         // bf16 path: [row chunks, 2, Hkv, kv_end - prefix_len, D] partials
   int64_t q_pos0;
   int64_t prefix_len;
   int64_t kv_begin, kv_end;

@@ -67,7 +67,7 @@ class ReplayStep:
             self.dq = torch.empty((R, Hq, D), **kw)
             self.dk = torch.zeros((cfg.kv_len - cfg.prefix_len, cfg.n_kv_heads, D), **kw)
             self.dv = torch.zeros((cfg.kv_len - cfg.prefix_len, cfg.n_kv_heads, Dv), **kw)
-            self.ws = B.bwd_workspace(q, self.kv)
+            self.ws = B.bwd_workspace(q, self.kv, prefix_len=cfg.prefix_len, q_pos0=cfg.q_pos0)
 
     def forward_splits(self):
         """Local (o_r, l_r) of every split in one launch."""

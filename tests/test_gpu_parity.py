@@ -119,6 +119,17 @@ def test_bf16_small_planted():
     full_case(BF16_SMALL)
 
 
+def test_bf16_dkdv_row_chunks_and_key_blocks():
+    """Response gradients summed over several row chunks of the dk/dv kernel
+    and several key blocks, every key and row compared.  640 tokens x G = 8 =
+    5,120 packed rows (chunks of 2,048: two full, one partial) against 640
+    response keys (five full blocks of 128); 650 tokens = 5,200 rows (a
+    partial last 32-row tile) and a sixth block of 10 keys."""
+    for r in (640, 650):
+        full_case(configs.C3.scaled(name=f"bf16_dkdv_{r}", prefix_len=1024, resp_len=r, n_shards=1,
+                                    splits_per_shard=2))
+
+
 def test_bf16_page16_unaligned_splits():
     cfg = BF16_SMALL.scaled(name="bf16_p16", page_size=16, prefix_len=3000, resp_len=77,
                             plant_frac=0.0)
