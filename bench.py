@@ -8,7 +8,11 @@ the backward (dq accumulated over the shards, response dK/dV).  Inputs are
 resident in HBM before the timed region.  Prints one JSON line.
 
 FLOP convention: fwd = 4*Hq*D*sum_i |V_i|; bwd = Hq*D*(6*sum_i |V_i & prefix| +
-10*sum_i |V_i & response|) (recompute counted, prefix dK/dV not counted).
+10*sum_i |V_i & response|) (recompute counted, prefix dK/dV not counted); the
+"useful" rate drops the backward's Q K^T recompute (4 and 8 instead of 6 and 10).
+Besides the step it reports HBM-bound page streaming (the split forward over
+the whole prefix with 16 query rows), ceilings measured on the same GPU (bf16
+GEMM, 4 GiB copy) and the clocks.
 """
 from __future__ import annotations
 
@@ -43,6 +47,83 @@ def flops(cfg):
 
 def log(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def useful_flops(cfg):
+    """The FLOP convention without the backward's recompute of Q K^T."""
+    pre, resp = visible_counts(cfg)
+    Hq, D = cfg.n_q_heads, cfg.head_dim
+    return 4 * Hq * D * (pre + resp) + Hq * D * (4 * pre + 8 * resp)
+
+
+def time_ms(fn, reps, stream=None):
+    """Median of per-rep HIP-event times (ms) after one untimed call."""
+    import torch
+    fn()
+    torch.cuda.synchronize()
+    ts = []
+    for _ in range(reps):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        fn()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        ts.append(e0.elapsed_time(e1))
+    ts.sort()
+    return ts[len(ts) // 2]
+
+
+def measured_ceilings():
+    """Ceilings measured on this GPU: a large bf16 GEMM through torch (hipBLASLt)
+    and a 4 GiB device-to-device copy (read + write bytes per second)."""
+    import torch
+    n = 8192
+    a = torch.randn((n, n), dtype=torch.bfloat16, device="cuda")
+    b = torch.randn((n, n), dtype=torch.bfloat16, device="cuda")
+    c = torch.empty((n, n), dtype=torch.bfloat16, device="cuda")
+    ms = time_ms(lambda: torch.matmul(a, b, out=c), 10)
+    gemm = 2 * n ** 3 / (ms * 1e-3) / 1e12
+    del a, b, c
+    src = torch.empty(1 << 30, dtype=torch.float32, device="cuda")
+    src.fill_(1.0)
+    dst = torch.empty_like(src)
+    ms = time_ms(lambda: dst.copy_(src), 5)
+    copy = 2 * src.numel() * 4 / (ms * 1e-3) / 1e9
+    del src, dst
+    torch.cuda.empty_cache()
+    return {"bf16_gemm_tflops": round(gemm, 1), "gemm_shape": [n, n, n],
+            "d2d_copy_gbs": round(copy, 1), "copy_bytes": 1 << 32}
+
+
+def gpu_clocks():
+    """Current shader / memory clocks as rocm-smi reports them (None when unavailable)."""
+    import subprocess
+    try:
+        r = subprocess.run(["rocm-smi", "--showclocks", "--json"], stdout=subprocess.PIPE,
+                           stderr=subprocess.DEVNULL, text=True, timeout=20)
+        d = json.loads(r.stdout)
+        card = next(iter(d.values()))
+        return {k: v for k, v in card.items() if "sclk" in k.lower() or "mclk" in k.lower()}
+    except Exception:  # pragma: no cover - tool missing or output changed
+        return None
+
+
+def page_streaming(cfg, dev, rows=16, n_splits=128):
+    """The split forward over the whole prefix with only `rows` query rows: an
+    HBM-bound pass that reads every K and V row of the prefix once."""
+    from paper_2607_14952_amd import binding as B
+    q = dev["q"][:rows].contiguous()
+    kv = B.PagedKV(dev["k_pool"], dev["v_pool"], dev["page_table"])
+    P = cfg.prefix_len
+    bounds = [P * i // n_splits for i in range(n_splits + 1)]
+    splits = list(zip(bounds[:-1], bounds[1:]))
+    op, lp = B.prefix_attn_fwd(q, kv, splits, prefix_len=P, q_pos0=P, scale=cfg.scale)
+    ms = time_ms(lambda: B.prefix_attn_fwd(q, kv, splits, prefix_len=P, q_pos0=P,
+                                           scale=cfg.scale, out_part=op, lse_part=lp), 5)
+    nbytes = 2 * P * cfg.n_kv_heads * cfg.head_dim * 2
+    gbs = nbytes / (ms * 1e-3) / 1e9
+    return {"rows": rows, "splits": n_splits, "bytes": nbytes, "ms": round(ms, 3),
+            "gbs": round(gbs, 1), "frac_of_hbm_peak": round(gbs / PEAK_HBM_GBS, 4)}
 
 
 def cpu_baseline(cfg, host, n_rows=16, n_shards=2):
@@ -195,9 +276,12 @@ def main():
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--config", default="c3")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-rows", type=int, default=16)
+    ap.add_argument("--cpu-rows", type=int, default=96)
     ap.add_argument("--calib-copy", action="store_true",
                     help="run a 1 GiB device copy first (reference for rocprofv3 byte counters)")
+    ap.add_argument("--skip-extras", action="store_true",
+                    help="skip page streaming, measured ceilings and clocks (profiling runs: the "
+                         "streaming pass reuses the forward kernel)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU: this build has no multi-GPU path "
@@ -327,6 +411,11 @@ def main():
         "flop_per_step": {"fwd": fwd_fl, "bwd": bwd_fl},
         "gpu": torch.cuda.get_device_name(0),
     }
+    result["useful_tflops"] = round(useful_flops(cfg) / (ms_per_step * 1e-3) / 1e12, 2)
+    if not args.skip_extras:
+        log("page streaming, clocks")
+        result["page_streaming"] = page_streaming(cfg, dev)
+        result["gpu_clocks"] = gpu_clocks()
     if not args.no_cpu_baseline:
         del dev, step
         torch.cuda.empty_cache()
@@ -335,6 +424,15 @@ def main():
         cb["cpu"] = platform.processor() or platform.machine()
         result["cpu_baseline"] = {k: (round(v, 6) if isinstance(v, float) else v)
                                   for k, v in cb.items()}
+    else:
+        del dev, step
+        torch.cuda.empty_cache()
+    if not args.skip_extras:
+        log("measured ceilings")
+        ceil = measured_ceilings()
+        ceil["frac_of_gemm"] = round(value / ceil["bf16_gemm_tflops"], 4)
+        ceil["roofline_frac_of_gemm"] = round(roofline["achieved"] / ceil["bf16_gemm_tflops"], 4)
+        result["measured_ceilings"] = ceil
     print(json.dumps(result), flush=True)
 
 

@@ -9,7 +9,7 @@ namespace ls {
 
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
-constexpr int kMaxSplitsPerLaunch = 64;
+constexpr int kMaxSplitsPerLaunch = 128;   // split bounds travel in the kernel arguments (< 4 KiB)
 constexpr int kDkdvRowChunk = 2048;   // packed query rows per dk/dv workgroup (bf16 path)
 
 // Row chunks of the bf16 dk/dv kernel (partials in the backward workspace).
