@@ -23,7 +23,8 @@ EXTRA = {"fwd_bf16.hip": ["-mllvm", "--amdgpu-mfma-vgpr-form=1"],
          "bwd_bf16.hip": ["-mllvm", "--amdgpu-mfma-vgpr-form=1"],
          "sparse_fwd.hip": ["-mllvm", "--amdgpu-mfma-vgpr-form=1",
                             "-mllvm", "-disable-promote-alloca-to-lds"],
-         "sparse_bwd.hip": ["-mllvm", "-disable-promote-alloca-to-lds"]}
+         "sparse_bwd.hip": ["-mllvm", "--amdgpu-mfma-vgpr-form=1",
+                            "-mllvm", "-disable-promote-alloca-to-lds"]}
 ARCH = os.environ.get("LS_OFFLOAD_ARCH", "gfx950")
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")

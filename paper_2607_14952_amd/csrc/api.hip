@@ -486,6 +486,9 @@ ls_status check_sparse(const ls_attn_params* p, const int32_t* idx, int32_t topk
     return fail(LS_ERR_INVALID_ARG, "idx must be non-NULL and 16-byte aligned");
   if (sparse_layout(p, topk).n_max > (int64_t)1 << 30)
     return fail(LS_ERR_UNSUPPORTED, "key list too long");
+  // rows are gathered with 32-bit offsets from the pool base
+  if (p->n_phys_pages * p->page_size * (int64_t)p->head_dim * 2 > (int64_t)0xFFFFFFFF)
+    return fail(LS_ERR_UNSUPPORTED, "sparse replay: the latent pool must be smaller than 4 GiB");
   return LS_OK;
 }
 

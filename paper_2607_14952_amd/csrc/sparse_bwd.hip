@@ -24,26 +24,100 @@ __global__ __launch_bounds__(256) void sparse_phys_kernel(SparseArgs a) {
   a.phys[i] = (int32_t)phys_pos(a.page_table, pos, a.log2_page);
 }
 
+constexpr int kBSlots = 3;   // ring slots: tile t is consumed in iteration t, two tiles in flight
+
+// One dS tile: S^T = C Q^T (36 steps) and dP^T = V dO^T (the first 32), dS
+// stored as bf16, then the next stage's direct loads.  `next` and `tile` are
+// distinct ring slots (restrict: no wait for the loads before reading `tile`).
+__device__ __forceinline__ void ds_tile(const SparseArgs& a, char* __restrict__ next,
+                                        const char* __restrict__ tile, const SFetch& f,
+                                        __amdgpu_buffer_rsrc_t pool, const int32_t* pr, int w,
+                                        const bf16x8* qreg, const bf16x8* dreg, const SOffsets& so,
+                                        int T, int n_t, int hh, float lse2, float delta,
+                                        __bf16* ds_row) {
+  bf16x8 kr[36];
+#pragma unroll
+  for (int i = 0; i < kSKAhead; ++i) kr[i] = s_row16(tile, so, i);
+  mfma_fence();
+  f32x16 s = zero16(), dp = zero16();
+#pragma unroll
+  for (int ks = 0; ks < 36; ++ks) {
+    if (ks + kSKAhead < 36) kr[ks + kSKAhead] = s_row16(tile, so, ks + kSKAhead);
+    s = mfma32(kr[ks], qreg[ks], s);
+    if (ks < 32) dp = mfma32(kr[ks], dreg[ks], dp);
+    mfma_fence();
+  }
+#pragma unroll
+  for (int q4 = 0; q4 < 4; ++q4) {
+    __bf16 v[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int r = 4 * q4 + e;
+      float p = __builtin_amdgcn_exp2f(fmaf(s[r], a.scale_log2, -lse2));
+      if (T * kKeys + acc_key(r, hh) >= n_t) p = 0.f;
+      v[e] = (__bf16)(p * (dp[r] - delta));
+    }
+    // keys 8*q4 + 4h + {0..3} of this tile: four consecutive bf16
+    u32x2 packed;
+    packed[0] = __builtin_bit_cast(uint16_t, v[0]) | ((uint32_t)__builtin_bit_cast(uint16_t, v[1]) << 16);
+    packed[1] = __builtin_bit_cast(uint16_t, v[2]) | ((uint32_t)__builtin_bit_cast(uint16_t, v[3]) << 16);
+    *reinterpret_cast<u32x2*>(ds_row + T * kKeys + 8 * q4 + 4 * hh) = packed;
+  }
+  // the stage's direct loads go after the dS stores, so they are the newest
+  // vector-memory operations at the end-of-iteration wait
+  __builtin_amdgcn_sched_barrier(0);
+  f.issue(next, pool, pr, w);
+}
+
+// One dq tile: dq^T += C^T dS^T over the 9 column blocks of this wave's half,
+// the next stage's direct loads spread over the first nine MFMAs (restrict:
+// see ds_tile).
+__device__ __forceinline__ void dq_tile(char* __restrict__ next, const char* __restrict__ tile,
+                                        const SFetch& f, __amdgpu_buffer_rsrc_t pool,
+                                        const int32_t* pr, int w, int half, const bf16x8* d,
+                                        const SOffsets& so, f32x16* acc) {
+  bf16x8 kt[18];
+  auto read = [&](int i) {
+    const int db = 9 * half + (i >> 1);
+    return (i & 1) ? s_col8(tile, so, db, 16, 24) : s_col8(tile, so, db, 0, 8);
+  };
+#pragma unroll
+  for (int i = 0; i < kSVAhead; ++i) kt[i] = read(i);
+  mfma_fence();
+#pragma unroll
+  for (int i = 0; i < 18; ++i) {
+    if (i + kSVAhead < 18) kt[i + kSVAhead] = read(i + kSVAhead);
+    acc[i >> 1] = mfma32(kt[i], d[i & 1], acc[i >> 1]);
+    if (i < 9) f.issue_one(next, pool, pr, w, i);
+    mfma_fence();
+  }
+}
+
 // ---------------------------------------------------------------- backward, phase 1
 // dS[t][head][k] = P (dP - Delta) in bf16, P = exp2(s*c - lse2), dP = dO . v_k.
+// Workgroup = 4 waves = one token x 128 heads (wave w: heads 32w .. +31).
 __global__ __launch_bounds__(256, 1) void sparse_ds_kernel(SparseArgs a) {
-  __shared__ __attribute__((aligned(1024))) char smem[kSlots * kTile];
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  __shared__ __attribute__((aligned(1024))) char smem[kBSlots * kTile];
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int l32 = lane & 31, hh = lane >> 5;
   const int t = blockIdx.x;
   const int head = blockIdx.y * 128 + w * 32 + l32;
   const int n_t = a.topk + (int)a.window0 + t + 1;
   const int n_tiles = (n_t + kKeys - 1) / kKeys;
-  const int32_t* phys_t = a.phys + (int64_t)t * a.n_max;
-  const char* pool = static_cast<const char*>(a.latent);
+  const __amdgpu_buffer_rsrc_t phys_t = phys_rsrc(a, t);
+  const __amdgpu_buffer_rsrc_t pool = pool_rsrc(a.latent);
+  auto clamp = [&](int T) { return T < n_tiles ? T : n_tiles - 1; };
 
   SFetch f;
   f.init(lane, w);
   const SOffsets so = s_offsets(lane);
-  int32_t pr[9];
+  int32_t pr[9], pn[9];
   f.rows_of(phys_t, 0, pr);
   f.issue(smem, pool, pr, w);
-  f.rows_of(phys_t, n_tiles > 1 ? 1 : 0, pr);
+  f.rows_of(phys_t, clamp(1), pr);
+  f.issue(smem + kTile, pool, pr, w);
+  f.rows_of(phys_t, clamp(2), pr);
 
   bf16x8 qreg[36], dreg[32];
   {
@@ -59,83 +133,44 @@ __global__ __launch_bounds__(256, 1) void sparse_ds_kernel(SparseArgs a) {
   const float lse2 = a.lse2[stat], delta = a.delta[stat];
   __bf16* ds_row = a.ds + ((int64_t)t * a.n_heads + head) * a.n_max;
   wait_fetch();
-  __syncthreads();
+  tile_barrier();
 
   for (int T = 0; T < n_tiles; ++T) {
-    const int tn = T + 1 < n_tiles ? T + 1 : T;
-    f.issue(smem + ((T + 1) % kSlots) * kTile, pool, pr, w);
-    f.rows_of(phys_t, tn + 1 < n_tiles ? tn + 1 : tn, pr);
-    const char* tile = smem + (T % kSlots) * kTile;
-    f32x16 s = zero16(), dp = zero16();
+    f.rows_of(phys_t, clamp(T + 3), pn);
+    __builtin_amdgcn_sched_barrier(0);   // row indices load ahead of this stage's direct loads
+    ds_tile(a, smem + ((T + 2) % kBSlots) * kTile, smem + (T % kBSlots) * kTile, f, pool, pr, w,
+            qreg, dreg, so, T, n_t, hh, lse2, delta, ds_row);
 #pragma unroll
-    for (int ks = 0; ks < 36; ++ks) {
-      const bf16x8 kv = s_row16(tile, so, ks);
-      s = mfma32(kv, qreg[ks], s);
-      if (ks < 32) dp = mfma32(kv, dreg[ks], dp);
-      if (ks % 6 == 5) __builtin_amdgcn_sched_barrier(0);
-    }
-#pragma unroll
-    for (int q4 = 0; q4 < 4; ++q4) {
-      __bf16 v[4];
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const int r = 4 * q4 + e;
-        float p = __builtin_amdgcn_exp2f(fmaf(s[r], a.scale_log2, -lse2));
-        if (T * kKeys + acc_key(r, hh) >= n_t) p = 0.f;
-        v[e] = (__bf16)(p * (dp[r] - delta));
-      }
-      // keys 8*q4 + 4h + {0..3} of this tile: four consecutive bf16
-      u32x2 packed;
-      packed[0] = __builtin_bit_cast(uint16_t, v[0]) | ((uint32_t)__builtin_bit_cast(uint16_t, v[1]) << 16);
-      packed[1] = __builtin_bit_cast(uint16_t, v[2]) | ((uint32_t)__builtin_bit_cast(uint16_t, v[3]) << 16);
-      *reinterpret_cast<u32x2*>(ds_row + T * kKeys + 8 * q4 + 4 * hh) = packed;
-    }
-    wait_fetch();
-    __syncthreads();
+    for (int i = 0; i < 9; ++i) pr[i] = pn[i];
+    __builtin_amdgcn_s_waitcnt(0x0F79);   // vmcnt(9): only this iteration's stage may be in flight
+    tile_barrier();
   }
+  wait_fetch();
 }
 
 // ---------------------------------------------------------------- backward, phase 2
-// dq[t][head][d] (+)= scale * sum_k dS[t][head][k] c_k[d]; wave w owns heads
-// 32*(w & 3) .. +31 and columns 288*(w >> 2) .. +287.
-__global__ __launch_bounds__(512, 1) void sparse_dq_kernel(SparseArgs a) {
-  __shared__ __attribute__((aligned(1024))) char smem[kSlots * kTile];
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+// dq[t][head][d] (+)= scale * sum_k dS[t][head][k] c_k[d].  Workgroup = 4 waves
+// = 64 heads of one token (token_and_half); wave w = 2 * half + g owns heads
+// 32g .. 32g+31 of the workgroup and columns 288 * half .. +287.
+__global__ __launch_bounds__(256, 1) void sparse_dq_kernel(SparseArgs a) {
+  __shared__ __attribute__((aligned(1024))) char smem[kBSlots * kTile];
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int l32 = lane & 31, hh = lane >> 5;
-  const int t = blockIdx.x;
-  const int head = blockIdx.y * 128 + (w & 3) * 32 + l32;
-  const int half = w >> 2;
-  const bool fetcher = w < 4;
+  const int g = w & 1, half = w >> 1;
+  int t, hs;
+  token_and_half(blockIdx.x, t, hs);
+  if (t >= a.n_q) return;
+  const int head = blockIdx.y * 128 + hs * 64 + g * 32 + l32;
   const int n_t = a.topk + (int)a.window0 + t + 1;
   const int n_tiles = (n_t + kKeys - 1) / kKeys;
-  const int32_t* phys_t = a.phys + (int64_t)t * a.n_max;
-  const char* pool = static_cast<const char*>(a.latent);
+  const __amdgpu_buffer_rsrc_t phys_t = phys_rsrc(a, t);
+  const __amdgpu_buffer_rsrc_t pool = pool_rsrc(a.latent);
   const __bf16* ds_row = a.ds + ((int64_t)t * a.n_heads + head) * a.n_max;
+  auto clamp = [&](int T) { return T < n_tiles ? T : n_tiles - 1; };
 
-  SFetch f;
-  f.init(lane, w & 3);
-  const SOffsets so = s_offsets(lane);
-  int32_t pr[9];
-  if (fetcher) {
-    f.rows_of(phys_t, 0, pr);
-    f.issue(smem, pool, pr, w);
-    f.rows_of(phys_t, n_tiles > 1 ? 1 : 0, pr);
-  }
-  f32x16 acc[9];
-#pragma unroll
-  for (int i = 0; i < 9; ++i) acc[i] = zero16();
-  wait_fetch();
-  __syncthreads();
-
-  for (int T = 0; T < n_tiles; ++T) {
-    const int tn = T + 1 < n_tiles ? T + 1 : T;
-    if (fetcher) {
-      f.issue(smem + ((T + 1) % kSlots) * kTile, pool, pr, w);
-      f.rows_of(phys_t, tn + 1 < n_tiles ? tn + 1 : tn, pr);
-    }
-    const char* tile = smem + (T % kSlots) * kTile;
-    // dS operand: keys 16kk + {4h..4h+3, 8+4h..8+4h+3}
-    bf16x8 d[2];
+  // dS operand of tile T: keys 16kk + {4h..4h+3, 8+4h..8+4h+3}
+  auto load_ds = [&](int T, bf16x8* d) {
 #pragma unroll
     for (int kk = 0; kk < 2; ++kk) {
       const u32x2 lo = *reinterpret_cast<const u32x2*>(ds_row + T * kKeys + 16 * kk + 4 * hh);
@@ -144,14 +179,39 @@ __global__ __launch_bounds__(512, 1) void sparse_dq_kernel(SparseArgs a) {
       both[0] = lo[0]; both[1] = lo[1]; both[2] = hi[0]; both[3] = hi[1];
       d[kk] = __builtin_bit_cast(bf16x8, both);
     }
+  };
+
+  SFetch f;
+  f.init(lane, w);
+  const SOffsets so = s_offsets(lane);
+  int32_t pr[9], pn[9];
+  f.rows_of(phys_t, 0, pr);
+  f.issue(smem, pool, pr, w);
+  f.rows_of(phys_t, clamp(1), pr);
+  f.issue(smem + kTile, pool, pr, w);
+  f.rows_of(phys_t, clamp(2), pr);
+  bf16x8 d[2], dn[2];
+  load_ds(0, d);
+  f32x16 acc[9];
 #pragma unroll
-    for (int db = 0; db < 9; ++db) {
-      acc[db] = mfma32(s_col8(tile, so, 9 * half + db, 0, 8), d[0], acc[db]);
-      acc[db] = mfma32(s_col8(tile, so, 9 * half + db, 16, 24), d[1], acc[db]);
-    }
-    wait_fetch();
-    __syncthreads();
+  for (int i = 0; i < 9; ++i) acc[i] = zero16();
+  wait_fetch();
+  tile_barrier();
+
+  for (int T = 0; T < n_tiles; ++T) {
+    load_ds(clamp(T + 1), dn);
+    f.rows_of(phys_t, clamp(T + 3), pn);
+    __builtin_amdgcn_sched_barrier(0);   // both load ahead of this stage's direct loads
+    dq_tile(smem + ((T + 2) % kBSlots) * kTile, smem + (T % kBSlots) * kTile, f, pool, pr, w, half,
+            d, so, acc);
+#pragma unroll
+    for (int i = 0; i < 9; ++i) pr[i] = pn[i];
+    d[0] = dn[0];
+    d[1] = dn[1];
+    __builtin_amdgcn_s_waitcnt(0x0F79);   // vmcnt(9): only this iteration's stage may be in flight
+    tile_barrier();
   }
+  wait_fetch();
 
   float* dq = a.dq + ((int64_t)t * a.n_heads + head) * kDk + 288 * half;
 #pragma unroll
@@ -182,7 +242,8 @@ hipError_t launch_sparse_bwd(const SparseArgs& a, hipStream_t stream) {
   hipLaunchKernelGGL(sparse_ds_kernel, dim3(a.n_q, a.n_heads / 128), dim3(256), 0, stream, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(sparse_dq_kernel, dim3(a.n_q, a.n_heads / 128), dim3(512), 0, stream, a);
+  hipLaunchKernelGGL(sparse_dq_kernel, dim3(token_half_blocks(a.n_q), a.n_heads / 128), dim3(256),
+                     0, stream, a);
   return hipGetLastError();
 }
 

@@ -83,11 +83,24 @@ __device__ __forceinline__ bf16x8 s_col8(const char* tile, const SOffsets& o, in
   return __builtin_bit_cast(bf16x8, __builtin_shufflevector(a, b, 0, 1, 2, 3, 4, 5, 6, 7));
 }
 
-// Direct loads of one 36 KiB tile by `nwaves_fetch` = 4 waves (9 x 1 KiB each):
-// lane l of instruction i of wave w carries LDS chunk q = (9w + i) * 64 + l,
-// i.e. row q / 72 and physical chunk q % 72 (logical chunk q % 72 ^ swizzle).
-// Row and chunk offsets are recomputed per instruction (a few integer ops)
-// rather than kept in registers.
+// Buffer resource over the whole latent pool (rows are addressed by 32-bit
+// byte offsets; the host limits the pool to 4 GiB).  Buffer loads (MUBUF)
+// rather than FLAT global_load_lds keep the compiler's LDS waits partial.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t pool_rsrc(const void* pool) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(pool), (short)0, -1, 0x00020000);
+}
+
+// Buffer resource over the resolved key list of token t (n_max entries).
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t phys_rsrc(const SparseArgs& a, int t) {
+  return __builtin_amdgcn_make_buffer_rsrc(a.phys + (int64_t)t * a.n_max, (short)0, a.n_max * 4,
+                                           0x00020000);
+}
+
+// Direct loads of one 36 KiB tile by 4 waves (9 x 1 KiB each): lane l of
+// instruction i of wave w carries LDS chunk q = (9w + i) * 64 + l, i.e. row
+// q / 72 and physical chunk q % 72 (logical chunk permuted by s_swz).  Row and
+// chunk offsets are recomputed per instruction (a few integer ops) rather than
+// kept in registers.
 struct SFetch {
   int q0;   // (9w) * 64 + lane
   __host__ __device__ inline void init(int lane, int w) { q0 = 9 * w * 64 + lane; }
@@ -97,18 +110,24 @@ struct SFetch {
     const int c = q - r * kChunks;
     return ((c & ~7) | ((c & 7) ^ s_swz(r))) * 16;
   }
-  // phys rows of this lane's 9 chunks for tile T (from the resolved key list)
-  __device__ __forceinline__ void rows_of(const int32_t* __restrict__ phys_t, int T,
-                                          int32_t* pr) const {
-#pragma unroll
-    for (int i = 0; i < 9; ++i) pr[i] = phys_t[T * kKeys + row(i)];
-  }
-  __device__ __forceinline__ void issue(char* tile, const char* pool, const int32_t* pr,
-                                        int w) const {
+  // phys rows of this lane's 9 chunks for tile T, read through a buffer
+  // resource over the token's resolved key list (32-bit offsets recomputed per
+  // call instead of nine 64-bit addresses held across the loop)
+  __device__ __forceinline__ void rows_of(__amdgpu_buffer_rsrc_t phys_t, int T, int32_t* pr) const {
 #pragma unroll
     for (int i = 0; i < 9; ++i)
-      __builtin_amdgcn_global_load_lds(pool + (int64_t)pr[i] * kRow + coff(i),
-                                       LS_LDS(tile + (9 * w + i) * 1024), 16, 0, 0);
+      pr[i] = __builtin_amdgcn_raw_buffer_load_b32(phys_t, (T * kKeys + row(i)) * 4, 0, 0);
+  }
+  __device__ __forceinline__ void issue_one(char* tile, __amdgpu_buffer_rsrc_t r, const int32_t* pr,
+                                            int w, int i) const {
+    const uint32_t off = (uint32_t)pr[i] * (uint32_t)kRow + (uint32_t)coff(i);
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, LS_LDS(tile + (9 * w + i) * 1024), 16, (int)off, 0,
+                                             0, 0);
+  }
+  __device__ __forceinline__ void issue(char* tile, __amdgpu_buffer_rsrc_t r, const int32_t* pr,
+                                        int w) const {
+#pragma unroll
+    for (int i = 0; i < 9; ++i) issue_one(tile, r, pr, w, i);
   }
 };
 
@@ -131,24 +150,58 @@ __device__ __forceinline__ float softmax_step(f32x16& s, float c, float& m_run, 
   return alpha;
 }
 
-// Scores over the 576-wide row; the scheduler is fenced every 6 steps so that
-// only a few operand reads are in flight (the Q operand already fills 144 VGPRs).
-__device__ __forceinline__ f32x16 s_scores(const char* tile, const bf16x8* qreg, const SOffsets& o) {
+// Workgroups own 64 heads of one token, so two workgroups share every token's
+// gathered rows.  Block b serves token (b / 16) * 8 + b % 8, head half
+// (b / 8) % 2: blocks b and b + 8 hold the two halves of one token, run on the
+// same XCD (blocks are dealt to the 8 XCDs round-robin) and are dispatched
+// back to back, so the second finds the rows in that XCD's L2.  The grid has
+// 16 * ceil(n_q / 8) blocks per 128 heads; blocks past n_q exit.
+__device__ __forceinline__ void token_and_half(int b, int& t, int& hs) {
+  t = (b >> 4) * 8 + (b & 7);
+  hs = (b >> 3) & 1;
+}
+inline unsigned token_half_blocks(int n_q) { return 16u * (unsigned)((n_q + 7) / 8); }
+
+// Operand reads run a fixed number of MFMAs ahead of their use (mfma_fence).
+constexpr int kSKAhead = 4;   // K row reads in flight
+constexpr int kSVAhead = 3;   // V operands in flight (two transposing reads each)
+
+// S^T over the 576-wide row (36 steps); load(ks) runs after MFMA ks < 9 (one
+// direct load of the next stage each).
+template <typename Load>
+__device__ __forceinline__ f32x16 s_scores(const char* tile, const bf16x8* qreg, const SOffsets& o,
+                                           Load&& load) {
+  bf16x8 kr[36];
+#pragma unroll
+  for (int i = 0; i < kSKAhead; ++i) kr[i] = s_row16(tile, o, i);
+  mfma_fence();
   f32x16 s = zero16();
 #pragma unroll
   for (int ks = 0; ks < 36; ++ks) {
-    s = mfma32(s_row16(tile, o, ks), qreg[ks], s);
-    if (ks % 6 == 5) __builtin_amdgcn_sched_barrier(0);
+    if (ks + kSKAhead < 36) kr[ks + kSKAhead] = s_row16(tile, o, ks + kSKAhead);
+    s = mfma32(kr[ks], qreg[ks], s);
+    if (ks < 9) load(ks);
+    mfma_fence();
   }
   return s;
 }
 
+// oacc[db] += V^T P^T for value-column blocks db0 .. db0 + kNdb - 1 (operand
+// i: block db0 + i/2, key half i%2).
+template <int kNdb>
 __device__ __forceinline__ void s_pv(const char* tile, const bf16x8& p0, const bf16x8& p1,
-                                     f32x16* oacc, const SOffsets& o) {
+                                     f32x16* oacc, const SOffsets& o, int db0) {
+  bf16x8 vr[2 * kNdb];
+  auto read = [&](int i) {
+    return (i & 1) ? s_col8(tile, o, db0 + (i >> 1), 16, 24) : s_col8(tile, o, db0 + (i >> 1), 0, 8);
+  };
 #pragma unroll
-  for (int db = 0; db < 16; ++db) {
-    oacc[db] = mfma32(s_col8(tile, o, db, 0, 8), p0, oacc[db]);
-    oacc[db] = mfma32(s_col8(tile, o, db, 16, 24), p1, oacc[db]);
+  for (int i = 0; i < kSVAhead; ++i) vr[i] = read(i);
+#pragma unroll
+  for (int i = 0; i < 2 * kNdb; ++i) {
+    if (i + kSVAhead < 2 * kNdb) vr[i + kSVAhead] = read(i + kSVAhead);
+    oacc[i >> 1] = mfma32(vr[i], (i & 1) ? p1 : p0, oacc[i >> 1]);
+    mfma_fence();
   }
 }
 
