@@ -126,6 +126,9 @@ ls_status check_supported(const ls_attn_params* p) {
     return fail(LS_ERR_UNSUPPORTED, "bf16 path: n_q * n_q_heads * head_dim * 2 must be < 2^31");
   if (p->n_logical_pages >= (int64_t(1) << 29))
     return fail(LS_ERR_UNSUPPORTED, "bf16 path: n_logical_pages must be < 2^29");
+  // key positions relative to a split's first tile are held in 32 bits
+  if (kv_len_of(p) >= (int64_t(1) << 31))
+    return fail(LS_ERR_UNSUPPORTED, "bf16 path: q_pos0 + n_q must be < 2^31");
   return LS_OK;
 }
 

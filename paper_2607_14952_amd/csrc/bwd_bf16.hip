@@ -41,10 +41,10 @@ constexpr int kKTAhead = 4;   // transposed K operands in flight (two reads each
 
 // S^T = K Q^T and dP^T = V dO^T for one 32-key tile.  After step ks < 8,
 // load(ks) issues one instruction of the next stage's direct loads.
-template <typename Load>
+template <typename Load, typename Valu>
 __device__ __forceinline__ void scores_dp(const char* Ks, const char* Vs, const bf16x8* qreg,
                                           const bf16x8* dreg, const TileOffsets& o, f32x16& s,
-                                          f32x16& dp, Load&& load) {
+                                          f32x16& dp, Load&& load, Valu&& valu) {
   bf16x8 kr[16], vr[16];
 #pragma unroll
   for (int i = 0; i < kSDAhead; ++i) {
@@ -63,6 +63,7 @@ __device__ __forceinline__ void scores_dp(const char* Ks, const char* Vs, const 
     s = mfma32(kr[ks], qreg[ks], s);
     dp = mfma32(vr[ks], dreg[ks], dp);
     if (ks < 8) load(ks);
+    valu(ks);
     mfma_fence();
   }
 }
@@ -86,8 +87,42 @@ __device__ __forceinline__ void dq_update(const char* Ks, const bf16x8& d0, cons
   }
 }
 
-// One pipelined step (ring slots are distinct; see the forward kernel).  `pe`
-// holds the page-table entry of t0_next on entry and that of t0_after on return.
+// dS = P (dP - Delta) of one tile, P = exp2(s*scale*log2e - lse2) (masked
+// keys carry s = -inf, so P = 0), cut into pieces issued between the S/dP
+// MFMAs of the next tile: pieces 0-7 two elements each, 8 and 9 the packed
+// bf16 operand halves.
+struct DsPieces {
+  f32x16& s;
+  const f32x16& dp;
+  float c, lse2, delta;
+  bf16x8 d0, d1;
+  __device__ __forceinline__ void piece(int k) {
+    if (k < 8) {
+#pragma unroll
+      for (int r = 2 * k; r < 2 * k + 2; ++r)
+        s[r] = __builtin_amdgcn_exp2f(fmaf(s[r], c, -lse2)) * (dp[r] - delta);
+      // keep the exponentials here (the compiler would sink them to their use)
+      asm volatile("" ::"v"(s[2 * k]), "v"(s[2 * k + 1]));
+    } else if (k == 8) {
+      d0 = pack8(s, 0);
+      asm volatile("" ::"v"(d0));
+    } else if (k == 9) {
+      d1 = pack8(s, 1);
+      asm volatile("" ::"v"(d1));
+    }
+  }
+  __device__ __forceinline__ void all() {
+#pragma unroll
+    for (int k = 0; k < 10; ++k) piece(k);
+  }
+};
+
+// One pipelined step: S^T and dP^T of the tile in `cur`, with dS of the
+// previous tile (s_prev / dp_prev) computed between their MFMAs, then that
+// tile's dq product (K in `prev_k`).  Ring slots are distinct (see the forward
+// kernel).  `pe` holds the page-table entry of t0_next on entry and that of
+// t0_after on return; on return s_prev / dp_prev hold this tile's masked
+// scores and dP.
 template <bool kPerKey, bool kFirst>
 __device__ __forceinline__ void dq_step(const BwdArgs& a, char* __restrict__ next,
                                         const char* __restrict__ cur,
@@ -97,12 +132,16 @@ __device__ __forceinline__ void dq_step(const BwdArgs& a, char* __restrict__ nex
                                         int64_t t0, int64_t kb, int64_t k_all, int64_t my_lim,
                                         const bf16x8* qreg, const bf16x8* dreg,
                                         const TileOffsets& to, int hh, float lse2, float delta,
-                                        f32x16* acc, bf16x8& d0, bf16x8& d1) {
+                                        f32x16* acc, f32x16& s_prev, f32x16& dp_prev) {
+  DsPieces ds{s_prev, dp_prev, a.scale_log2, lse2, delta};
+  auto valu = [&](int k) {
+    if (!kFirst) ds.piece(k);
+  };
   f32x16 s, dp;
   if (kPerKey) {
     kf.issue_rows(next, a.page_table, a.log2_page, t0_next, k_hi);
     vf.issue_rows(next + kTileBytes, a.page_table, a.log2_page, t0_next, k_hi);
-    scores_dp(cur, cur + kTileBytes, qreg, dreg, to, s, dp, [](int) {});
+    scores_dp(cur, cur + kTileBytes, qreg, dreg, to, s, dp, [](int) {}, valu);
   } else {
     const int64_t prow_next = pl.row(pe, t0_next);
     pe = pl.load(t0_after);
@@ -112,21 +151,12 @@ __device__ __forceinline__ void dq_step(const BwdArgs& a, char* __restrict__ nex
     scores_dp(cur, cur + kTileBytes, qreg, dreg, to, s, dp, [&](int i) {
       if (i < 4) kf.issue_one(next, rk, i, nv);
       else vf.issue_one(next + kTileBytes, rv, i - 4, nv);
-    });
+    }, valu);
   }
-  const bool edge = t0 < kb || t0 + kQBN > k_all;
-#pragma unroll
-  for (int r = 0; r < 16; ++r) {
-    float p = __builtin_amdgcn_exp2f(fmaf(s[r], a.scale_log2, -lse2));
-    if (edge) {
-      const int64_t j = t0 + acc_key(r, hh);
-      if (j < kb || j >= my_lim) p = 0.f;
-    }
-    s[r] = p * (dp[r] - delta);          // dS
-  }
-  if (!kFirst) dq_update(prev_k, d0, d1, acc, to);
-  d0 = pack8(s, 0);
-  d1 = pack8(s, 1);
+  if (t0 < kb || t0 + kQBN > k_all) mask_keys(s, t0, kb, my_lim, hh);
+  if (!kFirst) dq_update(prev_k, ds.d0, ds.d1, acc, to);
+  s_prev = s;
+  dp_prev = dp;
 }
 
 template <bool kPerKey>
@@ -209,7 +239,7 @@ __global__ __launch_bounds__(256, 1) void bwd_dq_bf16_d256_kernel(BwdArgs a) {
   f32x16 acc[8];
 #pragma unroll
   for (int i = 0; i < 8; ++i) acc[i] = zero16();
-  bf16x8 d0, d1;
+  f32x16 s_prev, dp_prev;   // masked scores and dP of the previous tile
 
   // (a full wait here: the Q/dO loads may have been scheduled after the stages)
   wait_fetch();
@@ -219,7 +249,7 @@ __global__ __launch_bounds__(256, 1) void bwd_dq_bf16_d256_kernel(BwdArgs a) {
   {
     dq_step<kPerKey, true>(a, smem + kQAhead * kQStage, smem, smem, kf, vf, pl, pe, tile0(kQAhead),
                            tile0(kQAhead + 1), k_hi, k_lo, kb, k_all, my_lim, qreg, dreg, to, hh,
-                           lse2, delta, acc, d0, d1);
+                           lse2, delta, acc, s_prev, dp_prev);
     wait_fetch_but_newest_stage();
     tile_barrier();
   }
@@ -228,11 +258,16 @@ __global__ __launch_bounds__(256, 1) void bwd_dq_bf16_d256_kernel(BwdArgs a) {
     dq_step<kPerKey, false>(a, smem + ((t + kQAhead) % kQSlots) * kQStage,
                             smem + (t % kQSlots) * kQStage, smem + ((t - 1) % kQSlots) * kQStage,
                             kf, vf, pl, pe, tile0(t + kQAhead), tile0(t + kQAhead + 1), k_hi, t0,
-                            kb, k_all, my_lim, qreg, dreg, to, hh, lse2, delta, acc, d0, d1);
+                            kb, k_all, my_lim, qreg, dreg, to, hh, lse2, delta, acc, s_prev,
+                            dp_prev);
     wait_fetch_but_newest_stage();
     tile_barrier();
   }
-  dq_update(smem + ((n_tiles - 1) % kQSlots) * kQStage, d0, d1, acc, to);
+  {
+    DsPieces ds{s_prev, dp_prev, a.scale_log2, lse2, delta};
+    ds.all();
+    dq_update(smem + ((n_tiles - 1) % kQSlots) * kQStage, ds.d0, ds.d1, acc, to);
+  }
   wait_fetch();   // no direct load is left in flight when the waves end
 
   if (row_ok) {
@@ -396,7 +431,7 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_bf16_d256_kernel(BwdArgs a, i
     __builtin_amdgcn_sched_barrier(0);
     f32x16 s, dp;
     scores_dp(cur, cur + kTileBytes, kreg, vreg, to, s, dp,
-              [&](int i) { fetch(next, row_next, i); });
+              [&](int i) { fetch(next, row_next, i); }, [](int) {});
     const float* st = reinterpret_cast<const float*>(cur + 2 * kTileBytes + kRStat * w);
     const int row0 = row_lo + 32 * t;
     const bool edge = a.q_pos0 + (row0 >> lg) < jw + 31 || row0 + 32 > rows_total;

@@ -1,24 +1,27 @@
 // bf16 split-KV forward for head_dim = 256 on gfx950 (Eq. qwen-local-attn).
 //
-// Workgroup = 4 waves = 128 packed query rows of one KV head: packed row r is
-// (token r / G, head g*G + r % G), so every K/V tile staged in LDS feeds all G
-// query heads that share it.  Each wave owns 32 rows; lane l owns row l % 32
-// (scores are computed transposed, S^T = K Q^T, so row statistics stay in one
-// lane).
+// Workgroup = 8 waves (4 for pages shorter than a tile) = 32 packed query rows
+// per wave of one KV head: packed row r is (token r / G, head g*G + r % G), so
+// every K/V tile staged in LDS feeds all G query heads that share it.  Lane l
+// owns row l % 32 (scores are computed transposed, S^T = K Q^T, so row
+// statistics stay in one lane).
 //
 // Keys are processed in 32-key tiles aligned to multiples of 32 (one page-table
 // entry per tile when pages hold >= 32 positions).  K and V rows are fetched
 // with direct global->LDS loads into a four-slot ring, two tiles ahead (each
 // wave waits only for the older of the two stages in flight); no VGPRs stage
-// them.  The K^T operand is one 16-byte LDS read per lane; the V^T
-// operand comes from transposing LDS reads of the row-major V tile.
+// them.  The K^T operand is one 16-byte LDS read per lane; the V^T operand
+// comes from transposing LDS reads of the row-major V tile.
 //
-// The loop is software-pipelined across tiles: iteration t issues the score
-// MFMAs of tile t, then the softmax of tile t (exp2 on the VALU) in the same
-// basic block as the PV MFMAs of tile t-1.  Statistics stay in fp32 registers
-// (base-2 exponent with the scale folded in); P is rounded to bf16 for the PV
-// product.  The split writes the normalized fp32 output and the natural-log
-// normalizer.
+// With 8 waves two waves share each SIMD, so one wave's softmax (exp2 on the
+// VALU) and LDS reads run beside the other's MFMAs; each wave fits in 256
+// registers (Q 64, O 128) with shallow operand rings and one-register LDS
+// offsets.  With 4 waves (one per SIMD) the loop is software-pipelined within
+// the wave instead: the softmax of tile t-1 is issued between the score MFMAs
+// of tile t, followed by the PV MFMAs of tile t-1.  Statistics stay in fp32
+// registers (base-2 exponent with the scale folded in); P is rounded to bf16
+// for the PV product.  The split writes the normalized fp32 output and the
+// natural-log normalizer.
 #include <math.h>
 
 #include "ls_internal.h"
@@ -28,32 +31,36 @@ namespace ls {
 namespace {
 
 constexpr int kD = 256;
-constexpr int kBM = 128;
 constexpr int kBN = kTileKeys;              // 32
 constexpr int kStage = 2 * kTileBytes;      // K tile + V tile
 constexpr int kAhead = 2;                   // tiles in flight beyond the one consumed
 constexpr int kSlots = kAhead + 2;          // + the tile being scored + the V of the previous one
 
-// Operand reads run a fixed number of MFMAs ahead of their use (see mfma_fence).
-constexpr int kKAhead = 6;   // K operand reads in flight (16-byte reads)
-constexpr int kVAhead = 4;   // V operands in flight (two transposing reads each)
+// Operand reads run a fixed number of MFMAs ahead of their use (see mfma_fence):
+// K operand reads in flight (16-byte reads) and V operands in flight (two
+// transposing reads each).  With two waves per SIMD the shallower rings keep
+// each wave within 256 registers.
+template <int kWaves> constexpr int kKAhead = kWaves == 4 ? 6 : 2;
+template <int kWaves> constexpr int kVAhead = kWaves == 4 ? 4 : 2;
 
 // S^T (32 keys x this lane's row) = K Q^T over the 256-wide head.  After
-// MFMA ks < 8, load(ks) issues one instruction of the next stage's direct
-// loads, so their issue overlaps the MFMA chain.
-template <typename Load>
-__device__ __forceinline__ f32x16 scores(const char* Ks, const bf16x8* qreg, const TileOffsets& o,
-                                         Load&& load) {
+// MFMA ks < kLoads, load(ks) issues one instruction of the next stage's direct
+// loads, so their issue overlaps the MFMA chain; valu(ks) issues a piece of
+// the previous tile's softmax.
+template <int kLoads, int kAheadK, typename Load, typename Valu>
+__device__ __forceinline__ f32x16 scores(const char* Ks, const bf16x8* qreg, const TileBase& o,
+                                         Load&& load, Valu&& valu) {
   bf16x8 kreg[16];
 #pragma unroll
-  for (int i = 0; i < kKAhead; ++i) kreg[i] = tile_row16(Ks, o, i);
+  for (int i = 0; i < kAheadK; ++i) kreg[i] = tile_row16(Ks, o, i);
   mfma_fence();
   f32x16 s = zero16();
 #pragma unroll
   for (int ks = 0; ks < 16; ++ks) {
-    if (ks + kKAhead < 16) kreg[ks + kKAhead] = tile_row16(Ks, o, ks + kKAhead);
+    if (ks + kAheadK < 16) kreg[ks + kAheadK] = tile_row16(Ks, o, ks + kAheadK);
     s = mfma32(kreg[ks], qreg[ks], s);
-    if (ks < 8) load(ks);
+    if (ks < kLoads) load(ks);
+    valu(ks);
     mfma_fence();
   }
   return s;
@@ -62,97 +69,147 @@ __device__ __forceinline__ f32x16 scores(const char* Ks, const bf16x8* qreg, con
 // O^T += V^T P^T for one 32-key tile.  P's register block kk holds keys
 // 16kk + {4h..4h+3, 8+4h..8+4h+3}; the V^T operand reads the same keys.
 // Operand i is dims block i/2, key half i%2.
+template <int kAheadV>
 __device__ __forceinline__ void pv(const char* Vs, const bf16x8& p0, const bf16x8& p1,
-                                   f32x16* oacc, const TileOffsets& o) {
+                                   f32x16* oacc, const TileBase& o) {
   bf16x8 vreg[16];
   auto read = [&](int i) {
     return (i & 1) ? tile_col8(Vs, o, i >> 1, 16, 24) : tile_col8(Vs, o, i >> 1, 0, 8);
   };
 #pragma unroll
-  for (int i = 0; i < kVAhead; ++i) vreg[i] = read(i);
+  for (int i = 0; i < kAheadV; ++i) vreg[i] = read(i);
 #pragma unroll
   for (int i = 0; i < 16; ++i) {
-    if (i + kVAhead < 16) vreg[i + kVAhead] = read(i + kVAhead);
+    if (i + kAheadV < 16) vreg[i + kAheadV] = read(i + kAheadV);
     oacc[i >> 1] = mfma32(vreg[i], (i & 1) ? p1 : p0, oacc[i >> 1]);
     mfma_fence();
   }
 }
 
-// Keys outside [lo, lim) (split begin, causal edge or split end) get -inf.
-__device__ __forceinline__ void mask_tile(f32x16& s, int64_t t0, int64_t lo, int64_t lim, int hh) {
-#pragma unroll
-  for (int r = 0; r < 16; ++r) {
-    const int64_t j = t0 + acc_key(r, hh);
-    if (j < lo || j >= lim) s[r] = -INFINITY;
-  }
-}
-
 // Online softmax step over one tile (base-2, scale folded in): s becomes
-// exp2(s*c - m_new); returns alpha = exp2(m_old - m_new), the factor that
-// rescales earlier partial sums.  A row with no visible key so far keeps
-// m = -inf and P = 0.
-__device__ __forceinline__ float softmax_tile(f32x16& s, float c, float& m_run, float& l_run) {
-  float mx = s[0];
+// exp2(s*c - m_new), alpha = exp2(m_old - m_new) rescales earlier partial
+// sums, and a row with no visible key so far keeps m = -inf and P = 0.  The
+// step is cut into pieces issued between the score MFMAs of the next tile so
+// that its VALU work overlaps the MFMA chain: pieces 0-1 the row max and
+// alpha, 2-9 two exponentials each, 10 the running sum and P's first half, 11
+// the second.
+struct OnlineSoftmax {
+  f32x16& s;
+  float c;
+  float& m_run;
+  float& l_run;
+  float mx, m_use, alpha, psum;
+  bf16x8 p0, p1;
+  __device__ __forceinline__ void piece(int k) {
+    if (k == 0) {
+      mx = s[0];
 #pragma unroll
-  for (int r = 1; r < 16; ++r) mx = fmaxf(mx, s[r]);
-  mx = half_max(mx);
-  const float m_new = fmaxf(m_run, mx * c);
-  const float m_use = m_new == -INFINITY ? 0.f : m_new;
-  const float alpha = __builtin_amdgcn_exp2f(m_run - m_use);
-  float psum = 0.f;
+      for (int r = 1; r < 8; ++r) mx = fmaxf(mx, s[r]);
+    } else if (k == 1) {
 #pragma unroll
-  for (int r = 0; r < 16; ++r) {
-    s[r] = __builtin_amdgcn_exp2f(fmaf(s[r], c, -m_use));
-    psum += s[r];
+      for (int r = 8; r < 16; ++r) mx = fmaxf(mx, s[r]);
+      mx = half_max(mx);
+      const float m_new = fmaxf(m_run, mx * c);
+      m_use = m_new == -INFINITY ? 0.f : m_new;
+      alpha = __builtin_amdgcn_exp2f(m_run - m_use);
+      m_run = m_new;
+      psum = 0.f;
+    } else if (k < 10) {
+      const int r = 2 * (k - 2);
+      s[r] = __builtin_amdgcn_exp2f(fmaf(s[r], c, -m_use));
+      s[r + 1] = __builtin_amdgcn_exp2f(fmaf(s[r + 1], c, -m_use));
+      psum += s[r] + s[r + 1];
+      // keep the exponentials here (the compiler would sink them to their use)
+      asm volatile("" ::"v"(s[r]), "v"(s[r + 1]));
+    } else if (k == 10) {
+      l_run = fmaf(l_run, alpha, psum);
+      p0 = pack8(s, 0);
+      asm volatile("" ::"v"(p0));
+    } else if (k == 11) {
+      p1 = pack8(s, 1);
+      asm volatile("" ::"v"(p1));
+    }
   }
-  l_run = fmaf(l_run, alpha, psum);
-  m_run = m_new;
-  return alpha;
+  __device__ __forceinline__ void all() {
+#pragma unroll
+    for (int k = 0; k < 12; ++k) piece(k);
+  }
+};
+
+// O^T = alpha * O^T + V^T P^T for the tile whose softmax `sm` holds.
+template <int kAheadV>
+__device__ __forceinline__ void rescale_pv(const char* Vs, const OnlineSoftmax& sm,
+                                           const float& l_run, f32x16* oacc,
+                                           const TileBase& to) {
+  // (l_run < 0 never holds; it keeps the exponentials ahead of this branch)
+  if (__any(sm.alpha != 1.f || l_run < 0.f)) {
+#pragma unroll
+    for (int i = 0; i < 8; ++i) oacc[i] *= sm.alpha;
+  }
+  pv<kAheadV>(Vs, sm.p0, sm.p1, oacc, to);
 }
 
-// One pipelined step: scores of the tile in `ks_cur`, the PV product of the
-// previous tile (V in `vs_prev`, P in p0/p1), while the tile at t0_next streams
-// into `next`.  The three LDS regions are distinct ring slots; the restrict
-// qualifiers tell the compiler so, which lets it keep LDS reads running while
-// the direct loads into `next` are in flight.  `pe` holds the page-table entry
-// of t0_next on entry and that of t0_after on return.
-template <bool kPerKey, bool kFirst>
-__device__ __forceinline__ float step(const FwdArgs& a, char* __restrict__ next,
-                                      const char* __restrict__ ks_cur,
-                                      const char* __restrict__ vs_prev, const TileFetch& kf,
-                                      const TileFetch& vf, const PageLookup& pl, int32_t& pe,
-                                      int64_t t0_next, int64_t t0_after, int64_t k_hi, int64_t t0,
-                                      int64_t kb, int64_t k_all, int64_t my_lim,
-                                      const bf16x8* qreg, const TileOffsets& to, int hh,
-                                      f32x16* oacc, bf16x8& p0, bf16x8& p1, float& m_run,
-                                      float& l_run) {
+// One step: the scores of the tile in `ks_cur` while the tile at t0_next
+// streams into `next`.  With kOverlap (one wave per SIMD) the online softmax of
+// the previous tile's scores (`s_prev`) is spread between the score MFMAs, then
+// the previous tile's rescale and PV product follow (V in `vs_prev`), and on
+// return s_prev holds this tile's masked scores.  Without it (two waves per
+// SIMD, whose MFMAs and VALU work interleave) the step finishes its own tile:
+// softmax, rescale and PV with the V half of `ks_cur`.  The LDS regions are
+// distinct ring slots; the restrict qualifiers tell the compiler so, which
+// lets it keep LDS reads running while the direct loads into `next` are in
+// flight.  `pe` holds the page-table entry of t0_next on entry and that of
+// t0_after on return.
+template <bool kPerKey, bool kFirst, bool kOverlap, int kInstr, int kAheadK, int kAheadV>
+__device__ __forceinline__ void step(const FwdArgs& a, char* __restrict__ next,
+                                     const char* __restrict__ ks_cur,
+                                     const char* __restrict__ vs_prev, const TileFetchN<kInstr>& kf,
+                                     const TileFetchN<kInstr>& vf, const PageLookup& pl, int32_t& pe,
+                                     int64_t t0_next, int64_t t0_after, int64_t k_hi, int64_t t0,
+                                     int64_t k_lo, int64_t kb, int64_t k_all, int lim_rel,
+                                     const bf16x8* qreg,
+                                     const TileBase& to, int hh, f32x16* oacc, f32x16& s_prev,
+                                     float& m_run, float& l_run) {
+  OnlineSoftmax sm{s_prev, a.scale_log2, m_run, l_run};
+  auto valu = [&](int k) {
+    if (kOverlap && !kFirst) sm.piece(k);
+  };
   f32x16 s;
   if (kPerKey) {
     kf.issue_rows(next, a.page_table, a.log2_page, t0_next, k_hi);
     vf.issue_rows(next + kTileBytes, a.page_table, a.log2_page, t0_next, k_hi);
-    s = scores(ks_cur, qreg, to, [](int) {});
+    s = scores<0, kAheadK>(ks_cur, qreg, to, [](int) {}, valu);
   } else {
     const int64_t prow_next = pl.row(pe, t0_next);
     pe = pl.load(t0_after);
     __builtin_amdgcn_sched_barrier(0);   // the entry load stays ahead of the stage's loads
     const __amdgpu_buffer_rsrc_t rk = kf.page_rsrc(prow_next), rv = vf.page_rsrc(prow_next);
     const int nv = (int)min(k_hi - t0_next, (int64_t)kBN);
-    s = scores(ks_cur, qreg, to, [&](int i) {
-      if (i < 4) kf.issue_one(next, rk, i, nv);
-      else vf.issue_one(next + kTileBytes, rv, i - 4, nv);
-    });
+    s = scores<2 * kInstr, kAheadK>(ks_cur, qreg, to, [&](int i) {
+      if (i < kInstr) kf.issue_one(next, rk, i, nv);
+      else vf.issue_one(next + kTileBytes, rv, i - kInstr, nv);
+    }, valu);
   }
-  if (t0 < kb || t0 + kBN > k_all) mask_tile(s, t0, kb, my_lim, hh);
-  const float alpha = softmax_tile(s, a.scale_log2, m_run, l_run);
-  if (!kFirst) pv(vs_prev, p0, p1, oacc, to);
-  p0 = pack8(s, 0);
-  p1 = pack8(s, 1);
-  return alpha;
+  if (t0 < kb || t0 + kBN > k_all) mask_keys_rel(s, (int)(t0 - k_lo), (int)(kb - k_lo), lim_rel, hh);
+  if (kOverlap) {
+    if (!kFirst) rescale_pv<kAheadV>(vs_prev, sm, l_run, oacc, to);
+    s_prev = s;
+  } else {
+    OnlineSoftmax cur{s, a.scale_log2, m_run, l_run};
+    cur.all();
+    rescale_pv<kAheadV>(ks_cur + kTileBytes, cur, l_run, oacc, to);
+  }
 }
 
-template <bool kPerKey>
-__global__ __launch_bounds__(256, 1) void fwd_bf16_d256_kernel(FwdArgs a) {
+// Workgroup = kWaves waves = 32 * kWaves packed rows; with 8 waves two waves
+// share each SIMD (one's VALU and LDS work overlaps the other's MFMAs).
+template <bool kPerKey, int kWaves>
+__global__ __launch_bounds__(64 * kWaves, 1) void fwd_bf16_d256_kernel(FwdArgs a) {
   __shared__ __attribute__((aligned(1024))) char smem[kSlots * kStage];
+  constexpr int kBM = 32 * kWaves;
+  constexpr int kInstr = 16 / kWaves;   // direct-load instructions per wave per 16 KiB tile
+  constexpr bool kOverlap = kWaves == 4;
+  constexpr int kAK = kKAhead<kWaves>, kAV = kVAhead<kWaves>;
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave-uniform (scalar)
@@ -172,6 +229,7 @@ __global__ __launch_bounds__(256, 1) void fwd_bf16_d256_kernel(FwdArgs a) {
   const int64_t k_all = min(ke, a.q_pos0 + tok_first + 1); // below: visible to every row
   const int64_t my_lim = min(ke, a.q_pos0 + tok + 1);
   const int64_t k_lo = kb & ~int64_t(kBN - 1);              // tile origin
+  const int lim_rel = (int)(my_lim - k_lo);                  // (a split spans < 2^31 keys)
 
   float* out = a.out_part + (((int64_t)sp * a.n_q + tok) * a.n_q_heads + head) * kD;
   float* lse_out = a.lse_part + (int64_t)sp * a.n_q * a.n_q_heads + (int64_t)head * a.n_q + tok;
@@ -186,7 +244,7 @@ __global__ __launch_bounds__(256, 1) void fwd_bf16_d256_kernel(FwdArgs a) {
     return;
   }
 
-  TileFetch kf, vf;
+  TileFetchN<kInstr> kf, vf;
   kf.init(static_cast<const __bf16*>(a.k_pool) + (int64_t)g * kD, a.k_pos_stride, lane, w);
   vf.init(static_cast<const __bf16*>(a.v_pool) + (int64_t)g * kD, a.v_pos_stride, lane, w);
   // Tile t lies in one page unless pages are shorter than a tile; in the loop
@@ -201,10 +259,10 @@ __global__ __launch_bounds__(256, 1) void fwd_bf16_d256_kernel(FwdArgs a) {
   auto fetch = [&](int t, int slot, int64_t prow) {
     const int64_t t0 = k_lo + (int64_t)t * kBN;
     char* st = smem + slot * kStage;
-    kf.issue<kPerKey>(st, a.page_table, a.log2_page, t0, k_hi, prow);
-    vf.issue<kPerKey>(st + kTileBytes, a.page_table, a.log2_page, t0, k_hi, prow);
+    kf.template issue<kPerKey>(st, a.page_table, a.log2_page, t0, k_hi, prow);
+    vf.template issue<kPerKey>(st + kTileBytes, a.page_table, a.log2_page, t0, k_hi, prow);
   };
-  const TileOffsets to = tile_offsets(lane);
+  const TileBase to = tile_base(lane);
   // tiles past the last one are clamped to it (refetched into an unread slot),
   // so every iteration issues exactly one stage of direct loads
   auto clamp = [&](int t) { return t < n_tiles ? t : n_tiles - 1; };
@@ -232,37 +290,39 @@ __global__ __launch_bounds__(256, 1) void fwd_bf16_d256_kernel(FwdArgs a) {
 #pragma unroll
   for (int i = 0; i < 8; ++i) oacc[i] = zero16();
   float m_run = -INFINITY, l_run = 0.f;
-  bf16x8 p0, p1;   // packed P of the previous tile
+  f32x16 s_prev;   // masked scores of the previous tile, before its softmax
 
   // (a full wait here: the Q loads may have been scheduled after the stages)
   wait_fetch();
   tile_barrier();
 
-  // tile 0 (peeled: no previous P to multiply).  Iteration t fetches tile
-  // t + kAhead and, before its barrier, waits for the loads of tile t + 1.
-  {
-    step<kPerKey, true>(a, smem + kAhead * kStage, smem, smem + kTileBytes, kf, vf, pl, pe,
-                        tile0(kAhead), tile0(kAhead + 1), k_hi, k_lo, kb, k_all, my_lim, qreg, to,
-                        hh, oacc, p0, p1, m_run, l_run);
-    wait_fetch_but_newest_stage();
+  // Iteration t fetches tile t + kAhead and, before its barrier, waits for
+  // the loads of tile t + 1.  With kOverlap tile 0 is peeled (no previous
+  // tile) and the last tile's softmax and PV follow the loop.
+  int t = 0;
+  if (kOverlap) {
+    step<kPerKey, true, kOverlap, kInstr, kAK, kAV>(
+        a, smem + kAhead * kStage, smem, smem + kTileBytes, kf, vf, pl, pe, tile0(kAhead),
+        tile0(kAhead + 1), k_hi, k_lo, k_lo, kb, k_all, lim_rel, qreg, to, hh, oacc, s_prev, m_run, l_run);
+    wait_newest_stage<2 * kInstr>();
     tile_barrier();
+    t = 1;
   }
-  for (int t = 1; t < n_tiles; ++t) {
+  for (; t < n_tiles; ++t) {
     const int64_t t0 = k_lo + (int64_t)t * kBN;
-    const float alpha = step<kPerKey, false>(
+    step<kPerKey, false, kOverlap, kInstr, kAK, kAV>(
         a, smem + ((t + kAhead) % kSlots) * kStage, smem + (t % kSlots) * kStage,
         smem + ((t - 1) % kSlots) * kStage + kTileBytes, kf, vf, pl, pe, tile0(t + kAhead),
-        tile0(t + kAhead + 1), k_hi, t0, kb, k_all, my_lim, qreg, to, hh, oacc, p0, p1, m_run,
+        tile0(t + kAhead + 1), k_hi, t0, k_lo, kb, k_all, lim_rel, qreg, to, hh, oacc, s_prev, m_run,
         l_run);
-    // (l_run < 0 never holds; it keeps the exponentials ahead of this branch)
-    if (__any(alpha != 1.f || l_run < 0.f)) {
-#pragma unroll
-      for (int i = 0; i < 8; ++i) oacc[i] *= alpha;
-    }
-    wait_fetch_but_newest_stage();
+    wait_newest_stage<2 * kInstr>();
     tile_barrier();
   }
-  pv(smem + ((n_tiles - 1) % kSlots) * kStage + kTileBytes, p0, p1, oacc, to);
+  if (kOverlap) {
+    OnlineSoftmax sm{s_prev, a.scale_log2, m_run, l_run};
+    sm.all();
+    rescale_pv<kAV>(smem + ((n_tiles - 1) % kSlots) * kStage + kTileBytes, sm, l_run, oacc, to);
+  }
   wait_fetch();   // no direct load is left in flight when the waves end
 
   const float l_tot = half_sum(l_run);
@@ -285,16 +345,26 @@ __global__ __launch_bounds__(256, 1) void fwd_bf16_d256_kernel(FwdArgs a) {
   }
 }
 
-}  // namespace
+#ifndef LS_FWD_WAVES
+#define LS_FWD_WAVES 8
+#endif
 
-hipError_t launch_fwd_bf16_d256(const FwdArgs& a, hipStream_t stream) {
+template <bool kPerKey, int kWaves>
+hipError_t launch_waves(const FwdArgs& a, hipStream_t stream) {
+  constexpr int kBM = 32 * kWaves;
   const unsigned row_tiles = (unsigned)(((int64_t)a.n_q * a.group + kBM - 1) / kBM);
   const dim3 grid(row_tiles, a.n_kv_heads, a.n_splits);
-  if (a.log2_page < 5)
-    hipLaunchKernelGGL(fwd_bf16_d256_kernel<true>, grid, dim3(256), 0, stream, a);
-  else
-    hipLaunchKernelGGL(fwd_bf16_d256_kernel<false>, grid, dim3(256), 0, stream, a);
+  hipLaunchKernelGGL((fwd_bf16_d256_kernel<kPerKey, kWaves>), grid, dim3(64 * kWaves), 0, stream, a);
   return hipGetLastError();
+}
+
+}  // namespace
+
+// Pages of at least one tile take the two-waves-per-SIMD kernel; shorter
+// pages (one lookup per key row, more registers) take four waves.
+hipError_t launch_fwd_bf16_d256(const FwdArgs& a, hipStream_t stream) {
+  if (a.log2_page < 5) return launch_waves<true, 4>(a, stream);
+  return launch_waves<false, LS_FWD_WAVES>(a, stream);
 }
 
 }  // namespace ls

@@ -142,6 +142,65 @@ __device__ __forceinline__ bf16x8 tile_col8(const char* tile, const TileOffsets&
   return __builtin_bit_cast(bf16x8, __builtin_shufflevector(a, b, 0, 1, 2, 3, 4, 5, 6, 7));
 }
 
+// The same offsets from one register each: the swizzle only XORs the
+// low chunk bits, so row_off[q] = row ^ 32q and col_off[par][d] =
+// col ^ (64d + 32par).  Costs a VALU XOR per read instead of 16 registers.
+struct TileBase {
+  int row;
+  int col;
+};
+
+__host__ __device__ inline TileBase tile_base(int lane) {
+  const int l32 = lane & 31, h = lane >> 5;
+  const int sw = tile_swz(l32);
+  const int s = lane & 15;
+  const int x = 2 * ((lane >> 4) & 1) + ((s & 3) >> 1);
+  const int row = 4 * h + (s >> 2);
+  TileBase b;
+  b.row = l32 * kTileRow + ((h ^ (sw & 1)) << 4) + ((sw >> 1) << 5);
+  b.col = row * kTileRow + ((s & 1) << 3) + ((row & 3) << 6) + ((x ^ (row >> 2)) << 4);
+  return b;
+}
+
+__host__ __device__ inline int tile_row_offset(const TileBase& b, int ks) {
+  return (b.row ^ ((ks & 7) << 5)) + 256 * (ks >> 3);
+}
+
+__host__ __device__ inline int tile_col_offset(const TileBase& b, int db, int r) {
+  return (b.col ^ (((db & 3) << 6) | (((r >> 3) & 1) << 5))) + 256 * (db >> 2) + r * kTileRow;
+}
+
+__device__ __forceinline__ bf16x8 tile_row16(const char* tile, const TileBase& b, int ks) {
+  return *reinterpret_cast<const bf16x8*>(tile + tile_row_offset(b, ks));
+}
+
+__device__ __forceinline__ bf16x8 tile_col8(const char* tile, const TileBase& b, int db, int r0,
+                                            int r1) {
+  const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(LS_LDS4(tile + tile_col_offset(b, db, r0)));
+  const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(LS_LDS4(tile + tile_col_offset(b, db, r1)));
+  return __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+}
+
+// Score tile of keys t0 .. t0+31 (result register layout above): keys outside
+// [lo, lim) (range begin, causal edge or range end) get -inf.
+__device__ __forceinline__ void mask_keys(f32x16& s, int64_t t0, int64_t lo, int64_t lim, int hh) {
+#pragma unroll
+  for (int r = 0; r < 16; ++r) {
+    const int64_t j = t0 + acc_key(r, hh);
+    if (j < lo || j >= lim) s[r] = -INFINITY;
+  }
+}
+
+// The same with positions relative to a common origin (32-bit, so the bound
+// held per lane takes one register).
+__device__ __forceinline__ void mask_keys_rel(f32x16& s, int t0, int lo, int lim, int hh) {
+#pragma unroll
+  for (int r = 0; r < 16; ++r) {
+    const int j = t0 + acc_key(r, hh);
+    if (j < lo || j >= lim) s[r] = -INFINITY;
+  }
+}
+
 // Scheduling fence placed after every MFMA of an operand pipeline: LDS reads
 // and MFMAs keep their source order (VALU and SALU work may still move across),
 // so operand reads issued a fixed number of MFMAs ahead stay ahead and each
@@ -199,10 +258,10 @@ struct PageLookup {
 };
 
 // Direct global->LDS loads of the key rows [t0, t0 + 32) of one KV head into
-// a tile (swizzled layout above).  Each wave writes rows 8w .. 8w+7 with four
-// 1 KiB instructions: lane l of instruction i carries row 8w + 2i + l/32,
-// physical chunk l % 32 (logical chunk (l % 32) ^ tile_swz(row)).  Completion
-// is tracked by vmcnt.
+// a tile (swizzled layout above).  With n waves each wave writes 32 / n rows
+// with kInstr = 16 / n 1 KiB instructions: lane l of instruction i of wave w
+// carries row 2 kInstr w + 2i + l/32, physical chunk l % 32 (logical chunk
+// (l % 32) ^ tile_swz(row)).  Completion is tracked by vmcnt.
 //
 // Tiles inside one page use buffer loads (MUBUF) with the page's first row as
 // the resource base and 32-bit lane offsets.  Unlike the FLAT-encoded
@@ -210,20 +269,21 @@ struct PageLookup {
 // for the compiler's wait insertion, so LDS reads issued while they are in
 // flight keep partial waits.  Pages shorter than a tile use the per-row FLAT
 // form.
-struct TileFetch {
+template <int kInstr = 4>   // 1 KiB instructions per wave per 16 KiB tile (16 / waves)
+struct TileFetchN {
   const char* pool;    // pool base + KV head offset (bytes)
   int64_t row_bytes;   // bytes between positions
-  int lane_off[4];     // byte offset (logical chunk * 16) of the lane's source in its row
-  int lds_row[4];      // first LDS row written by instruction i
-  int lane_row[4];     // row carried by this lane in instruction i
+  int lane_off[kInstr];  // byte offset (logical chunk * 16) of the lane's source in its row
+  int lds_row[kInstr];   // first LDS row written by instruction i
+  int lane_row[kInstr];  // row carried by this lane in instruction i
 
   __host__ __device__ inline void init(const void* pool_head, int64_t pos_stride_elems, int lane,
                                         int w) {
     pool = static_cast<const char*>(pool_head);
     row_bytes = pos_stride_elems * 2;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      lds_row[i] = 8 * w + 2 * i;
+    for (int i = 0; i < kInstr; ++i) {
+      lds_row[i] = 2 * kInstr * w + 2 * i;
       lane_row[i] = lds_row[i] + (lane >> 5);
       lane_off[i] = ((lane & 31) ^ tile_swz(lane_row[i])) * 16;
     }
@@ -235,7 +295,7 @@ struct TileFetch {
                                              0x7FFFFFFF, 0x00020000);
   }
 
-  // Load instruction i (0..3) of a tile inside one page (resource from
+  // Load instruction i (< kInstr) of a tile inside one page (resource from
   // page_rsrc of its first row); rows at or beyond n_valid (1 <= n_valid <= 32)
   // repeat row n_valid - 1.  32 rows of a page span less than 2 GiB, so the
   // lane offsets are 32-bit.
@@ -252,14 +312,14 @@ struct TileFetch {
   __device__ __forceinline__ void issue_page(char* tile, int64_t prow, int n_valid) const {
     const __amdgpu_buffer_rsrc_t r = page_rsrc(prow);
 #pragma unroll
-    for (int i = 0; i < 4; ++i) issue_one(tile, r, i, n_valid);
+    for (int i = 0; i < kInstr; ++i) issue_one(tile, r, i, n_valid);
   }
 
   // Any tile: one page-table lookup per row; rows at or beyond k_hi repeat k_hi - 1.
   __device__ __forceinline__ void issue_rows(char* tile, const int32_t* __restrict__ table,
                                              int log2_page, int64_t t0, int64_t k_hi) const {
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
+    for (int i = 0; i < kInstr; ++i) {
       int64_t j = t0 + lane_row[i];
       if (j >= k_hi) j = k_hi - 1;
       __builtin_amdgcn_global_load_lds(pool + phys_pos(table, j, log2_page) * row_bytes + lane_off[i],
@@ -278,6 +338,7 @@ struct TileFetch {
     }
   }
 };
+using TileFetch = TileFetchN<4>;
 
 // Wait for this wave's direct loads (vmcnt = 0).
 __device__ __forceinline__ void wait_fetch() { __builtin_amdgcn_s_waitcnt(0x0F70); }
@@ -286,6 +347,13 @@ __device__ __forceinline__ void wait_fetch() { __builtin_amdgcn_s_waitcnt(0x0F70
 // (vmcnt = 8: a stage is 4 K and 4 V instructions per wave, and they are the
 // newest vector-memory operations when this is reached).
 __device__ __forceinline__ void wait_fetch_but_newest_stage() { __builtin_amdgcn_s_waitcnt(0x0F78); }
+
+// The same for a stage of kN instructions (kN < 16).
+template <int kN>
+__device__ __forceinline__ void wait_newest_stage() {
+  static_assert(kN > 0 && kN < 16, "vmcnt immediate");
+  __builtin_amdgcn_s_waitcnt(0x0F70 | kN);
+}
 
 // Workgroup barrier without the release/acquire fence of __syncthreads: that
 // fence counts the direct loads as LDS writes and would wait for every one in

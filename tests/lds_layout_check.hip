@@ -78,9 +78,38 @@ static void dense() {
       }
     }
   for (int v : tag) CHECK(v >= 0, "dense fetch leaves a slot unwritten");
+  // eight waves with two instructions each write the same tile image
+  {
+    std::vector<int> tag8(kTileBytes / 2, -1);
+    for (int w = 0; w < 8; ++w)
+      for (int lane = 0; lane < 64; ++lane) {
+        TileFetchN<2> f;
+        f.init(nullptr, cols, lane, w);
+        for (int i = 0; i < 2; ++i) {
+          const int dst = f.lds_row[i] * kTileRow + 16 * lane;
+          for (int e = 0; e < 8; ++e) {
+            CHECK(tag8[dst / 2 + e] == -1, "8-wave fetch writes slot %d twice", dst / 2 + e);
+            tag8[dst / 2 + e] = f.lane_row[i] * cols + (int)(f.lane_off[i] / 2) + e;
+          }
+        }
+      }
+    CHECK(tag8 == tag, "8-wave fetch lays the tile out differently");
+  }
 
   TileOffsets o[64];
   for (int l = 0; l < 64; ++l) o[l] = tile_offsets(l);
+  // the one-register form gives the table's offsets
+  for (int l = 0; l < 64; ++l) {
+    const TileBase b = tile_base(l);
+    for (int ks = 0; ks < 16; ++ks)
+      CHECK(tile_row_offset(b, ks) == o[l].row_off[ks & 7] + 256 * (ks >> 3),
+            "compact row offset lane=%d ks=%d", l, ks);
+    for (int db = 0; db < 8; ++db)
+      for (int r = 0; r < 32; r += 8)
+        CHECK(tile_col_offset(b, db, r) ==
+                  256 * (db >> 2) + o[l].col_off[(r >> 3) & 1][db & 3] + r * kTileRow,
+              "compact column offset lane=%d db=%d r=%d", l, db, r);
+  }
   for (int ks = 0; ks < 16; ++ks) {
     int off[64];
     for (int l = 0; l < 64; ++l) {
