@@ -36,7 +36,7 @@ constexpr int kQAhead = 2;                        // tiles in flight beyond the 
 constexpr int kQSlots = kQAhead + 2;
 
 // Operand reads run a fixed number of MFMAs ahead of their use (see mfma_fence).
-constexpr int kSDAhead = 3;   // steps of (K row, V row) reads in flight
+constexpr int kSDAhead = 2;   // steps of (K row, V row) reads in flight
 constexpr int kKTAhead = 4;   // transposed K operands in flight (two reads each)
 
 // S^T = K Q^T and dP^T = V dO^T for one 32-key tile.  After step ks < 8,

@@ -361,9 +361,12 @@ hipError_t launch_waves(const FwdArgs& a, hipStream_t stream) {
 }  // namespace
 
 // Pages of at least one tile take the two-waves-per-SIMD kernel; shorter
-// pages (one lookup per key row, more registers) take four waves.
+// pages (one lookup per key row, more registers) take four waves, and so do
+// calls with at most 128 packed rows, which would leave half of a 256-row
+// workgroup empty.
 hipError_t launch_fwd_bf16_d256(const FwdArgs& a, hipStream_t stream) {
   if (a.log2_page < 5) return launch_waves<true, 4>(a, stream);
+  if ((int64_t)a.n_q * a.group <= 128) return launch_waves<false, 4>(a, stream);
   return launch_waves<false, LS_FWD_WAVES>(a, stream);
 }
 

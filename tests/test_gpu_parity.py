@@ -150,6 +150,14 @@ def test_bf16_gqa_groups(G, Hkv):
     full_case(cfg)
 
 
+def test_bf16_few_rows_four_wave_path():
+    """At most 128 packed rows take the 4-wave forward on the page path (15
+    tokens x G = 8 = 120 rows: one ragged row tile), over several splits."""
+    cfg = BF16_SMALL.scaled(name="bf16_r15", prefix_len=6144, resp_len=15, plant_frac=0.0,
+                            n_shards=3, splits_per_shard=2)
+    full_case(cfg)
+
+
 def test_bf16_single_row_and_response_only():
     cfg = BF16_SMALL.scaled(name="bf16_r1", prefix_len=512, resp_len=1, plant_frac=0.0,
                             n_shards=1, splits_per_shard=1)
