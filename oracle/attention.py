@@ -54,12 +54,14 @@ def _kv(pool, page_table, page_size, positions, g, width=None):
 # --------------------------------------------------------------------------
 def attn_fwd(q, k_pool, v_pool, page_table, *, page_size, q_pos0, scale,
              kv_begin=0, kv_end=None, rows=None, heads=None, head_dim_v=None,
-             row_block=64):
+             row_block=64, key_positions=None):
     """Normalized output and log-normalizer of one KV range.
 
     Returns ``o [n_rows, n_heads, Dv]`` and ``lse [n_heads, n_rows]`` (natural
     log).  A row that sees no key of the range gets ``o = 0`` and
-    ``lse = -inf``.  ``rows``/``heads`` select a subset (default: all)."""
+    ``lse = -inf``.  ``rows``/``heads`` select a subset (default: all).
+    ``key_positions`` (sorted logical positions) replaces the range
+    ``[kv_begin, kv_end)``: the key set of a shard that owns scattered pages."""
     R, Hq, D = q.shape
     Hkv = k_pool.shape[2]
     G = Hq // Hkv
@@ -71,10 +73,13 @@ def attn_fwd(q, k_pool, v_pool, page_table, *, page_size, q_pos0, scale,
     o = np.zeros((rows.size, heads.size, Dv))
     lse = np.full((heads.size, rows.size), -np.inf)
     last_visible = int(q_pos0 + rows.max()) + 1 if rows.size else kv_begin
-    hi = min(kv_end, last_visible)
-    if hi <= kv_begin or rows.size == 0:
+    if key_positions is not None:
+        keys = np.asarray(key_positions, dtype=np.int64)
+        keys = keys[keys < last_visible] if rows.size else keys[:0]
+    else:
+        keys = np.arange(kv_begin, min(kv_end, last_visible))
+    if keys.size == 0 or rows.size == 0:
         return o, lse
-    keys = np.arange(kv_begin, hi)
     for g in sorted({int(h) // G for h in heads}):
         K = _kv(k_pool, page_table, page_size, keys, g)
         V = _kv(v_pool, page_table, page_size, keys, g, Dv)
@@ -99,6 +104,21 @@ def attn_fwd(q, k_pool, v_pool, page_table, *, page_size, q_pos0, scale,
     return o, lse
 
 
+def _merge_weights(lse_parts):
+    """Shared part of Eq. qwen-lse-parts / qwen-global-attn: the part weights
+    e^(l_r - m) with m = max_r l_r (0 for empty parts), a = sum of the weights
+    (1 where every part is empty) and l = m + log a (-inf there)."""
+    L = np.stack([np.asarray(x, dtype=np.float64) for x in lse_parts])      # [S, H, R]
+    m = L.max(axis=0)
+    alive = np.isfinite(m)
+    m_safe = np.where(alive, m, 0.0)
+    w = np.where(np.isfinite(L), np.exp(L - m_safe[None]), 0.0)             # [S, H, R]
+    a = w.sum(axis=0)
+    a_safe = np.where(alive, a, 1.0)
+    lse = np.where(alive, m_safe + np.log(a_safe), -np.inf)
+    return w, a_safe, lse
+
+
 def lse_merge(o_parts, lse_parts):
     """Compose range results (Eq. qwen-lse-parts, Eq. qwen-global-attn).
 
@@ -106,18 +126,51 @@ def lse_merge(o_parts, lse_parts):
     m = max_r l_r;  a = sum_r e^(l_r - m);  n = sum_r e^(l_r - m) o_r;
     o = n / a;  l = m + log a.  Ranges with l_r = -inf carry weight 0; a row whose
     every range is empty stays o = 0, l = -inf."""
-    L = np.stack([np.asarray(x, dtype=np.float64) for x in lse_parts])      # [S, H, R]
+    w, a_safe, lse = _merge_weights(lse_parts)
     O = np.stack([np.asarray(x, dtype=np.float64) for x in o_parts])        # [S, R, H, Dv]
-    m = L.max(axis=0)
-    alive = np.isfinite(m)
-    m_safe = np.where(alive, m, 0.0)
-    w = np.where(np.isfinite(L), np.exp(L - m_safe[None]), 0.0)             # [S, H, R]
-    a = w.sum(axis=0)
     n = np.einsum("shr,srhd->rhd", w, O)
-    a_safe = np.where(alive, a, 1.0)
     o = n / a_safe.T[:, :, None]
-    lse = np.where(alive, m_safe + np.log(a_safe), -np.inf)
     return o, lse
+
+
+def bf16_round(x):
+    """Nearest bfloat16 value (ties to even) of each float64 in ``x``, as float64.
+
+    bfloat16 keeps 8 significant bits and float32's exponent range.  Written
+    from that definition: x = m 2^e with 0.5 <= |m| < 1, and m 2^8 is rounded
+    to an integer, ties to even (normal range only, which is all this oracle
+    meets; zero stays zero)."""
+    x = np.asarray(x, dtype=np.float64)
+    m, e = np.frexp(x)
+    return np.ldexp(np.rint(np.ldexp(m, 8)), e - 8)
+
+
+def lse_merge_bf16_numerator(o_parts, lse_parts):
+    """Eq. qwen-lse-parts / qwen-global-attn with the numerator reduced in
+    bf16, the production composition described right after Eq.
+    qwen-global-attn: m, a and l are exact; each part's numerator term
+    e^(l_r - m) o_r is rounded to bf16, and the terms are summed in part order
+    with the running sum rounded to bf16 after every addition; o = n / a.
+    (The order and the rounding of each term are this oracle's reading of a
+    bf16 all-reduce.)"""
+    w, a_safe, lse = _merge_weights(lse_parts)
+    n = None
+    for r, o_r in enumerate(o_parts):
+        term = bf16_round(w[r].T[:, :, None] * np.asarray(o_r, dtype=np.float64))
+        n = term if n is None else bf16_round(n + term)
+    return n / a_safe.T[:, :, None], lse
+
+
+# --------------------------------------------------------------------------
+# block-cyclic page ownership (Sec. "From Logical Shards to Physical Pages")
+# --------------------------------------------------------------------------
+def cyclic_owned_positions(prefix_len, page_size, n_shards, shard):
+    """Logical prefix positions of shard ``shard`` when logical page p is owned
+    by shard p mod n_shards (Eq. qwen-page-owner), in increasing order."""
+    n_pages = -(-prefix_len // page_size)
+    pages = np.arange(shard, n_pages, n_shards, dtype=np.int64)
+    pos = (pages[:, None] * page_size + np.arange(page_size)[None, :]).reshape(-1)
+    return pos[pos < prefix_len]
 
 
 # --------------------------------------------------------------------------

@@ -338,7 +338,87 @@ def pin_sparse_subset(O):
     assert rel_l2(dq, num) < 1e-6, f"sparse dq vs finite differences {rel_l2(dq, num):.2e}"
 
 
+# ---------------------------------------------------------------- production composition
+def pin_bf16_round(O):
+    """bf16 rounding equals torch's float32 -> bfloat16 cast (round to nearest
+    even) on float32 values, and hand-checked ties: 1 + 2^-8 -> 1 (even),
+    1 + 3 * 2^-8 -> 1 + 2^-6 (even), -(1 + 2^-7 + 2^-9) -> -(1 + 2^-7)."""
+    import torch
+    rng = np.random.default_rng(21)
+    x = (rng.standard_normal(4096) * np.exp2(rng.integers(-30, 30, 4096))).astype(np.float32)
+    x[:8] = [1.0, 0.0, -2.5, 3.0e38, 1.17549435e-38, 65504.0, 1.0 / 3, -7.0]
+    want = torch.from_numpy(x).to(torch.bfloat16).to(torch.float64).numpy()
+    got = O.bf16_round(x.astype(np.float64))
+    assert np.array_equal(got, want), "bf16 rounding differs from torch's cast"
+    ties = np.array([1 + 2.0 ** -8, 1 + 3 * 2.0 ** -8, -(1 + 2.0 ** -7 + 2.0 ** -9)])
+    assert np.array_equal(O.bf16_round(ties), [1.0, 1 + 2.0 ** -6, -(1 + 2.0 ** -7)]), "bf16 ties"
+
+
+def pin_bf16_numerator_merge(O):
+    """The bf16-numerator composition: one part gives bf16(o); terms are
+    rounded and the sum is rounded after every addition, in part order
+    (1, 2^-8, 2^-8 sums to 1, but 2^-8, 2^-8, 1 to 1 + 2^-7); m, a and l stay
+    exact; with bf16-exact terms and sums it equals the exact merge."""
+    rng = np.random.default_rng(22)
+    o1 = rng.standard_normal((3, 2, 5))
+    l1 = rng.standard_normal((2, 3))
+    o, lse = O.lse_merge_bf16_numerator([o1], [l1])
+    assert np.array_equal(o, O.bf16_round(o1)), "one part: o = bf16(o)"
+    _close(lse, l1, 1e-15, "one part: lse")
+    ones = np.zeros((1, 1))
+    parts = [np.full((1, 1, 1), 1.0), np.full((1, 1, 1), 2.0 ** -8), np.full((1, 1, 1), 2.0 ** -8)]
+    o, lse = O.lse_merge_bf16_numerator(parts, [ones, ones, ones])
+    assert o[0, 0, 0] == 1.0 / 3, "running sum rounded after each addition"
+    _close(lse, np.log([[3.0]]), 1e-15, "lse with the exact denominator")
+    o, _ = O.lse_merge_bf16_numerator(parts[::-1], [ones, ones, ones])
+    assert o[0, 0, 0] == (1 + 2.0 ** -7) / 3, "parts summed in the given order"
+    # bf16-exact data: small integers with weights 1, 1/2 (l = 0, -ln 2)
+    oa = rng.integers(-8, 8, (4, 3, 6)).astype(np.float64)
+    ob = rng.integers(-8, 8, (4, 3, 6)).astype(np.float64) * 2.0
+    la, lb = np.zeros((3, 4)), np.full((3, 4), -np.log(2.0))
+    want_o, want_l = O.lse_merge([oa, ob], [la, lb])
+    got_o, got_l = O.lse_merge_bf16_numerator([oa, ob], [la, lb])
+    _close(got_o, want_o, 1e-15, "bf16-exact merge o")
+    _close(got_l, want_l, 1e-15, "bf16-exact merge lse")
+    # random data: within the rounding bound of S terms and S - 1 additions
+    parts = [rng.standard_normal((6, 2, 8)) for _ in range(5)]
+    lses = [rng.standard_normal((2, 6)) for _ in range(5)]
+    eo, _ = O.lse_merge(parts, lses)
+    go, _ = O.lse_merge_bf16_numerator(parts, lses)
+    bound = 10 * 2.0 ** -9 * np.max(np.abs(np.stack(parts)))
+    assert np.max(np.abs(go - eo)) <= bound, "bf16 numerator error bound"
+    assert np.max(np.abs(go - eo)) > 0, "bf16 numerator must round"
+
+
+def pin_cyclic_ownership(O):
+    """owner(p) = p mod C (Eq. qwen-page-owner): the shards' positions
+    partition the prefix, shard c holds exactly the pages congruent to c, and
+    composing the shards' results with the response range equals the unsplit
+    forward."""
+    t = make(P=75, R=6, Hq=4, Hkv=2, D=8, S=8, seed=23)
+    C = 3
+    owned = [O.cyclic_owned_positions(t.P, t.S, C, c) for c in range(C)]
+    allp = np.sort(np.concatenate(owned))
+    assert np.array_equal(allp, np.arange(t.P)), "shards partition the prefix"
+    for c in range(C):
+        assert np.all((owned[c] // t.S) % C == c), "shard c owns pages p with p mod C = c"
+        assert np.all(np.diff(owned[c]) > 0), "positions in increasing order"
+    full_o, full_l = O.attn_fwd(t.q, t.k_pool, t.v_pool, t.page_table, **t.kw())
+    parts = [O.attn_fwd(t.q, t.k_pool, t.v_pool, t.page_table, key_positions=owned[c], **t.kw())
+             for c in range(C)]
+    parts.append(O.attn_fwd(t.q, t.k_pool, t.v_pool, t.page_table, kv_begin=t.P,
+                            kv_end=t.kv_len, **t.kw()))
+    o, lse = O.lse_merge([p[0] for p in parts], [p[1] for p in parts])
+    _close(o, full_o, 1e-12, "cyclic shards o")
+    _close(lse, full_l, 1e-12, "cyclic shards lse")
+    # a key set given as positions equals the same contiguous range
+    a = O.attn_fwd(t.q, t.k_pool, t.v_pool, t.page_table, kv_begin=10, kv_end=50, **t.kw())
+    b = O.attn_fwd(t.q, t.k_pool, t.v_pool, t.page_table, key_positions=np.arange(10, 50), **t.kw())
+    assert np.array_equal(a[0], b[0]) and np.array_equal(a[1], b[1]), "positions == range"
+
+
 ALL_PINS = [pin_single_key, pin_identical_keys, pin_zero_query, pin_scale_and_gqa,
             pin_merge_closed_form, pin_split_merge_invariance, pin_causal, pin_gather_bruteforce,
             pin_finite_differences, pin_bwd_partition, pin_torch_autograd, pin_sampled_rows,
-            pin_sparse_full_index_is_dense, pin_sparse_subset]
+            pin_sparse_full_index_is_dense, pin_sparse_subset, pin_bf16_round,
+            pin_bf16_numerator_merge, pin_cyclic_ownership]

@@ -39,6 +39,20 @@ MUTATIONS = [
     ("sparse_values_tail", "o[k_] = (w / z[:, None]) @ C[:, :head_dim_v]",
      "o[k_] = (w / z[:, None]) @ C[:, -head_dim_v:]"),
     ("sparse_dq_no_delta", "dS = P * (dP - delta[:, None])\n        dq[k_]", "dS = P * dP\n        dq[k_]"),
+    ("bf16_truncate", "return np.ldexp(np.rint(np.ldexp(m, 8)), e - 8)",
+     "return np.ldexp(np.trunc(np.ldexp(m, 8)), e - 8)"),
+    ("bf16_fp16_width", "return np.ldexp(np.rint(np.ldexp(m, 8)), e - 8)",
+     "return np.ldexp(np.rint(np.ldexp(m, 11)), e - 11)"),
+    ("bf16_num_terms_unrounded", "term = bf16_round(w[r].T[:, :, None] * np.asarray(o_r, dtype=np.float64))",
+     "term = w[r].T[:, :, None] * np.asarray(o_r, dtype=np.float64)"),
+    ("bf16_num_final_round_only", "n = term if n is None else bf16_round(n + term)",
+     "n = term if n is None else n + term"),
+    ("bf16_num_unweighted", "term = bf16_round(w[r].T[:, :, None] * np.asarray(o_r, dtype=np.float64))",
+     "term = bf16_round(np.asarray(o_r, dtype=np.float64))"),
+    ("cyclic_block_contiguous", "pages = np.arange(shard, n_pages, n_shards, dtype=np.int64)",
+     "pages = np.arange(shard * (n_pages // n_shards), (shard + 1) * (n_pages // n_shards), dtype=np.int64)"),
+    ("key_positions_ignored", "keys = np.asarray(key_positions, dtype=np.int64)",
+     "keys = np.arange(kv_begin, min(kv_end, last_visible))"),
 ]
 
 
