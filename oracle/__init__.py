@@ -3,5 +3,6 @@
 Imported by the tests, the smoke check and the benchmark's CPU-baseline leg;
 never by the library or its binding.
 """
-from .attention import (attn_bwd, attn_fwd, decode, gather, lse_merge,  # noqa: F401
-                        sparse_bwd, sparse_fwd)
+from .attention import (attn_bwd, attn_fwd, bf16_round, cyclic_owned_positions,  # noqa: F401
+                        decode, dsa_index_scores, gather, lse_merge, lse_merge_bf16_numerator,
+                        sparse_bwd, sparse_fwd, topk_select)

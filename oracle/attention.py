@@ -305,3 +305,43 @@ def sparse_bwd(q, latent_pool, page_table, idx, d_out, *, page_size, prefix_len,
         dS = P * (dP - delta[:, None])
         dq[k_] = scale * (dS @ C)
     return dq
+
+
+# --------------------------------------------------------------------------
+# DSA index selection (Eq. dsa-index, Eq. glm-global-dsa)
+# --------------------------------------------------------------------------
+def dsa_index_scores(q_index, w_index, k_index_pool, page_table, *, page_size, pos_begin,
+                     pos_end, rows=None):
+    """Index scores of Eq. dsa-index: I[t, s] = sum_j w[t, j] ReLU(<q[t, j], k_s>)
+    for rows t and prefix positions s in [pos_begin, pos_end).
+
+    ``q_index`` [R, H_I, d] and ``k_index_pool`` [n_phys, S, d] (bf16 bit
+    patterns or floats; one index key per position, shared by the heads),
+    ``w_index`` [R, H_I].  Returns ``[n_rows, pos_end - pos_begin]`` float64."""
+    R = q_index.shape[0]
+    rows = np.arange(R) if rows is None else np.asarray(rows)
+    K = decode(gather(k_index_pool, page_table, page_size, np.arange(pos_begin, pos_end)))
+    out = np.zeros((rows.size, pos_end - pos_begin))
+    for k_, t in enumerate(rows):
+        Q = decode(q_index[t])                              # [H_I, d]
+        W = np.asarray(w_index[t], dtype=np.float64)        # [H_I]
+        out[k_] = W @ np.maximum(Q @ K.T, 0.0)
+    return out
+
+
+def topk_select(scores, k, positions=None):
+    """TopK of Eq. dsa-attention / glm-global-dsa for each row of ``scores``
+    [rows, n]: the k largest scores, equal scores ordered by lower position
+    first (the deterministic rule of a candidate merge), returned as positions
+    in ascending order ([rows, min(k, n)] int64).  ``positions`` [n] or
+    [rows, n] names each column's position (default 0 .. n - 1)."""
+    scores = np.asarray(scores, dtype=np.float64)
+    rows, n = scores.shape
+    pos = np.broadcast_to(np.arange(n) if positions is None else np.asarray(positions),
+                          (rows, n))
+    take = min(k, n)
+    out = np.empty((rows, take), dtype=np.int64)
+    for r in range(rows):
+        order = np.lexsort((pos[r], -scores[r]))            # by score desc, then position asc
+        out[r] = np.sort(pos[r][order[:take]])
+    return out

@@ -417,8 +417,73 @@ def pin_cyclic_ownership(O):
     assert np.array_equal(a[0], b[0]) and np.array_equal(a[1], b[1]), "positions == range"
 
 
+# ---------------------------------------------------------------- DSA index selection
+def pin_dsa_index_closed_form(O):
+    """Eq. dsa-index on hand-made keys: one head with weight 1 gives ReLU(q.k)
+    (negative dot products give 0); weights scale each head's term linearly and
+    may be negative; the page layout does not matter."""
+    S, d = 4, 3
+    k_dense = np.array([[1.0, 0, 0], [0, 1.0, 0], [-1.0, 0, 0], [0, 0, 2.0],
+                        [1.0, 1.0, 1.0], [0, -2.0, 0], [0.5, 0, 0], [0, 0, -1.0]])
+    pool = k_dense.reshape(2, S, d)
+    ident = np.arange(2, dtype=np.int32)
+    q = np.array([[[2.0, 3.0, -1.0], [1.0, -1.0, 1.0]]])              # [R=1, H=2, d]
+    w1 = np.array([[1.0, 0.0]])
+    got = O.dsa_index_scores(q, w1, pool, ident, page_size=S, pos_begin=0, pos_end=8)
+    want = np.maximum(k_dense @ q[0, 0], 0.0)[None]
+    _close(got, want, 1e-15, "one head, weight 1")
+    assert got[0, 2] == 0.0 and got[0, 5] == 0.0, "negative dot products give 0"
+    w2 = np.array([[2.0, -0.5]])
+    got = O.dsa_index_scores(q, w2, pool, ident, page_size=S, pos_begin=2, pos_end=7)
+    want = (2.0 * np.maximum(k_dense @ q[0, 0], 0) - 0.5 * np.maximum(k_dense @ q[0, 1], 0))[2:7]
+    _close(got[0], want, 1e-15, "weighted heads over a sub-range")
+    perm_pool = pool[::-1].copy()
+    perm = np.array([1, 0], dtype=np.int32)
+    got2 = O.dsa_index_scores(q, w2, perm_pool, perm, page_size=S, pos_begin=2, pos_end=7)
+    assert np.array_equal(got, got2), "layout invariance"
+
+
+def pin_topk_ties_and_order(O):
+    """TopK equals a brute-force sort on (score descending, position
+    ascending); equal scores go to the lower position; the result is in
+    ascending position order; k >= n returns every position."""
+    sc = np.array([[3.0, 1.0, 3.0, 2.0, 3.0, 0.5, 2.0]])
+    assert O.topk_select(sc, 2).tolist() == [[0, 2]], "ties: lowest positions"
+    assert O.topk_select(sc, 4).tolist() == [[0, 2, 3, 4]], "then the next score, lowest first"
+    assert O.topk_select(sc, 10).tolist() == [list(range(7))], "k >= n: all"
+    pos = np.array([40, 10, 30, 20, 50, 60, 70])
+    assert O.topk_select(sc, 2, positions=pos).tolist() == [[30, 40]], "named positions"
+    rng = np.random.default_rng(31)
+    sc = rng.integers(-5, 6, (5, 300)).astype(np.float64)            # many ties
+    for r in range(5):
+        want = sorted(sorted(range(300), key=lambda j: (-sc[r, j], j))[:37])
+        assert O.topk_select(sc[r:r + 1], 37)[0].tolist() == want, "brute force"
+
+
+def pin_topk_local_candidates_merge(O):
+    """Eq. glm-global-dsa: the top-k of the union of every shard's local top-k
+    candidates (with their global positions) equals the global top-k; a
+    shard's local selection alone (Eq. glm-local-dsa) generally does not."""
+    rng = np.random.default_rng(32)
+    sc = rng.integers(-20, 20, (4, 1000)).astype(np.float64)
+    k = 50
+    glob = O.topk_select(sc, k)
+    bounds = [0, 137, 400, 401, 800, 1000]
+    cand_pos, cand_sc = [], []
+    for b, e in zip(bounds[:-1], bounds[1:]):
+        loc = O.topk_select(sc[:, b:e], k) + b
+        cand_pos.append(loc)
+        cand_sc.append(np.take_along_axis(sc, loc, axis=1))
+    cp, cs = np.concatenate(cand_pos, axis=1), np.concatenate(cand_sc, axis=1)
+    merged = np.stack([O.topk_select(cs[r:r + 1], k, positions=cp[r])[0] for r in range(4)])
+    assert np.array_equal(merged, glob), "candidate merge == global top-k"
+    local0 = O.topk_select(sc[:, 0:137], k)
+    assert not np.array_equal(local0, glob), "a local selection is not the global one"
+
+
 ALL_PINS = [pin_single_key, pin_identical_keys, pin_zero_query, pin_scale_and_gqa,
             pin_merge_closed_form, pin_split_merge_invariance, pin_causal, pin_gather_bruteforce,
             pin_finite_differences, pin_bwd_partition, pin_torch_autograd, pin_sampled_rows,
             pin_sparse_full_index_is_dense, pin_sparse_subset, pin_bf16_round,
-            pin_bf16_numerator_merge, pin_cyclic_ownership]
+            pin_bf16_numerator_merge, pin_cyclic_ownership, pin_dsa_index_closed_form,
+            pin_topk_ties_and_order, pin_topk_local_candidates_merge]

@@ -51,6 +51,12 @@ MUTATIONS = [
      "term = bf16_round(np.asarray(o_r, dtype=np.float64))"),
     ("cyclic_block_contiguous", "pages = np.arange(shard, n_pages, n_shards, dtype=np.int64)",
      "pages = np.arange(shard * (n_pages // n_shards), (shard + 1) * (n_pages // n_shards), dtype=np.int64)"),
+    ("dsa_no_relu", "out[k_] = W @ np.maximum(Q @ K.T, 0.0)", "out[k_] = W @ (Q @ K.T)"),
+    ("dsa_unweighted", "out[k_] = W @ np.maximum(Q @ K.T, 0.0)", "out[k_] = np.maximum(Q @ K.T, 0.0).sum(axis=0)"),
+    ("dsa_abs_not_relu", "out[k_] = W @ np.maximum(Q @ K.T, 0.0)", "out[k_] = W @ np.abs(Q @ K.T)"),
+    ("topk_ties_high_pos", "order = np.lexsort((pos[r], -scores[r]))", "order = np.lexsort((-pos[r], -scores[r]))"),
+    ("topk_smallest", "order = np.lexsort((pos[r], -scores[r]))", "order = np.lexsort((pos[r], scores[r]))"),
+    ("topk_unsorted_out", "out[r] = np.sort(pos[r][order[:take]])", "out[r] = pos[r][order[:take]]"),
     ("key_positions_ignored", "keys = np.asarray(key_positions, dtype=np.int64)",
      "keys = np.arange(kv_begin, min(kv_end, last_visible))"),
 ]
