@@ -12,7 +12,11 @@ FLOP convention: fwd = 4*Hq*D*sum_i |V_i|; bwd = Hq*D*(6*sum_i |V_i & prefix| +
 "useful" rate drops the backward's Q K^T recompute (4 and 8 instead of 6 and 10).
 Besides the step it reports HBM-bound page streaming (the split forward over
 the whole prefix with 16 query rows), ceilings measured on the same GPU (bf16
-GEMM, 4 GiB copy) and the clocks.
+GEMM, 4 GiB copy), the clocks, and the cost of the production composition
+(the cross-shard merge with its numerator reduced in bf16: time and distance
+from the fp32 composition on the same shard results).  ``--ownership cyclic``
+deals prefix pages to the shards block-cyclically (page p to shard p mod 8)
+and ``--bf16-numerator`` makes the step's cross-shard merge the bf16 one.
 """
 from __future__ import annotations
 
@@ -106,6 +110,29 @@ def gpu_clocks():
         return {k: v for k, v in card.items() if "sclk" in k.lower() or "mclk" in k.lower()}
     except Exception:  # pragma: no cover - tool missing or output changed
         return None
+
+
+def bf16_numerator_cost(step, stream, reps=20):
+    """The cross-shard merge of the step's shard results with the numerator
+    reduced in bf16 and in fp32 (both to fp32 outputs): times and differences."""
+    import torch
+    from paper_2607_14952_amd import binding as B
+    R, Hq, Dv = step.out.shape
+    o32 = torch.empty((R, Hq, Dv), dtype=torch.float32, device=step.out.device)
+    o16 = torch.empty_like(o32)
+    l32, l16 = torch.empty_like(step.lse), torch.empty_like(step.lse)
+    f32 = lambda: B.lse_merge(step.shard_out, step.shard_lse, out=o32, lse=l32,  # noqa: E731
+                              stream=stream)
+    b16 = lambda: B.lse_merge(step.shard_out, step.shard_lse, out=o16, lse=l16,  # noqa: E731
+                              flags=B.FLAG_BF16_NUMERATOR, stream=stream)
+    t32, t16 = time_ms(f32, reps, stream), time_ms(b16, reps, stream)
+    torch.cuda.synchronize()
+    d = (o16 - o32).abs()
+    return {"parts": int(step.shard_out.shape[0]), "merge_ms_fp32": round(t32, 4),
+            "merge_ms_bf16": round(t16, 4), "max_abs_diff": float(d.max()),
+            "max_abs_out": float(o32.abs().max()),
+            "rel_l2_diff": float(torch.linalg.norm(o16 - o32) / torch.linalg.norm(o32)),
+            "lse_identical": bool(torch.equal(l16, l32))}
 
 
 def page_streaming(cfg, dev, rows=16, n_splits=128):
@@ -269,6 +296,61 @@ def run_sparse(cfg, args):
         flush=True)
 
 
+def run_capture(cfg, args):
+    """Chunked no-grad capture of one attention layer's prompt into the paged
+    store: every chunk's K/V scatter, split forward and merge, timed over the
+    whole prompt with its rows resident in HBM."""
+    import torch
+    from paper_2607_14952_amd import inputs
+    from paper_2607_14952_amd.capture import PrefixCapture
+    from paper_2607_14952_amd.replay import to_device
+    log(f"generating inputs for {cfg.name}")
+    t = time.perf_counter()
+    h = inputs.capture_inputs(cfg)
+    log(f"inputs ready in {time.perf_counter() - t:.1f} s; copying to HBM")
+    dev = {k: to_device(v) for k, v in h.items()}
+    del h
+    stream = torch.cuda.current_stream()
+    cap = PrefixCapture(cfg, dev, stream=stream)
+    for c in range(min(args.warmup, cfg.n_chunks)):   # warm the kernels on the first chunks
+        cap.chunk(c)
+    torch.cuda.synchronize()
+    E = lambda: torch.cuda.Event(enable_timing=True)  # noqa: E731
+    probes = sorted({0, cfg.n_chunks // 4, cfg.n_chunks // 2, cfg.n_chunks - 1})
+    pev = {c: (E(), E()) for c in probes}
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for c in range(cfg.n_chunks):
+        if c in pev:
+            pev[c][0].record(stream)
+        cap.chunk(c)
+        if c in pev:
+            pev[c][1].record(stream)
+        if c % 64 == 63:
+            log(f"captured {c + 1}/{cfg.n_chunks} chunks")
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    fl = 4 * cfg.n_q_heads * cfg.head_dim * cfg.visible()
+    chunk_ms = {str(c): round(pev[c][0].elapsed_time(pev[c][1]), 3) for c in probes}
+    result = {
+        "metric": "prefix capture, one attention layer (s)",
+        "value": round(wall, 3), "unit": "s", "n_gpus": 1, "steps": 1, "warmup": args.warmup,
+        "ms_per_step": round(wall * 1e3, 1), "higher_is_better": False, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": f"{cfg.name}: {cfg.length} prompt positions in "
+                               f"{cfg.n_chunks} chunks of {cfg.chunk}, bf16 GQA "
+                               f"{cfg.n_q_heads}q/{cfg.n_kv_heads}kv, head_dim {cfg.head_dim}, "
+                               f"{cfg.page_size}-position pages; per chunk: K/V scatter into "
+                               f"its pages, split forward over earlier + own keys, merge",
+                   "length": cfg.length, "chunk": cfg.chunk, "page_size": cfg.page_size},
+        "tflops": round(fl / wall / 1e12, 2),
+        "flop": fl,
+        "chunk_ms": chunk_ms,
+        "gpu": torch.cuda.get_device_name(0),
+    }
+    print(json.dumps(result), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -279,6 +361,10 @@ def main():
     ap.add_argument("--cpu-rows", type=int, default=96)
     ap.add_argument("--calib-copy", action="store_true",
                     help="run a 1 GiB device copy first (reference for rocprofv3 byte counters)")
+    ap.add_argument("--ownership", choices=("contiguous", "cyclic"), default="contiguous",
+                    help="prefix pages to shards: contiguous ranges or page p to shard p mod 8")
+    ap.add_argument("--bf16-numerator", action="store_true",
+                    help="the step's cross-shard merge reduces the numerator in bf16")
     ap.add_argument("--skip-extras", action="store_true",
                     help="skip page streaming, measured ceilings and clocks (profiling runs: the "
                          "streaming pass reuses the forward kernel)")
@@ -297,6 +383,11 @@ def main():
         print("no GPU visible", file=sys.stderr)
         sys.exit(1)
     cfg = configs.get(args.config)
+    if isinstance(cfg, configs.CaptureConfig):
+        run_capture(cfg, args)
+        return
+    if args.ownership != "contiguous" or args.bf16_numerator:
+        cfg = cfg.scaled(ownership=args.ownership, bf16_numerator=args.bf16_numerator)
     if cfg.members > 1:
         run_blockwise(cfg, args)
         return
@@ -359,7 +450,8 @@ def main():
     dq_tf = dq_launch_fl / (dq_launch_ms * 1e-3) / 1e12
     fwd_total, dq_total = fwd_avg, dq_launch_ms * len(pre_ranges)
     if fwd_total >= dq_total:
-        roof = {"kernel": "fwd_bf16_d256_kernel (all 33 splits, one launch)",
+        roof = {"kernel": "fwd_bf16_d256_kernel (all splits: one launch, one per shard "
+                          "when cyclic)",
                 "achieved": fwd_tf, "flop_per_launch": fwd_fl, "avg_launch_ms": fwd_avg}
     else:
         roof = {"kernel": "bwd_dq_bf16_d256_kernel (one 262,144-key shard per launch)",
@@ -394,8 +486,11 @@ def main():
         "config": {"workload": f"{cfg.name}: bf16 GQA {cfg.n_q_heads}q/{cfg.n_kv_heads}kv, "
                                f"head_dim {cfg.head_dim}, prefix {cfg.prefix_len} in "
                                f"{cfg.page_size}-position pages (seeded permutation), "
-                               f"{cfg.n_shards} shards x {cfg.splits_per_shard} splits + "
-                               f"response split, response {cfg.resp_len} causal, fwd+bwd",
+                               f"{cfg.n_shards} {cfg.ownership} shards x "
+                               f"{cfg.splits_per_shard} splits + response split, response "
+                               f"{cfg.resp_len} causal, fwd+bwd"
+                               + (", bf16-numerator merge" if cfg.bf16_numerator else ""),
+                   "ownership": cfg.ownership, "bf16_numerator": cfg.bf16_numerator,
                    "prefix_len": cfg.prefix_len, "resp_len": cfg.resp_len,
                    "n_q_heads": cfg.n_q_heads, "n_kv_heads": cfg.n_kv_heads,
                    "head_dim": cfg.head_dim, "page_size": cfg.page_size,
@@ -413,6 +508,8 @@ def main():
     }
     result["useful_tflops"] = round(useful_flops(cfg) / (ms_per_step * 1e-3) / 1e12, 2)
     if not args.skip_extras:
+        log("bf16-numerator merge cost")
+        result["bf16_numerator"] = bf16_numerator_cost(step, stream)
         log("page streaming, clocks")
         result["page_streaming"] = page_streaming(cfg, dev)
         result["gpu_clocks"] = gpu_clocks()

@@ -77,7 +77,8 @@ typedef enum { LS_BF16 = 0, LS_F32 = 1 } ls_dtype;
 enum {
   LS_FLAG_CHECKED = 1u,        /* validate the page table (synchronous D2H copy) */
   LS_FLAG_ACCUMULATE_DQ = 4u,  /* backward: dq += contribution instead of dq = */
-  LS_FLAG_ACCUMULATE_DKV = 8u  /* backward: dk/dv_resp += instead of = */
+  LS_FLAG_ACCUMULATE_DKV = 8u, /* backward: dk/dv_resp += instead of = */
+  LS_FLAG_BF16_NUMERATOR = 16u /* merge: reduce the numerator in bf16 (see ls_lse_merge) */
 };
 
 /* One replay call: a block of n_q response rows against one paged KV store. */
@@ -161,8 +162,11 @@ ls_status ls_prefix_attn_fwd(const ls_attn_params* p, const ls_split* splits, in
  * Parts with l_r = -inf carry weight 0; a row whose every part is empty gets
  * o = 0 and l = -inf.  out_dtype is LS_BF16 or LS_F32 (an fp32 result can be
  * merged again: the merge is associative).  out_part/lse_part as produced by
- * ls_prefix_attn_fwd with n_q_heads = n_heads and head_dim_v = dv.  flags must
- * be 0.
+ * ls_prefix_attn_fwd with n_q_heads = n_heads and head_dim_v = dv.  flags is 0
+ * or LS_FLAG_BF16_NUMERATOR: the production composition noted after Eq.
+ * qwen-global-attn, where n is reduced in bf16 (each term e^(l_r - m) o_r is
+ * rounded to bf16 and the terms are added in part order, the running sum
+ * rounded to bf16 after every addition) while m, a and l stay fp32.
  */
 ls_status ls_lse_merge(const float* out_part, const float* lse_part, int32_t n_splits,
                        int32_t n_q, int32_t n_heads, int32_t dv, int32_t out_dtype,

@@ -18,6 +18,7 @@ LS_BF16, LS_F32 = 0, 1
 FLAG_CHECKED = 1
 FLAG_ACCUMULATE_DQ = 4
 FLAG_ACCUMULATE_DKV = 8
+FLAG_BF16_NUMERATOR = 16
 STATUS = {0: "LS_OK", -1: "LS_ERR_INVALID_ARG", -2: "LS_ERR_UNSUPPORTED", -3: "LS_ERR_WORKSPACE",
           -4: "LS_ERR_ALIAS", -5: "LS_ERR_STALE", -6: "LS_ERR_PAGE_OOB", -7: "LS_ERR_HIP"}
 EXPORTS = ["ls_abi_version", "ls_status_string", "ls_last_error", "ls_gather_kv", "ls_scatter_kv",

@@ -40,6 +40,8 @@ class ReplayConfig:
     topk: int = 0
     members: int = 1           # responses replayed against one prefix pool
     block: int = 0             # rows per replay call in blockwise replay (0 = whole response)
+    ownership: str = "contiguous"  # "contiguous" ranges or "cyclic": page p to shard p mod n_shards
+    bf16_numerator: bool = False   # cross-shard merge reduces the numerator in bf16
 
     # -- derived sizes ---------------------------------------------------
     @property
@@ -102,6 +104,27 @@ class ReplayConfig:
         out.append((self.prefix_len, self.kv_len))
         return out
 
+    def shard_pages(self, shard: int):
+        """Logical prefix pages of ``shard`` under cyclic ownership (Eq.
+        qwen-page-owner: owner(p) = p mod n_shards), in increasing order."""
+        return list(range(shard, self.n_prefix_pages, self.n_shards))
+
+    def shard_len(self, shard: int) -> int:
+        """Prefix positions owned by ``shard`` under cyclic ownership."""
+        pages = self.shard_pages(shard)
+        if not pages:
+            return 0
+        last = min(self.page_size, self.prefix_len - pages[-1] * self.page_size)
+        return (len(pages) - 1) * self.page_size + last
+
+    def virtual_splits(self, shard: int):
+        """Cyclic ownership: the shard's ``splits_per_shard`` ranges over its
+        owned positions renumbered 0 .. shard_len - 1 (page i of the shard's
+        table is its i-th owned page)."""
+        n = self.shard_len(shard)
+        step = -(-n // self.splits_per_shard) if n else 1
+        return [(b, min(n, b + step)) for b in range(0, n, step)]
+
     def shard_ranges(self):
         shard = self.prefix_len // self.n_shards
         out = [(s * shard, self.prefix_len if s == self.n_shards - 1 else (s + 1) * shard)
@@ -140,9 +163,87 @@ C5 = ReplayConfig(name="c5_sparse_mla_2m", seed=5, dtype="bf16", n_q_heads=128, 
                   head_dim=576, head_dim_v=512, page_size=64, prefix_len=2_097_152,
                   resp_len=2048, table="perm", sparse=True, topk=2048)
 
+
+
+@dataclasses.dataclass(frozen=True)
+class CaptureConfig:
+    """No-grad chunked capture of a prompt into a paged store, one attention
+    layer (Phase 1 of the replay transaction; the shared prompt is captured in
+    4,096-token chunks, Sec. "Four-Block Response Replay").  Chunk c's queries
+    attend to every earlier position and causally within the chunk; its K/V
+    rows are copied into pages of their own (right-sized pages, Sec. "From
+    Logical Shards to Physical Pages")."""
+    name: str
+    seed: int
+    n_q_heads: int
+    n_kv_heads: int
+    head_dim: int
+    page_size: int
+    length: int                    # prompt positions captured
+    chunk: int                     # positions per capture chunk
+    keys_per_split: int = 262_144  # earlier-chunk keys per split of a chunk's forward
+    q_blocks: int = 0              # distinct query blocks; chunk c uses block c mod q_blocks (0: own)
+    pool_slack: float = 1.0
+    table: str = "perm"
+    dtype: str = "bf16"
+
+    @property
+    def head_dim_v(self) -> int:
+        return self.head_dim
+
+    @property
+    def group(self) -> int:
+        return self.n_q_heads // self.n_kv_heads
+
+    @property
+    def n_chunks(self) -> int:
+        return -(-self.length // self.chunk)
+
+    @property
+    def n_logical_pages(self) -> int:
+        return -(-self.length // self.page_size)
+
+    @property
+    def n_phys_pages(self) -> int:
+        return max(self.n_logical_pages, math.ceil(self.n_logical_pages * self.pool_slack - 1e-9))
+
+    @property
+    def n_q_blocks(self) -> int:
+        return self.q_blocks or self.n_chunks
+
+    @property
+    def scale(self) -> float:
+        return 1.0 / math.sqrt(self.head_dim)
+
+    def chunk_range(self, c: int):
+        return c * self.chunk, min(self.length, (c + 1) * self.chunk)
+
+    def chunk_splits(self, c: int):
+        """Key ranges of chunk c's forward: the earlier positions in pieces of
+        at most keys_per_split, then the chunk's own positions (causal)."""
+        b, e = self.chunk_range(c)
+        n = -(-b // self.keys_per_split) if b else 0
+        step = -(-b // n) if n else 0
+        out = [(s, min(b, s + step)) for s in range(0, b, step)] if n else []
+        out.append((b, e))
+        return out
+
+    def visible(self) -> int:
+        """Sum over captured rows of the keys each sees (positions 0 .. t)."""
+        return self.length * (self.length + 1) // 2
+
+
+# One attention layer's capture of a 2,097,152-position prompt in 512 chunks of
+# 4,096 (the c3 layer shape); eight query blocks are cycled (query values do
+# not change the work).
+CAPTURE_2M = CaptureConfig(name="capture_2m", seed=6, n_q_heads=16, n_kv_heads=2, head_dim=256,
+                           page_size=256, length=2_097_152, chunk=4096, q_blocks=8)
+
 CONFIGS = {c.name: c for c in (C1, C2, C3, C4, C5)}
 BY_SHORT = {"c1": C1, "c2": C2, "c3": C3, "c4": C4, "c5": C5}
 
 
-def get(name: str) -> ReplayConfig:
+def get(name: str):
+    if name in ("capture", CAPTURE_2M.name):
+        return CAPTURE_2M
     return BY_SHORT.get(name) or CONFIGS[name]

@@ -318,7 +318,7 @@ LS_API ls_status ls_lse_merge(const float* out_part, const float* lse_part, int3
                 n_splits, n_q, n_heads, dv);
   if (out_dtype != LS_BF16 && out_dtype != LS_F32)
     return fail(LS_ERR_UNSUPPORTED, "out_dtype %d", out_dtype);
-  if (flags != 0) return fail(LS_ERR_UNSUPPORTED, "merge flags 0x%x", flags);
+  if (flags & ~LS_FLAG_BF16_NUMERATOR) return fail(LS_ERR_UNSUPPORTED, "merge flags 0x%x", flags);
   if (dv % 4 != 0) return fail(LS_ERR_UNSUPPORTED, "merge needs dv %% 4 == 0 (got %d)", dv);
   if (n_q == 0) return LS_OK;
   if (!out_part || !lse_part || !out || !lse)
@@ -333,7 +333,8 @@ LS_API ls_status ls_lse_merge(const float* out_part, const float* lse_part, int3
   ls_status st = check_alias(outs, ins);
   if (st != LS_OK) return st;
   hipError_t e = ls::launch_merge(out_part, lse_part, n_splits, n_q, n_heads, dv,
-                                  out_dtype == LS_BF16, out, lse, (hipStream_t)stream);
+                                  out_dtype == LS_BF16, (flags & LS_FLAG_BF16_NUMERATOR) != 0,
+                                  out, lse, (hipStream_t)stream);
   return e == hipSuccess ? LS_OK : hip_fail(e, "merge launch");
 }
 

@@ -96,8 +96,8 @@ hipError_t launch_scatter(void* k_pool, void* v_pool, const int32_t* page_table,
                           int64_t v_row_elems, int esize, const void* k_src, const void* v_src,
                           hipStream_t stream);
 hipError_t launch_merge(const float* out_part, const float* lse_part, int n_splits, int n_q,
-                        int n_heads, int dv, bool out_bf16, void* out, float* lse,
-                        hipStream_t stream);
+                        int n_heads, int dv, bool out_bf16, bool bf16_numerator, void* out,
+                        float* lse, hipStream_t stream);
 hipError_t launch_fwd_f32(const FwdArgs& a, hipStream_t stream);
 hipError_t launch_fwd_bf16_d256(const FwdArgs& a, hipStream_t stream);
 hipError_t launch_bwd_prep(const void* d_out, const void* out, bool dout_bf16, bool out_bf16,

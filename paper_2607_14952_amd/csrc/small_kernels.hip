@@ -69,7 +69,13 @@ __global__ __launch_bounds__(256) void scatter_kernel(char* __restrict__ k_pool,
 // One thread per 4 output values of one (row, head).  Eq. qwen-lse-parts:
 // m = max l_r, a = sum e^(l_r - m), n = sum e^(l_r - m) o_r; o = n / a,
 // l = m + log a (computed with exp2/log2 and converted to natural log).
-template <bool OUT_BF16>
+// BF16_NUM: the production composition described after Eq. qwen-global-attn,
+// n reduced in bf16: each term e^(l_r - m) o_r is rounded to bf16 and added
+// in part order with the running sum rounded to bf16 after every addition
+// (m, a and l stay fp32).
+__device__ __forceinline__ float round_bf16(float x) { return (float)(__bf16)x; }
+
+template <bool OUT_BF16, bool BF16_NUM>
 __global__ __launch_bounds__(256) void merge_kernel(const float* __restrict__ out_part,
                                                     const float* __restrict__ lse_part,
                                                     int n_splits, int n_q, int n_heads, int dv4,
@@ -96,7 +102,12 @@ __global__ __launch_bounds__(256) void merge_kernel(const float* __restrict__ ou
       const float w = __builtin_amdgcn_exp2f(fmaf(l, kLog2e, -m2));   // 0 for l = -inf
       a += w;
       const f32x4 o = src[s * (part_out / 4)];
-      acc += w * o;
+      if (BF16_NUM) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) acc[e] = round_bf16(acc[e] + round_bf16(w * o[e]));
+      } else {
+        acc += w * o;
+      }
     }
     acc *= 1.0f / a;
   }
@@ -167,17 +178,19 @@ hipError_t launch_scatter(void* k_pool, void* v_pool, const int32_t* page_table,
 }
 
 hipError_t launch_merge(const float* out_part, const float* lse_part, int n_splits, int n_q,
-                        int n_heads, int dv, bool out_bf16, void* out, float* lse,
-                        hipStream_t stream) {
+                        int n_heads, int dv, bool out_bf16, bool bf16_numerator, void* out,
+                        float* lse, hipStream_t stream) {
   const int dv4 = dv / 4;
   const int64_t threads = (int64_t)n_q * n_heads * dv4;
   const unsigned blocks = (unsigned)((threads + 255) / 256);
-  if (out_bf16)
-    hipLaunchKernelGGL(merge_kernel<true>, dim3(blocks), dim3(256), 0, stream, out_part,
-                       lse_part, n_splits, n_q, n_heads, dv4, out, lse);
-  else
-    hipLaunchKernelGGL(merge_kernel<false>, dim3(blocks), dim3(256), 0, stream, out_part,
-                       lse_part, n_splits, n_q, n_heads, dv4, out, lse);
+#define LS_MERGE(OB, BN)                                                                  \
+  hipLaunchKernelGGL((merge_kernel<OB, BN>), dim3(blocks), dim3(256), 0, stream, out_part, \
+                     lse_part, n_splits, n_q, n_heads, dv4, out, lse)
+  if (out_bf16 && bf16_numerator) LS_MERGE(true, true);
+  else if (out_bf16) LS_MERGE(true, false);
+  else if (bf16_numerator) LS_MERGE(false, true);
+  else LS_MERGE(false, false);
+#undef LS_MERGE
   return hipGetLastError();
 }
 

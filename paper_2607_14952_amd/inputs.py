@@ -25,7 +25,7 @@ from concurrent.futures import ThreadPoolExecutor
 
 import numpy as np
 
-STREAM_TABLE, STREAM_K, STREAM_V, STREAM_Q, STREAM_DO, STREAM_PLANT, STREAM_IDX = range(7)
+STREAM_TABLE, STREAM_K, STREAM_V, STREAM_Q, STREAM_DO, STREAM_PLANT, STREAM_IDX, STREAM_PARTS = range(8)
 _CHUNK = 1 << 20
 
 
@@ -228,3 +228,42 @@ def response_inputs(cfg, member: int) -> dict:
                 k=draw(STREAM_K, (R, cfg.n_kv_heads, cfg.head_dim)),
                 v=draw(STREAM_V, (R, cfg.n_kv_heads, cfg.head_dim_v)),
                 d_out=draw(STREAM_DO, (R, cfg.n_q_heads, cfg.head_dim_v)))
+
+
+def merge_parts(seed: int, n_parts: int, n_q: int, n_heads: int, dv: int,
+                empty_frac: float = 0.05):
+    """Partial results to compose: o [n_parts, n_q, n_heads, dv] fp32 standard
+    normals and lse [n_parts, n_heads, n_q] fp32 normals of spread 3, with a
+    fraction of (part, head, row) entries empty (lse = -inf, o = 0), and (with
+    at least 3 rows) one row empty in every part."""
+    rng = _rng(seed, STREAM_PARTS)
+    o = rng.standard_normal((n_parts, n_q, n_heads, dv), dtype=np.float32)
+    lse = (3.0 * rng.standard_normal((n_parts, n_heads, n_q))).astype(np.float32)
+    empty = rng.random((n_parts, n_heads, n_q)) < empty_frac
+    if n_q >= 3:
+        empty[:, :, n_q // 2] = True
+    lse[empty] = -np.inf
+    o[np.transpose(empty, (0, 2, 1))] = 0.0
+    return o, lse
+
+
+def capture_inputs(cfg) -> dict:
+    """Prompt rows for a chunked capture: q_blocks [n_q_blocks, chunk, Hq, D]
+    (block b from stream (seed, Q, b)), k and v [length, Hkv, D] (chunk c's rows
+    from streams (seed, K|V, c)), all bf16 bit patterns, and the page table.
+    Chunk c's queries are the first rows of block c mod n_q_blocks."""
+    Hq, Hkv, D, C = cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim, cfg.chunk
+
+    def block(stream, key, rows, heads):
+        x = _rng(cfg.seed, stream, key).standard_normal((rows, heads, D), dtype=np.float32)
+        return to_bf16_bits(x)
+
+    with ThreadPoolExecutor(_threads()) as ex:
+        qb = list(ex.map(lambda b: block(STREAM_Q, b, C, Hq), range(cfg.n_q_blocks)))
+        rows = [cfg.chunk_range(c) for c in range(cfg.n_chunks)]
+        ks = list(ex.map(lambda c: block(STREAM_K, c, rows[c][1] - rows[c][0], Hkv),
+                         range(cfg.n_chunks)))
+        vs = list(ex.map(lambda c: block(STREAM_V, c, rows[c][1] - rows[c][0], Hkv),
+                         range(cfg.n_chunks)))
+    return {"q_blocks": np.stack(qb), "k": np.concatenate(ks), "v": np.concatenate(vs),
+            "page_table": page_table(cfg)}
