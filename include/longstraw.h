@@ -225,6 +225,52 @@ ls_status ls_sparse_attn_bwd(const ls_attn_params* p, const int32_t* idx, int32_
                              const float* lse, float* dq, void* workspace,
                              size_t workspace_bytes, void* stream);
 
+/*
+ * DSA index selection (Eq. dsa-index, Eq. dsa-attention, Eq. glm-global-dsa).
+ * One index key of head_dim bf16 per position, stored in pages like the KV
+ * pools ([n_phys_pages, page_size, head_dim], page_table as for
+ * ls_attn_params); per query row t, n_heads index queries [n_q, n_heads,
+ * head_dim] bf16 and head weights w [n_q, n_heads] fp32.  Supported:
+ * head_dim = 128, n_heads in {8, 16, 24, 32}, page_size a power of two >= 32.
+ * All pointers are device pointers, 16-byte aligned.
+ */
+typedef struct ls_dsa_params {
+  const void* q_index;
+  const float* w_index;
+  const void* k_index_pool;
+  const int32_t* page_table;
+  int64_t n_phys_pages, n_logical_pages;
+  int32_t n_q, n_heads, head_dim, page_size;
+} ls_dsa_params;
+
+/*
+ * ls_dsa_index_scores: I[t, s] = sum_j w[t, j] ReLU(<q[t, j], k_s>) (fp32,
+ * accumulated in fp32 from the bf16 products) for every row t < n_q and
+ * position s in [pos_begin, pos_end), written to scores[t * ld + s - pos_begin].
+ * pos_begin must be a multiple of 32, pos_end <= n_logical_pages * page_size
+ * and < 2^31, ld >= pos_end - pos_begin and a multiple of 4; scores must not
+ * overlap the inputs.  Page-table entries are not range-checked.
+ */
+ls_status ls_dsa_index_scores(const ls_dsa_params* p, int64_t pos_begin, int64_t pos_end,
+                              float* scores, int64_t ld, void* stream);
+
+/*
+ * ls_topk_select: for each row r < n_rows of scores (row r at scores + r * ld,
+ * n columns), the k largest scores; among equal scores the lower position is
+ * taken first (deterministic, so a merge of per-shard candidates reproduces
+ * the global selection).  Column i names position positions[r * ld + i] when
+ * positions is not NULL (the columns must then be in ascending position order,
+ * as concatenated per-shard candidates of contiguous shards are), else
+ * pos_offset + i.  Writes the selected positions in ascending order to
+ * out_pos[r * k ..] and, when out_scores is not NULL, their scores to
+ * out_scores[r * k ..]; when n < k the remaining entries get position -1 and
+ * score -inf.  NaN scores are the caller's error.  k >= 1, ld >= n, positions
+ * < 2^31.
+ */
+ls_status ls_topk_select(const float* scores, int64_t ld, const int32_t* positions,
+                         int32_t n_rows, int64_t n, int64_t pos_offset, int32_t k,
+                         int32_t* out_pos, float* out_scores, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

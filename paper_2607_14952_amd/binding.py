@@ -24,7 +24,7 @@ STATUS = {0: "LS_OK", -1: "LS_ERR_INVALID_ARG", -2: "LS_ERR_UNSUPPORTED", -3: "L
 EXPORTS = ["ls_abi_version", "ls_status_string", "ls_last_error", "ls_gather_kv", "ls_scatter_kv",
            "ls_prefix_attn_fwd", "ls_lse_merge", "ls_prefix_attn_bwd_workspace_size",
            "ls_prefix_attn_bwd", "ls_sparse_attn_workspace_size", "ls_sparse_attn_fwd",
-           "ls_sparse_attn_bwd"]
+           "ls_sparse_attn_bwd", "ls_dsa_index_scores", "ls_topk_select"]
 
 
 class AttnParams(ctypes.Structure):
@@ -35,6 +35,13 @@ class AttnParams(ctypes.Structure):
                 ("softmax_scale", c_float), ("flags", c_uint32), ("q", c_void_p),
                 ("k_pool", c_void_p), ("v_pool", c_void_p), ("page_table", c_void_p),
                 ("pool_epoch", c_uint64), ("expected_epoch", c_uint64)]
+
+
+class DsaParams(ctypes.Structure):
+    _fields_ = [("q_index", c_void_p), ("w_index", c_void_p), ("k_index_pool", c_void_p),
+                ("page_table", c_void_p), ("n_phys_pages", c_int64), ("n_logical_pages", c_int64),
+                ("n_q", c_int32), ("n_heads", c_int32), ("head_dim", c_int32),
+                ("page_size", c_int32)]
 
 
 class Split(ctypes.Structure):
@@ -87,6 +94,12 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.ls_sparse_attn_bwd.restype = c_int32
     lib.ls_sparse_attn_bwd.argtypes = [P, c_void_p, c_int32, c_void_p, c_void_p, c_int32, c_void_p,
                                        c_void_p, c_void_p, c_size_t, c_void_p]
+    lib.ls_dsa_index_scores.restype = c_int32
+    lib.ls_dsa_index_scores.argtypes = [POINTER(DsaParams), c_int64, c_int64, c_void_p, c_int64,
+                                        c_void_p]
+    lib.ls_topk_select.restype = c_int32
+    lib.ls_topk_select.argtypes = [c_void_p, c_int64, c_void_p, c_int32, c_int64, c_int64, c_int32,
+                                   c_void_p, c_void_p, c_void_p]
     if lib.ls_abi_version() != ABI_VERSION:
         raise RuntimeError("liblongstraw ABI version mismatch")
     _lib = lib
@@ -319,3 +332,38 @@ def sparse_attn_bwd(q, latent: PagedKV, idx, d_out, out, lse, *, prefix_len: int
                                             _ptr(out), _dtype_code(out), _ptr(lse), _ptr(dq),
                                             _ptr(workspace), workspace.numel(), _stream(stream)))
     return dq
+
+
+def dsa_index_scores(q_index, w_index, k_index_pool, page_table, *, pos_begin: int, pos_end: int,
+                     scores=None, stream=None):
+    """ls_dsa_index_scores: I [n_q, pos_end - pos_begin] fp32 (or into ``scores``,
+    a [n_q, ld] view with ld a multiple of 4)."""
+    torch = _torch()
+    n_q, H, d = q_index.shape
+    n = pos_end - pos_begin
+    if scores is None:
+        scores = torch.empty((n_q, max(n, 1) + (-n) % 4), dtype=torch.float32,
+                             device=q_index.device)
+    p = DsaParams(q_index.data_ptr(), w_index.data_ptr(), k_index_pool.data_ptr(),
+                  page_table.data_ptr(), k_index_pool.shape[0], page_table.shape[0], n_q, H, d,
+                  k_index_pool.shape[1])
+    check(load_library().ls_dsa_index_scores(ctypes.byref(p), pos_begin, pos_end, _ptr(scores),
+                                             scores.stride(0), _stream(stream)))
+    return scores[:, :n]
+
+
+def topk_select(scores, k: int, *, n: int | None = None, positions=None, pos_offset: int = 0,
+                out_pos=None, out_scores=None, stream=None):
+    """ls_topk_select over the rows of ``scores`` [rows, >= n] (row stride ld):
+    positions [rows, k] int32 ascending and their scores [rows, k]."""
+    torch = _torch()
+    rows = scores.shape[0]
+    n = scores.shape[1] if n is None else n
+    if out_pos is None:
+        out_pos = torch.empty((rows, k), dtype=torch.int32, device=scores.device)
+    if out_scores is None:
+        out_scores = torch.empty((rows, k), dtype=torch.float32, device=scores.device)
+    check(load_library().ls_topk_select(_ptr(scores), scores.stride(0), _ptr(positions), rows, n,
+                                        pos_offset, k, _ptr(out_pos), _ptr(out_scores),
+                                        _stream(stream)))
+    return out_pos, out_scores

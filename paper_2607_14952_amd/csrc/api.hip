@@ -613,3 +613,80 @@ LS_API ls_status ls_sparse_attn_bwd(const ls_attn_params* p, const int32_t* idx,
   if (e == hipSuccess) e = ls::launch_sparse_bwd(a, s);
   return e == hipSuccess ? LS_OK : hip_fail(e, "sparse backward launch");
 }
+
+LS_API ls_status ls_dsa_index_scores(const ls_dsa_params* p, int64_t pos_begin, int64_t pos_end,
+                                     float* scores, int64_t ld, void* stream) {
+  if (!p) return fail(LS_ERR_INVALID_ARG, "NULL params");
+  if (p->head_dim != 128) return fail(LS_ERR_UNSUPPORTED, "index head_dim must be 128");
+  if (p->n_heads != 8 && p->n_heads != 16 && p->n_heads != 24 && p->n_heads != 32)
+    return fail(LS_ERR_UNSUPPORTED, "index heads must be 8, 16, 24 or 32 (got %d)", p->n_heads);
+  if (!is_pow2(p->page_size) || p->page_size < 32)
+    return fail(LS_ERR_UNSUPPORTED, "page_size must be a power of two >= 32");
+  if (p->n_q < 0 || p->n_phys_pages <= 0 || p->n_logical_pages <= 0)
+    return fail(LS_ERR_INVALID_ARG, "bad sizes");
+  if (pos_begin < 0 || pos_end < pos_begin || pos_begin % 32 != 0 ||
+      pos_end > p->n_logical_pages * (int64_t)p->page_size || pos_end >= (int64_t(1) << 31))
+    return fail(LS_ERR_INVALID_ARG, "bad position range [%lld, %lld)", (long long)pos_begin,
+                (long long)pos_end);
+  if (ld < pos_end - pos_begin || ld % 4 != 0)
+    return fail(LS_ERR_INVALID_ARG, "ld %lld must be >= %lld and a multiple of 4",
+                (long long)ld, (long long)(pos_end - pos_begin));
+  if (p->n_q == 0 || pos_end == pos_begin) return LS_OK;
+  if (!p->q_index || !p->w_index || !p->k_index_pool || !p->page_table || !scores)
+    return fail(LS_ERR_INVALID_ARG, "NULL device pointer");
+  if (!aligned16(p->q_index) || !aligned16(p->w_index) || !aligned16(p->k_index_pool) ||
+      !aligned16(p->page_table) || !aligned16(scores))
+    return fail(LS_ERR_INVALID_ARG, "device pointers must be 16-byte aligned");
+  std::vector<Range> ins{rng("q_index", p->q_index, (size_t)p->n_q * p->n_heads * 256),
+                         rng("w_index", p->w_index, (size_t)p->n_q * p->n_heads * 4),
+                         rng("k_index_pool", p->k_index_pool,
+                             (size_t)p->n_phys_pages * p->page_size * 256),
+                         rng("page_table", p->page_table, (size_t)p->n_logical_pages * 4)};
+  std::vector<Range> outs{rng("scores", scores, ((size_t)(p->n_q - 1) * ld + (pos_end - pos_begin)) * 4)};
+  ls_status st = check_alias(outs, ins);
+  if (st != LS_OK) return st;
+  ls::DsaArgs a{};
+  a.q = p->q_index;
+  a.w = p->w_index;
+  a.k_pool = p->k_index_pool;
+  a.page_table = p->page_table;
+  a.scores = scores;
+  a.ld = ld;
+  a.pos_begin = pos_begin;
+  a.pos_end = pos_end;
+  a.n_q = p->n_q;
+  a.n_heads = p->n_heads;
+  a.log2_page = ilog2(p->page_size);
+  hipError_t e = ls::launch_dsa_scores(a, (hipStream_t)stream);
+  return e == hipSuccess ? LS_OK : hip_fail(e, "dsa score launch");
+}
+
+LS_API ls_status ls_topk_select(const float* scores, int64_t ld, const int32_t* positions,
+                                int32_t n_rows, int64_t n, int64_t pos_offset, int32_t k,
+                                int32_t* out_pos, float* out_scores, void* stream) {
+  if (k < 1 || n < 0 || n_rows < 0 || ld < n || pos_offset < 0 ||
+      pos_offset + n > (int64_t(1) << 31))
+    return fail(LS_ERR_INVALID_ARG, "bad top-k shape (rows %d, n %lld, ld %lld, k %d)", n_rows,
+                (long long)n, (long long)ld, k);
+  if (n_rows == 0) return LS_OK;
+  if ((n > 0 && !scores) || !out_pos) return fail(LS_ERR_INVALID_ARG, "NULL device pointer");
+  const size_t in_bytes = n > 0 ? ((size_t)(n_rows - 1) * ld + n) * 4 : 0;
+  std::vector<Range> ins{rng("scores", scores, in_bytes),
+                         rng("positions", positions, positions ? in_bytes : 0)};
+  std::vector<Range> outs{rng("out_pos", out_pos, (size_t)n_rows * k * 4),
+                          rng("out_scores", out_scores, out_scores ? (size_t)n_rows * k * 4 : 0)};
+  ls_status st = check_alias(outs, ins);
+  if (st != LS_OK) return st;
+  ls::TopkArgs a{};
+  a.scores = scores;
+  a.positions = positions;
+  a.out_pos = out_pos;
+  a.out_scores = out_scores;
+  a.ld = ld;
+  a.n = n;
+  a.pos_offset = pos_offset;
+  a.n_rows = n_rows;
+  a.k = k;
+  hipError_t e = ls::launch_topk(a, (hipStream_t)stream);
+  return e == hipSuccess ? LS_OK : hip_fail(e, "top-k launch");
+}

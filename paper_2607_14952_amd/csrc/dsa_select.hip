@@ -1,0 +1,368 @@
+// DSA index selection on gfx950: index scores (Eq. dsa-index) and the
+// deterministic top-k over them (Eq. dsa-attention, Eq. glm-global-dsa).
+//
+// Score kernel.  I[t, s] = sum_j w[t, j] ReLU(<q[t, j], k_s>) with H index
+// heads of width 128 and one index key per position (shared by the heads).
+// Workgroup = 4 waves = 32 tokens x a chunk of 8,192 positions; wave w holds
+// the queries of heads w H/4 .. (w+1) H/4 - 1 for the 32 tokens in registers.
+// Index-key tiles of 32 positions (8 KiB) stream by direct loads into a
+// four-slot LDS ring, two tiles ahead; the key operand of a tile is read once
+// per wave and reused by all of its heads.  Per tile a wave forms S^T = K Q^T
+// for each of its heads (8 MFMAs 32x32x16 over the 128-wide head, two heads'
+// chains interleaved), folds w ReLU(S) into a partial sum, and writes the
+// partial tile to LDS; after the tile barrier wave w adds the four partials of
+// tokens 8w .. 8w+7 and stores those rows of I (fp32).  Partials are double
+// buffered, so one barrier per tile serves the ring and the exchange.
+//
+// Top-k kernel.  One workgroup per row: three histogram passes over an
+// order-preserving 32-bit key of the fp32 scores (11, 11 and 10 bits) find the
+// exact k-th largest key T and the count of keys above it; a collection pass
+// then keeps every key above T and the first k - above keys equal to T in
+// position order (lower position first), writing positions in ascending
+// order.  Each of the 8 waves owns a contiguous segment of the row, so the
+// order survives: wave totals are scanned once between two passes.
+#include "ls_internal.h"
+#include "mfma_common.h"
+
+namespace ls {
+namespace {
+
+constexpr int kID = 128;                  // index head width
+constexpr int kIRow = kID * 2;            // bytes per index key
+constexpr int kITile = 32 * kIRow;        // 32 positions: 8 KiB
+constexpr int kIAhead = 2;
+constexpr int kISlots = kIAhead + 2;
+constexpr int kIChunk = 8192;             // positions per workgroup
+constexpr int kXWave = 32 * 32 * 4;       // one wave's partial tile (fp32)
+constexpr int kIKAhead = 3;               // key operand reads in flight
+
+// Key tile layout: 16-byte chunk c of row r sits at chunk c ^ (r & 15), so the
+// 16 rows a 16-lane phase reads at one logical chunk hit 16 distinct bank groups.
+__device__ __forceinline__ int ikey_off(int r, int c) { return r * kIRow + ((c ^ (r & 15)) << 4); }
+
+// Direct loads of one key tile: wave w issues instructions i = 0, 1, each
+// 1 KiB = 4 rows; lane l writes LDS row 4(2w+i) + l/16, physical chunk l%16,
+// which holds logical chunk (l%16) ^ (row & 15).
+struct IKeyFetch {
+  int lds_row[2], lane_row[2], lane_off[2];
+  __device__ __forceinline__ void init(int lane, int w) {
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      lds_row[i] = 4 * (2 * w + i);
+      lane_row[i] = lds_row[i] + (lane >> 4);
+      lane_off[i] = ((lane & 15) ^ (lane_row[i] & 15)) << 4;
+    }
+  }
+  // r: resource based at the tile's first physical row; rows at or beyond
+  // n_valid (1..32) repeat row n_valid - 1.
+  __device__ __forceinline__ void issue(char* tile, __amdgpu_buffer_rsrc_t r, int i,
+                                        int n_valid) const {
+    const int off = min(lane_row[i], n_valid - 1) * kIRow + lane_off[i];
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, LS_LDS(tile + lds_row[i] * kIRow), 16, off, 0, 0,
+                                             0);
+  }
+};
+
+// Partial tile of one wave: [token][position] fp32, 16-byte chunk (position/4)
+// stored at chunk ^ (token & 7).
+__device__ __forceinline__ int xoff(int tok, int c) { return tok * 128 + ((c ^ (tok & 7)) << 4); }
+
+template <int kHPW>   // heads per wave (H / 4), even
+__global__ __launch_bounds__(256, 1) void dsa_score_kernel(DsaArgs a) {
+  __shared__ __attribute__((aligned(1024))) char smem[kISlots * kITile + 2 * 4 * kXWave];
+  char* xbase = smem + kISlots * kITile;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int l32 = lane & 31, hh = lane >> 5;
+  const int tok0 = blockIdx.y * 32;
+  const int tok = tok0 + l32;
+  const bool row_ok = tok < a.n_q;
+  const int64_t c0 = a.pos_begin + (int64_t)blockIdx.x * kIChunk;   // multiple of 32
+  const int64_t c1 = min(a.pos_end, c0 + kIChunk);
+  const int n_tiles = (int)((c1 - c0 + 31) / 32);
+
+  // this wave's heads: queries (B operand: lane = token, dims 16ks + 8hh ..) and weights
+  bf16x8 qreg[kHPW][8];
+  float wv[kHPW];
+#pragma unroll
+  for (int j = 0; j < kHPW; ++j) {
+    const int head = w * kHPW + j;
+    const __bf16* qrow = static_cast<const __bf16*>(a.q) + ((int64_t)tok * a.n_heads + head) * kID;
+#pragma unroll
+    for (int ks = 0; ks < 8; ++ks) {
+      if (row_ok) {
+        qreg[j][ks] = *reinterpret_cast<const bf16x8*>(qrow + ks * 16 + hh * 8);
+      } else {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) qreg[j][ks][e] = (__bf16)0.f;
+      }
+    }
+    wv[j] = row_ok ? a.w[(int64_t)tok * a.n_heads + head] : 0.f;
+  }
+
+  IKeyFetch f;
+  f.init(lane, w);
+  PageLookup pl;
+  pl.init(a.page_table, a.log2_page);
+  auto tile0 = [&](int t) { return c0 + (int64_t)(t < n_tiles ? t : n_tiles - 1) * 32; };
+  auto rsrc_of = [&](int64_t prow) {
+    return __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<char*>(static_cast<const char*>(a.k_pool) + prow * kIRow), (short)0, 0x7FFFFFFF,
+        0x00020000);
+  };
+#pragma unroll
+  for (int i = 0; i < kIAhead; ++i) {
+    const int64_t t0 = tile0(i);
+    const auto r = rsrc_of(phys_pos_uniform(a.page_table, t0, a.log2_page));
+    const int nv = (int)min(c1 - t0, (int64_t)32);
+    f.issue(smem + i * kITile, r, 0, nv);
+    f.issue(smem + i * kITile, r, 1, nv);
+  }
+  int32_t pe = pl.load(tile0(kIAhead));
+
+  wait_fetch();   // (a full wait: the query loads may have been scheduled after the stages)
+  tile_barrier();
+
+  for (int t = 0; t < n_tiles; ++t) {
+    const char* __restrict__ kt = smem + (t % kISlots) * kITile;
+    char* __restrict__ next = smem + ((t + kIAhead) % kISlots) * kITile;
+    char* __restrict__ xw = xbase + ((t & 1) * 4 + w) * kXWave;
+    const int64_t t0n = tile0(t + kIAhead);
+    const int64_t prow_next = pl.row(pe, t0n);
+    pe = pl.load(tile0(t + kIAhead + 1));
+    __builtin_amdgcn_sched_barrier(0);
+    const auto rn = rsrc_of(prow_next);
+    const int nvn = (int)min(c1 - t0n, (int64_t)32);
+
+    // key operand (A: lane = position l32, dims 16ks + 8hh ..), read once per tile
+    bf16x8 kreg[8];
+#pragma unroll
+    for (int i = 0; i < kIKAhead; ++i)
+      kreg[i] = *reinterpret_cast<const bf16x8*>(kt + ikey_off(l32, 2 * i + hh));
+    mfma_fence();
+    f32x16 part = zero16();
+#pragma unroll
+    for (int j = 0; j < kHPW; j += 2) {
+      f32x16 s0 = zero16(), s1 = zero16();
+#pragma unroll
+      for (int ks = 0; ks < 8; ++ks) {
+        if (j == 0 && ks + kIKAhead < 8)
+          kreg[ks + kIKAhead] =
+              *reinterpret_cast<const bf16x8*>(kt + ikey_off(l32, 2 * (ks + kIKAhead) + hh));
+        s0 = mfma32(kreg[ks], qreg[j][ks], s0);
+        s1 = mfma32(kreg[ks], qreg[j + 1][ks], s1);
+        if (j == 0 && ks < 2) f.issue(next, rn, ks, nvn);
+        mfma_fence();
+      }
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        part[r] = fmaf(wv[j], fmaxf(s0[r], 0.f), part[r]);
+        part[r] = fmaf(wv[j + 1], fmaxf(s1[r], 0.f), part[r]);
+      }
+    }
+    // partial tile: lane (token l32, half hh) holds positions 8q + 4hh + {0..3}
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      f32x4 v = {part[4 * q], part[4 * q + 1], part[4 * q + 2], part[4 * q + 3]};
+      *reinterpret_cast<f32x4*>(xw + xoff(l32, 2 * q + hh)) = v;
+    }
+    wait_newest_stage<2>();
+    __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0): the partial tile is in LDS
+    tile_barrier();
+    // wave w: tokens 8w + lane/8, positions 4 (lane%8) .. +3 of this tile
+    {
+      const int rt = 8 * w + (lane >> 3), c = lane & 7;
+      const char* xb = xbase + (t & 1) * 4 * kXWave;
+      f32x4 sum = *reinterpret_cast<const f32x4*>(xb + xoff(rt, c));
+#pragma unroll
+      for (int v = 1; v < 4; ++v) sum += *reinterpret_cast<const f32x4*>(xb + v * kXWave + xoff(rt, c));
+      const int otok = tok0 + rt;
+      const int64_t pos = c0 + (int64_t)t * 32 + 4 * c;
+      if (otok < a.n_q) {
+        float* dst = a.scores + (int64_t)otok * a.ld + (pos - a.pos_begin);
+        if (pos + 4 <= c1) {
+          *reinterpret_cast<f32x4*>(dst) = sum;
+        } else {
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            if (pos + e < c1) dst[e] = sum[e];
+        }
+      }
+    }
+  }
+  wait_fetch();   // no direct load is left in flight when the waves end
+}
+
+// ---------------------------------------------------------------- top-k
+constexpr int kKThreads = 512;
+constexpr int kKWaves = kKThreads / 64;
+constexpr int kKUnroll = 8;   // independent loads in flight per thread
+
+__device__ __forceinline__ uint32_t okey(float x) {
+  const uint32_t u = __float_as_uint(x);
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+__global__ __launch_bounds__(kKThreads) void topk_kernel(TopkArgs a) {
+  __shared__ uint32_t hist[2048];
+  __shared__ uint32_t wave_gt[kKWaves], wave_eq[kKWaves];
+  __shared__ uint32_t sh_bin, sh_above;
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  const int64_t row = blockIdx.x;
+  const float* x = a.scores + row * a.ld;
+  const int32_t* px = a.positions ? a.positions + row * a.ld : nullptr;
+  int32_t* op = a.out_pos + row * a.k;
+  float* os = a.out_scores ? a.out_scores + row * a.k : nullptr;
+  auto pos_of = [&](int64_t i) { return px ? px[i] : (int32_t)(a.pos_offset + i); };
+
+  if (a.n <= a.k) {   // everything is selected
+    for (int64_t i = tid; i < a.k; i += kKThreads) {
+      op[i] = i < a.n ? pos_of(i) : -1;
+      if (os) os[i] = i < a.n ? x[i] : -INFINITY;
+    }
+    return;
+  }
+
+  // exact k-th largest key: 11 + 11 + 10 bits
+  uint32_t prefix = 0, above = 0;
+#pragma unroll 1
+  for (int pass = 0; pass < 3; ++pass) {
+    const int shift = pass == 0 ? 21 : (pass == 1 ? 10 : 0);
+    const int nbins = pass == 2 ? 1024 : 2048;
+    for (int b = tid; b < nbins; b += kKThreads) hist[b] = 0;
+    if (tid == 0) {
+      sh_bin = 0;
+      sh_above = above;
+    }
+    __syncthreads();
+    for (int64_t i0 = tid; i0 < a.n; i0 += kKUnroll * kKThreads) {
+      float v[kKUnroll];
+#pragma unroll
+      for (int u = 0; u < kKUnroll; ++u) {
+        const int64_t i = i0 + (int64_t)u * kKThreads;
+        v[u] = i < a.n ? x[i] : 0.f;
+      }
+#pragma unroll
+      for (int u = 0; u < kKUnroll; ++u) {
+        const int64_t i = i0 + (int64_t)u * kKThreads;
+        const uint32_t key = okey(v[u]);
+        const bool in = i < a.n && (pass == 0 || (key >> (shift + (pass == 1 ? 11 : 10))) == prefix);
+        if (in) atomicAdd(&hist[(key >> shift) & (nbins - 1)], 1u);
+      }
+    }
+    __syncthreads();
+    if (wv == 0) {
+      // lane owns bins [lane*per, (lane+1)*per); scan from the top
+      const int per = nbins / 64;
+      uint32_t mine = 0;
+      for (int b = 0; b < per; ++b) mine += hist[lane * per + b];
+      // suffix sum over lanes: total of lanes > lane
+      uint32_t incl = mine;
+#pragma unroll
+      for (int d = 1; d < 64; d <<= 1) {
+        const uint32_t o = __shfl_down(incl, d);
+        if (lane + d < 64) incl += o;
+      }
+      const uint32_t excl = incl - mine;   // keys in bins of higher lanes
+      const uint32_t need = (uint32_t)a.k - above;
+      // the crossing lane: excl < need <= incl
+      if (excl < need && need <= incl) {
+        uint32_t acc = excl;
+        int b = lane * per + per - 1;
+        for (; b > lane * per; --b) {
+          if (acc + hist[b] >= need) break;
+          acc += hist[b];
+        }
+        sh_bin = (uint32_t)b;
+        sh_above = above + acc;
+      }
+    }
+    __syncthreads();
+    prefix = (prefix << (pass == 2 ? 10 : 11)) | sh_bin;
+    above = sh_above;
+    __syncthreads();
+  }
+  const uint32_t T = prefix;
+  const uint32_t need_eq = (uint32_t)a.k - above;   // keys equal to T to keep, lowest first
+
+  // collection: wave v owns the contiguous segment [lo, hi)
+  const int64_t seg = ((a.n + kKWaves - 1) / kKWaves + 63) / 64 * 64;
+  const int64_t lo = (int64_t)wv * seg, hi = min(a.n, lo + seg);
+  const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+  uint32_t n_gt = 0, n_eq = 0;
+  for (int64_t i0 = lo; i0 < hi; i0 += 64 * kKUnroll) {
+    float v[kKUnroll];
+#pragma unroll
+    for (int u = 0; u < kKUnroll; ++u) {
+      const int64_t i = i0 + 64 * u + lane;
+      v[u] = i < hi ? x[i] : 0.f;
+    }
+#pragma unroll
+    for (int u = 0; u < kKUnroll; ++u) {
+      const bool ok = i0 + 64 * u + lane < hi;
+      const uint32_t key = okey(v[u]);
+      n_gt += __popcll(__ballot(ok && key > T));
+      n_eq += __popcll(__ballot(ok && key == T));
+    }
+  }
+  if (lane == 0) {
+    wave_gt[wv] = n_gt;
+    wave_eq[wv] = n_eq;
+  }
+  __syncthreads();
+  uint32_t base = 0, eq_before = 0;
+  for (int v = 0; v < wv; ++v) {
+    const uint32_t take = eq_before >= need_eq ? 0u : min(wave_eq[v], need_eq - eq_before);
+    base += wave_gt[v] + take;
+    eq_before += wave_eq[v];
+  }
+  uint32_t run_sel = 0, run_eq = 0;
+  for (int64_t i0 = lo; i0 < hi; i0 += 64 * kKUnroll) {
+    float v[kKUnroll];
+#pragma unroll
+    for (int u = 0; u < kKUnroll; ++u) {
+      const int64_t i = i0 + 64 * u + lane;
+      v[u] = i < hi ? x[i] : 0.f;
+    }
+#pragma unroll
+    for (int u = 0; u < kKUnroll; ++u) {
+      const int64_t i = i0 + 64 * u + lane;
+      const bool ok = i < hi;
+      const uint32_t key = okey(v[u]);
+      const bool gt = ok && key > T, eq = ok && key == T;
+      const uint64_t eqm = __ballot(eq);
+      const uint32_t eq_rank = eq_before + run_eq + (uint32_t)__popcll(eqm & below);
+      const bool sel = gt || (eq && eq_rank < need_eq);
+      const uint64_t selm = __ballot(sel);
+      const uint32_t o = base + run_sel + (uint32_t)__popcll(selm & below);
+      if (sel && o < (uint32_t)a.k) {   // (exactly k are selected; the test only guards)
+        op[o] = pos_of(i);
+        if (os) os[o] = v[u];
+      }
+      run_sel += (uint32_t)__popcll(selm);
+      run_eq += (uint32_t)__popcll(eqm);
+    }
+  }
+}
+
+}  // namespace
+
+hipError_t launch_dsa_scores(const DsaArgs& a, hipStream_t stream) {
+  const unsigned chunks = (unsigned)((a.pos_end - a.pos_begin + kIChunk - 1) / kIChunk);
+  const dim3 grid(chunks, (unsigned)((a.n_q + 31) / 32));
+  switch (a.n_heads) {
+    case 8: hipLaunchKernelGGL(dsa_score_kernel<2>, grid, dim3(256), 0, stream, a); break;
+    case 16: hipLaunchKernelGGL(dsa_score_kernel<4>, grid, dim3(256), 0, stream, a); break;
+    case 24: hipLaunchKernelGGL(dsa_score_kernel<6>, grid, dim3(256), 0, stream, a); break;
+    case 32: hipLaunchKernelGGL(dsa_score_kernel<8>, grid, dim3(256), 0, stream, a); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_topk(const TopkArgs& a, hipStream_t stream) {
+  hipLaunchKernelGGL(topk_kernel, dim3((unsigned)a.n_rows), dim3(kKThreads), 0, stream, a);
+  return hipGetLastError();
+}
+
+}  // namespace ls

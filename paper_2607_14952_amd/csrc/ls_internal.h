@@ -63,6 +63,27 @@ struct BwdArgs {
   int32_t accumulate_dq, accumulate_dkv;
 };
 
+// DSA index scores (Eq. dsa-index) over positions [pos_begin, pos_end).
+struct DsaArgs {
+  const void* q;             // [n_q, n_heads, 128] bf16 index queries
+  const float* w;            // [n_q, n_heads] head weights
+  const void* k_pool;        // [n_phys, page, 128] bf16 index keys, one per position
+  const int32_t* page_table;
+  float* scores;             // [n_q, ld]: I[t, s] at t * ld + (s - pos_begin)
+  int64_t ld, pos_begin, pos_end;
+  int32_t n_q, n_heads, log2_page;
+};
+
+// Top-k of each row of a score matrix (Eq. glm-global-dsa).
+struct TopkArgs {
+  const float* scores;       // [n_rows, ld]
+  const int32_t* positions;  // [n_rows, ld] or null (position = pos_offset + column)
+  int32_t* out_pos;          // [n_rows, k]
+  float* out_scores;         // [n_rows, k] or null
+  int64_t ld, n, pos_offset;
+  int32_t n_rows, k;
+};
+
 // Sparse latent replay (one shared latent row per position, 576 / 512 wide).
 struct SparseArgs {
   const void* q;             // [n_q, H, 576] bf16
@@ -99,6 +120,8 @@ hipError_t launch_merge(const float* out_part, const float* lse_part, int n_spli
                         int n_heads, int dv, bool out_bf16, bool bf16_numerator, void* out,
                         float* lse, hipStream_t stream);
 hipError_t launch_fwd_f32(const FwdArgs& a, hipStream_t stream);
+hipError_t launch_dsa_scores(const DsaArgs& a, hipStream_t stream);
+hipError_t launch_topk(const TopkArgs& a, hipStream_t stream);
 hipError_t launch_fwd_bf16_d256(const FwdArgs& a, hipStream_t stream);
 hipError_t launch_bwd_prep(const void* d_out, const void* out, bool dout_bf16, bool out_bf16,
                            const float* lse, int n_q, int n_heads, int dv, float* delta,

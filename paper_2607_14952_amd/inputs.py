@@ -25,7 +25,8 @@ from concurrent.futures import ThreadPoolExecutor
 
 import numpy as np
 
-STREAM_TABLE, STREAM_K, STREAM_V, STREAM_Q, STREAM_DO, STREAM_PLANT, STREAM_IDX, STREAM_PARTS = range(8)
+STREAM_TABLE, STREAM_K, STREAM_V, STREAM_Q, STREAM_DO, STREAM_PLANT, STREAM_IDX, STREAM_PARTS, \
+    STREAM_IQ, STREAM_IW, STREAM_IK = range(11)
 _CHUNK = 1 << 20
 
 
@@ -267,3 +268,22 @@ def capture_inputs(cfg) -> dict:
                          range(cfg.n_chunks)))
     return {"q_blocks": np.stack(qb), "k": np.concatenate(ks), "v": np.concatenate(vs),
             "page_table": page_table(cfg)}
+
+
+def dsa_index_inputs(seed: int, n_q: int, n_heads: int, n_pos: int, page_size: int,
+                     head_dim: int = 128, pool_slack: float = 1.25) -> dict:
+    """Index-selection inputs (Eq. dsa-index): q_index [n_q, n_heads, head_dim]
+    and one index key per position in a paged pool [n_phys, page_size,
+    head_dim] (bf16 bit patterns, N(0,1) before rounding), head weights
+    w_index [n_q, n_heads] fp32 N(0,1) / sqrt(n_heads), and a page table
+    (seeded choice of distinct physical pages)."""
+    n_log = -(-n_pos // page_size)
+    n_phys = max(n_log, int(np.ceil(n_log * pool_slack)))
+    q = _rng(seed, STREAM_IQ).standard_normal((n_q, n_heads, head_dim), dtype=np.float32)
+    w = (_rng(seed, STREAM_IW).standard_normal((n_q, n_heads), dtype=np.float32)
+         / np.float32(np.sqrt(n_heads)))
+    k = normal_chunks(seed, STREAM_IK, n_phys * page_size * head_dim).reshape(
+        n_phys, page_size, head_dim)
+    table = _rng(seed, STREAM_TABLE).choice(n_phys, size=n_log, replace=False).astype(np.int32)
+    return {"q_index": to_bf16_bits(q), "w_index": w, "k_index_pool": to_bf16_bits(k),
+            "page_table": table}

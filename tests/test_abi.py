@@ -166,3 +166,45 @@ def test_scatter_rejects():
     assert lib.ls_scatter_kv(ctypes.byref(p), 0, 64 * 256 + 1, FAKE * 300, FAKE * 400, None) == -1
     assert lib.ls_scatter_kv(ctypes.byref(p), 0, 0, FAKE * 300, FAKE * 400, None) == 0
     assert lib.ls_scatter_kv(ctypes.byref(p), 0, 16, 0, FAKE * 400, None) == -1
+
+
+def _dsa_params(**kw):
+    f = dict(q_index=FAKE, w_index=FAKE * 16, k_index_pool=FAKE * 32, page_table=FAKE * 64,
+             n_phys_pages=256, n_logical_pages=256, n_q=64, n_heads=32, head_dim=128,
+             page_size=64)
+    f.update(kw)
+    return B.DsaParams(**f)
+
+
+@pytest.mark.parametrize("kw,rng,status", [
+    (dict(head_dim=64), (0, 4096), -2),
+    (dict(n_heads=12), (0, 4096), -2),
+    (dict(page_size=16), (0, 4096), -2),
+    (dict(), (16, 4096), -1),                  # pos_begin not a multiple of 32
+    (dict(), (0, 256 * 64 + 1), -1),           # beyond the table
+    (dict(), (4096, 0), -1),
+])
+def test_dsa_scores_rejects(kw, rng, status):
+    lib = B.load_library()
+    p = _dsa_params(**kw)
+    assert lib.ls_dsa_index_scores(ctypes.byref(p), rng[0], rng[1], FAKE * 1024, 4096, None) == status
+    assert lib.ls_last_error()
+
+
+def test_dsa_scores_rejects_ld_and_alias():
+    lib = B.load_library()
+    p = _dsa_params()
+    assert lib.ls_dsa_index_scores(ctypes.byref(p), 0, 4096, FAKE * 1024, 4095, None) == -1
+    assert lib.ls_dsa_index_scores(ctypes.byref(p), 0, 4096, FAKE * 1024, 4094, None) == -1
+    assert lib.ls_dsa_index_scores(ctypes.byref(p), 0, 4096, FAKE * 32, 4096, None) == -4
+
+
+def test_topk_rejects():
+    lib = B.load_library()
+    ok = (FAKE, 1000, None, 4, 1000, 0, 16, FAKE * 64, FAKE * 96, None)
+    assert lib.ls_topk_select(*ok[:6], 0, *ok[7:]) == -1                         # k = 0
+    assert lib.ls_topk_select(FAKE, 999, None, 4, 1000, 0, 16, FAKE * 64, None, None) == -1   # ld < n
+    assert lib.ls_topk_select(FAKE, 1000, None, 4, 1000, (1 << 31) - 10, 16, FAKE * 64, None,
+                              None) == -1                                       # positions >= 2^31
+    assert lib.ls_topk_select(FAKE, 1000, None, 4, 1000, 0, 16, FAKE + 64, None, None) == -4
+    assert lib.ls_topk_select(FAKE, 1000, None, 0, 1000, 0, 16, FAKE * 64, None, None) == 0

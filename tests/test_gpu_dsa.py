@@ -1,0 +1,142 @@
+"""DSA index selection on the HIP path (needs an MI355X): index scores
+(Eq. dsa-index) against the fp64 oracle, and the deterministic top-k
+(Eq. glm-global-dsa).
+
+Bars: scores within 2e-6 of the oracle relative to the sum of the terms'
+magnitudes (fp32 sums of exact bf16 products); the top-k of the GPU's fp32
+scores equals the oracle's top-k of the same scores exactly (the selection
+is integer work, decided in the kernel's precision); a merge of per-shard
+candidates equals the global selection exactly; against the fp64 scores the
+selection is valid: no unselected position scores above a selected one by
+more than the score tolerance."""
+from __future__ import annotations
+
+import numpy as np
+import pytest
+
+import oracle as O
+from paper_2607_14952_amd import binding as B
+from paper_2607_14952_amd import inputs
+from paper_2607_14952_amd.replay import to_device
+from tests._gpu import announce, host
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu_ready():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    B.load_library()
+
+
+def _inputs(seed, n_q, H, n_pos, S=64):
+    h = inputs.dsa_index_inputs(seed, n_q, H, n_pos, S)
+    return h, {k: to_device(v) for k, v in h.items()}
+
+
+def _term_scale(h, S, b, e):
+    """sum_j |w_j| |q_j . k_s| per (row, position): the scale of the fp32 sums."""
+    K = O.decode(O.gather(h["k_index_pool"], h["page_table"], S, np.arange(b, e)))
+    Q = O.decode(h["q_index"])
+    return np.einsum("rh,rhn->rn", np.abs(h["w_index"].astype(np.float64)),
+                     np.abs(np.einsum("rhd,nd->rhn", Q, K)))
+
+
+@pytest.mark.parametrize("H,n_q,rng", [(32, 70, (0, 20000 + 17)), (8, 33, (4096, 9000)),
+                                       (16, 32, (0, 64)), (24, 5, (8192, 8192 + 8192 + 31))])
+def test_index_scores(H, n_q, rng):
+    import torch
+    S = 64
+    b, e = rng
+    h, dev = _inputs(41 + H, n_q, H, e + 100, S)
+    announce(f"dsa scores H={H} n_q={n_q} [{b},{e})")
+    sc = B.dsa_index_scores(dev["q_index"], dev["w_index"], dev["k_index_pool"],
+                            dev["page_table"], pos_begin=b, pos_end=e)
+    torch.cuda.synchronize()
+    got = host(sc)
+    ref = O.dsa_index_scores(h["q_index"], h["w_index"], h["k_index_pool"], h["page_table"],
+                             page_size=S, pos_begin=b, pos_end=e)
+    scale = _term_scale(h, S, b, e)
+    err = np.abs(got - ref) / (scale + 1e-30)
+    assert err.max() <= 2e-6, f"max scaled error {err.max():.2e}"
+
+
+def _gpu_scores(seed=51, n_q=40, H=32, n_pos=30000, S=64):
+    h, dev = _inputs(seed, n_q, H, n_pos, S)
+    sc = B.dsa_index_scores(dev["q_index"], dev["w_index"], dev["k_index_pool"],
+                            dev["page_table"], pos_begin=0, pos_end=n_pos)
+    return h, sc
+
+
+@pytest.mark.parametrize("k,quant", [(2048, None), (100, 0.25), (1, None), (777, 4.0)])
+def test_topk_exact_on_gpu_scores(k, quant):
+    """The kernel's selection equals the oracle's rule applied to the same
+    fp32 scores; quantized scores give heavy ties (lower position first)."""
+    import torch
+    h, sc = _gpu_scores()
+    if quant is not None:
+        sc = torch.round(sc / quant) * quant          # many equal scores
+    sc = sc.contiguous()
+    announce(f"topk k={k} quant={quant}")
+    pos, val = B.topk_select(sc, k)
+    torch.cuda.synchronize()
+    s_host = host(sc)
+    want = O.topk_select(s_host.astype(np.float64), k)
+    assert np.array_equal(host(pos), want)
+    assert np.array_equal(host(val), np.take_along_axis(s_host, want, axis=1))
+
+
+def test_topk_fewer_than_k_and_offsets():
+    import torch
+    sc = torch.tensor([[1.0, 3.0, 2.0, 3.0, -1.0], [0.0, 0.0, 0.0, 0.0, 0.0]], device="cuda")
+    pos, val = B.topk_select(sc, 8, pos_offset=100)
+    torch.cuda.synchronize()
+    assert host(pos).tolist() == [[100, 101, 102, 103, 104, -1, -1, -1]] * 2
+    assert np.all(np.isneginf(host(val)[:, 5:]))
+    pos, _ = B.topk_select(sc, 3, pos_offset=100)
+    assert host(pos).tolist() == [[101, 102, 103], [100, 101, 102]]
+
+
+def test_candidate_merge_equals_global():
+    """Eq. glm-global-dsa: each contiguous shard's local top-k with global
+    positions, concatenated in shard order and merged by the same kernel, is
+    the global top-k; one shard's local selection is not."""
+    import torch
+    h, sc = _gpu_scores(seed=52, n_pos=40000)
+    sc = (torch.round(sc * 8) / 8).contiguous()      # ties across shard borders too
+    k = 512
+    glob, _ = B.topk_select(sc, k)
+    bounds = [0, 4096, 13000, 13001, 29999, 40000]
+    cps, css = [], []
+    for b, e in zip(bounds[:-1], bounds[1:]):
+        announce(f"local topk [{b},{e})")
+        p, v = B.topk_select(sc[:, b:], k, n=e - b, pos_offset=b)
+        keep = min(k, e - b)
+        cps.append(p[:, :keep])
+        css.append(v[:, :keep])
+    cand_pos = torch.cat(cps, dim=1).contiguous()
+    cand_sc = torch.cat(css, dim=1).contiguous()
+    merged, _ = B.topk_select(cand_sc, k, positions=cand_pos)
+    torch.cuda.synchronize()
+    assert np.array_equal(host(merged), host(glob))
+    assert not np.array_equal(host(cps[0][:, :k]), host(glob))
+
+
+def test_selection_valid_against_fp64_scores():
+    """Against the oracle's fp64 scores, the GPU's top-2048 is a valid top-2048
+    up to the score tolerance: min selected >= max unselected - tol."""
+    import torch
+    h, sc = _gpu_scores(seed=53, n_q=20, n_pos=50000)
+    pos, _ = B.topk_select(sc, 2048)
+    torch.cuda.synchronize()
+    ref = O.dsa_index_scores(h["q_index"], h["w_index"], h["k_index_pool"], h["page_table"],
+                             page_size=64, pos_begin=0, pos_end=50000)
+    scale = _term_scale(h, 64, 0, 50000)
+    tol = 2e-6 * scale.max(axis=1)
+    sel = pos.cpu().numpy().astype(np.int64)
+    for r in range(ref.shape[0]):
+        mask = np.zeros(50000, bool)
+        mask[sel[r]] = True
+        assert ref[r][mask].min() >= ref[r][~mask].max() - 2 * tol[r]
