@@ -239,9 +239,16 @@ def run_sparse(cfg, args):
     h = inputs.sparse_inputs(cfg)
     q = to_device(h["q"])
     lat = to_device(h["latent_pool"])
-    kv = B.PagedKV(lat, lat, to_device(h["page_table"]))
+    table = to_device(h["page_table"])
+    kv = B.PagedKV(lat, lat, table)
     idx = to_device(h["idx"])
     d_out = to_device(h["d_out"])
+    sel = None
+    if cfg.index_heads:
+        from paper_2607_14952_amd.dsa import DsaSelect
+        sel = DsaSelect(cfg, {"q_index": to_device(h["q_index"]), "w_index": to_device(h["w_index"]),
+                              "k_index_pool": to_device(h["k_index_pool"]), "page_table": table},
+                        mode=args.dsa_mode)
     del h
     kw = dict(prefix_len=cfg.prefix_len, q_pos0=cfg.q_pos0, scale=cfg.scale)
     ws = B.sparse_workspace(q, kv, cfg.topk, backward=True, prefix_len=cfg.prefix_len,
@@ -252,6 +259,14 @@ def run_sparse(cfg, args):
     dq = torch.empty((cfg.resp_len, cfg.n_q_heads, 576), dtype=torch.float32, device="cuda")
 
     def step(ev=None):
+        nonlocal idx
+        if sel is not None:   # the step selects its indices (Eq. dsa-index, top-k)
+            if ev:
+                ev[3].record()
+            sel.score()
+            if ev:
+                ev[4].record()
+            idx = sel.select()
         if ev:
             ev[0].record()
         B.sparse_attn_fwd(q, kv, idx, out=out, lse=lse, workspace=ws, **kw)
@@ -266,7 +281,7 @@ def run_sparse(cfg, args):
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
     t0 = time.perf_counter()
     for s in range(args.steps):
         step(evs[s])
@@ -280,19 +295,37 @@ def run_sparse(cfg, args):
     fwd_ms = sum(e[0].elapsed_time(e[1]) for e in evs) / args.steps
     bwd_ms = sum(e[1].elapsed_time(e[2]) for e in evs) / args.steps
     ms = wall * 1e3 / args.steps
+    extra = {}
+    if sel is not None:
+        score_ms = sum(e[3].elapsed_time(e[4]) for e in evs) / args.steps
+        topk_ms = sum(e[4].elapsed_time(e[0]) for e in evs) / args.steps
+        score_fl = 2 * R * cfg.prefix_len * cfg.index_heads * 128
+        extra["selection"] = {
+            "mode": args.dsa_mode, "index_heads": cfg.index_heads, "topk": cfg.topk,
+            "score_ms": round(score_ms, 3),
+            "score_tflops": round(score_fl / (score_ms * 1e-3) / 1e12, 2),
+            "topk_ms": round(topk_ms, 3),
+            "topk_score_gbs_per_pass": round(R * cfg.prefix_len * 4 / (topk_ms * 1e-3) / 1e9, 1),
+            "score_flop": score_fl}
     print(json.dumps({
         "metric": "sparse latent replay TFLOP/s (fwd+bwd dq), MLA 576/512 with top-k selection",
-        "value": round((fwd_fl + bwd_fl) / (ms * 1e-3) / 1e12, 2), "unit": "TFLOP/s",
+        "value": round((fwd_fl + bwd_fl + extra.get("selection", {}).get("score_flop", 0))
+                       / (ms * 1e-3) / 1e12, 2), "unit": "TFLOP/s",
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 3),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
         "data": "synthetic",
         "config": {"workload": f"{cfg.name}: {H} heads sharing one 576-wide latent row, prefix "
                                f"{cfg.prefix_len} in {cfg.page_size}-entry pages, {R} tokens x "
-                               f"top-{cfg.topk} + causal window", "parallelism": "single-gpu"},
+                               f"top-{cfg.topk} + causal window"
+                               + (f"; indices selected in the step by DSA index scores "
+                                  f"({cfg.index_heads} heads x 128, counted in the FLOP) and "
+                                  f"top-{cfg.topk} ({args.dsa_mode})" if sel is not None else
+                                  "; seeded indices"), "parallelism": "single-gpu"},
         "fwd_ms": round(fwd_ms, 3), "fwd_tflops": round(fwd_fl / (fwd_ms * 1e-3) / 1e12, 2),
         "fwd_gather_gbs": round(gathered / (fwd_ms * 1e-3) / 1e9, 1),
         "bwd_ms": round(bwd_ms, 3), "bwd_tflops": round(bwd_fl / (bwd_ms * 1e-3) / 1e12, 2),
-        "flop_per_step": {"fwd": fwd_fl, "bwd": bwd_fl}, "gpu": torch.cuda.get_device_name(0)}),
+        "flop_per_step": {"fwd": fwd_fl, "bwd": bwd_fl}, "gpu": torch.cuda.get_device_name(0),
+        **extra}),
         flush=True)
 
 
@@ -365,6 +398,10 @@ def main():
                     help="prefix pages to shards: contiguous ranges or page p to shard p mod 8")
     ap.add_argument("--bf16-numerator", action="store_true",
                     help="the step's cross-shard merge reduces the numerator in bf16")
+    ap.add_argument("--dsa-select", action="store_true",
+                    help="c5: select each row's top-k with the DSA index scores inside the step")
+    ap.add_argument("--dsa-mode", choices=("global", "candidates"), default="global",
+                    help="selection: one top-k per row, or per-shard candidates and a merge")
     ap.add_argument("--skip-extras", action="store_true",
                     help="skip page streaming, measured ceilings and clocks (profiling runs: the "
                          "streaming pass reuses the forward kernel)")
@@ -386,6 +423,8 @@ def main():
     if isinstance(cfg, configs.CaptureConfig):
         run_capture(cfg, args)
         return
+    if args.dsa_select:
+        cfg = cfg.scaled(index_heads=32)
     if args.ownership != "contiguous" or args.bf16_numerator:
         cfg = cfg.scaled(ownership=args.ownership, bf16_numerator=args.bf16_numerator)
     if cfg.members > 1:

@@ -262,14 +262,14 @@ ls_status ls_dsa_index_scores(const ls_dsa_params* p, int64_t pos_begin, int64_t
  * positions is not NULL (the columns must then be in ascending position order,
  * as concatenated per-shard candidates of contiguous shards are), else
  * pos_offset + i.  Writes the selected positions in ascending order to
- * out_pos[r * k ..] and, when out_scores is not NULL, their scores to
- * out_scores[r * k ..]; when n < k the remaining entries get position -1 and
- * score -inf.  NaN scores are the caller's error.  k >= 1, ld >= n, positions
- * < 2^31.
+ * out_pos[r * out_ld ..] and, when out_scores is not NULL, their scores to
+ * out_scores[r * out_ld ..] (k entries per row); when n < k the remaining
+ * entries get position -1 and score -inf.  NaN scores are the caller's error.
+ * k >= 1, ld >= n, out_ld >= k, positions < 2^31.
  */
 ls_status ls_topk_select(const float* scores, int64_t ld, const int32_t* positions,
                          int32_t n_rows, int64_t n, int64_t pos_offset, int32_t k,
-                         int32_t* out_pos, float* out_scores, void* stream);
+                         int32_t* out_pos, float* out_scores, int64_t out_ld, void* stream);
 
 #ifdef __cplusplus
 }

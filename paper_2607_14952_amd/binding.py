@@ -99,7 +99,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
                                         c_void_p]
     lib.ls_topk_select.restype = c_int32
     lib.ls_topk_select.argtypes = [c_void_p, c_int64, c_void_p, c_int32, c_int64, c_int64, c_int32,
-                                   c_void_p, c_void_p, c_void_p]
+                                   c_void_p, c_void_p, c_int64, c_void_p]
     if lib.ls_abi_version() != ABI_VERSION:
         raise RuntimeError("liblongstraw ABI version mismatch")
     _lib = lib
@@ -355,7 +355,8 @@ def dsa_index_scores(q_index, w_index, k_index_pool, page_table, *, pos_begin: i
 def topk_select(scores, k: int, *, n: int | None = None, positions=None, pos_offset: int = 0,
                 out_pos=None, out_scores=None, stream=None):
     """ls_topk_select over the rows of ``scores`` [rows, >= n] (row stride ld):
-    positions [rows, k] int32 ascending and their scores [rows, k]."""
+    positions [rows, k] int32 ascending and their scores [rows, k] (outputs may
+    be column slices of wider arrays: their row stride is passed on)."""
     torch = _torch()
     rows = scores.shape[0]
     n = scores.shape[1] if n is None else n
@@ -363,7 +364,10 @@ def topk_select(scores, k: int, *, n: int | None = None, positions=None, pos_off
         out_pos = torch.empty((rows, k), dtype=torch.int32, device=scores.device)
     if out_scores is None:
         out_scores = torch.empty((rows, k), dtype=torch.float32, device=scores.device)
+    assert out_pos.stride(0) == out_scores.stride(0) and out_pos.stride(1) == 1
+    if positions is not None:
+        assert positions.stride(0) == scores.stride(0)
     check(load_library().ls_topk_select(_ptr(scores), scores.stride(0), _ptr(positions), rows, n,
                                         pos_offset, k, _ptr(out_pos), _ptr(out_scores),
-                                        _stream(stream)))
+                                        out_pos.stride(0), _stream(stream)))
     return out_pos, out_scores

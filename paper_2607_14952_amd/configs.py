@@ -40,6 +40,8 @@ class ReplayConfig:
     topk: int = 0
     members: int = 1           # responses replayed against one prefix pool
     block: int = 0             # rows per replay call in blockwise replay (0 = whole response)
+    index_heads: int = 0           # sparse: DSA index heads (Eq. dsa-index, width 128) selecting
+                                   # the top-k; 0 = seeded indices
     ownership: str = "contiguous"  # "contiguous" ranges or "cyclic": page p to shard p mod n_shards
     bf16_numerator: bool = False   # cross-shard merge reduces the numerator in bf16
 

@@ -663,8 +663,9 @@ LS_API ls_status ls_dsa_index_scores(const ls_dsa_params* p, int64_t pos_begin, 
 
 LS_API ls_status ls_topk_select(const float* scores, int64_t ld, const int32_t* positions,
                                 int32_t n_rows, int64_t n, int64_t pos_offset, int32_t k,
-                                int32_t* out_pos, float* out_scores, void* stream) {
-  if (k < 1 || n < 0 || n_rows < 0 || ld < n || pos_offset < 0 ||
+                                int32_t* out_pos, float* out_scores, int64_t out_ld,
+                                void* stream) {
+  if (k < 1 || n < 0 || n_rows < 0 || ld < n || out_ld < k || pos_offset < 0 ||
       pos_offset + n > (int64_t(1) << 31))
     return fail(LS_ERR_INVALID_ARG, "bad top-k shape (rows %d, n %lld, ld %lld, k %d)", n_rows,
                 (long long)n, (long long)ld, k);
@@ -673,8 +674,9 @@ LS_API ls_status ls_topk_select(const float* scores, int64_t ld, const int32_t* 
   const size_t in_bytes = n > 0 ? ((size_t)(n_rows - 1) * ld + n) * 4 : 0;
   std::vector<Range> ins{rng("scores", scores, in_bytes),
                          rng("positions", positions, positions ? in_bytes : 0)};
-  std::vector<Range> outs{rng("out_pos", out_pos, (size_t)n_rows * k * 4),
-                          rng("out_scores", out_scores, out_scores ? (size_t)n_rows * k * 4 : 0)};
+  const size_t out_bytes = ((size_t)(n_rows - 1) * out_ld + k) * 4;
+  std::vector<Range> outs{rng("out_pos", out_pos, out_bytes),
+                          rng("out_scores", out_scores, out_scores ? out_bytes : 0)};
   ls_status st = check_alias(outs, ins);
   if (st != LS_OK) return st;
   ls::TopkArgs a{};
@@ -683,6 +685,7 @@ LS_API ls_status ls_topk_select(const float* scores, int64_t ld, const int32_t* 
   a.out_pos = out_pos;
   a.out_scores = out_scores;
   a.ld = ld;
+  a.out_ld = out_ld;
   a.n = n;
   a.pos_offset = pos_offset;
   a.n_rows = n_rows;

@@ -211,8 +211,8 @@ __global__ __launch_bounds__(kKThreads) void topk_kernel(TopkArgs a) {
   const int64_t row = blockIdx.x;
   const float* x = a.scores + row * a.ld;
   const int32_t* px = a.positions ? a.positions + row * a.ld : nullptr;
-  int32_t* op = a.out_pos + row * a.k;
-  float* os = a.out_scores ? a.out_scores + row * a.k : nullptr;
+  int32_t* op = a.out_pos + row * a.out_ld;
+  float* os = a.out_scores ? a.out_scores + row * a.out_ld : nullptr;
   auto pos_of = [&](int64_t i) { return px ? px[i] : (int32_t)(a.pos_offset + i); };
 
   if (a.n <= a.k) {   // everything is selected

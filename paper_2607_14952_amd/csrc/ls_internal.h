@@ -78,9 +78,9 @@ struct DsaArgs {
 struct TopkArgs {
   const float* scores;       // [n_rows, ld]
   const int32_t* positions;  // [n_rows, ld] or null (position = pos_offset + column)
-  int32_t* out_pos;          // [n_rows, k]
-  float* out_scores;         // [n_rows, k] or null
-  int64_t ld, n, pos_offset;
+  int32_t* out_pos;          // [n_rows, out_ld], k used per row
+  float* out_scores;         // [n_rows, out_ld] or null
+  int64_t ld, out_ld, n, pos_offset;
   int32_t n_rows, k;
 };
 

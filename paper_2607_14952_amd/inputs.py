@@ -193,6 +193,17 @@ def sparse_inputs(cfg, with_dout: bool = True) -> dict:
     out = dict(q=q, latent_pool=latent, page_table=table, idx=sparse_indices(cfg))
     if with_dout:
         out["d_out"] = _dense_tensor(cfg, STREAM_DO, (R, H, cfg.head_dim_v))
+    if cfg.index_heads:
+        # index queries, head weights and one 128-wide index key per position in
+        # pages parallel to the latent pages (same table)
+        Hi = cfg.index_heads
+        out["q_index"] = to_bf16_bits(
+            _rng(cfg.seed, STREAM_IQ).standard_normal((R, Hi, 128), dtype=np.float32))
+        out["w_index"] = (_rng(cfg.seed, STREAM_IW).standard_normal((R, Hi), dtype=np.float32)
+                          / np.float32(np.sqrt(Hi)))
+        out["k_index_pool"] = to_bf16_bits(normal_chunks(
+            cfg.seed, STREAM_IK, cfg.n_phys_pages * cfg.page_size * 128).reshape(
+                cfg.n_phys_pages, cfg.page_size, 128))
     return out
 
 

@@ -201,10 +201,12 @@ def test_dsa_scores_rejects_ld_and_alias():
 
 def test_topk_rejects():
     lib = B.load_library()
-    ok = (FAKE, 1000, None, 4, 1000, 0, 16, FAKE * 64, FAKE * 96, None)
+    ok = (FAKE, 1000, None, 4, 1000, 0, 16, FAKE * 64, FAKE * 96, 16, None)
     assert lib.ls_topk_select(*ok[:6], 0, *ok[7:]) == -1                         # k = 0
-    assert lib.ls_topk_select(FAKE, 999, None, 4, 1000, 0, 16, FAKE * 64, None, None) == -1   # ld < n
+    assert lib.ls_topk_select(*ok[:9], 15, None) == -1                           # out_ld < k
+    assert lib.ls_topk_select(FAKE, 999, None, 4, 1000, 0, 16, FAKE * 64, None, 16,
+                              None) == -1                                       # ld < n
     assert lib.ls_topk_select(FAKE, 1000, None, 4, 1000, (1 << 31) - 10, 16, FAKE * 64, None,
-                              None) == -1                                       # positions >= 2^31
-    assert lib.ls_topk_select(FAKE, 1000, None, 4, 1000, 0, 16, FAKE + 64, None, None) == -4
-    assert lib.ls_topk_select(FAKE, 1000, None, 0, 1000, 0, 16, FAKE * 64, None, None) == 0
+                              16, None) == -1                                   # positions >= 2^31
+    assert lib.ls_topk_select(FAKE, 1000, None, 4, 1000, 0, 16, FAKE + 64, None, 16, None) == -4
+    assert lib.ls_topk_select(FAKE, 1000, None, 0, 1000, 0, 16, FAKE * 64, None, 16, None) == 0

@@ -140,3 +140,31 @@ def test_selection_valid_against_fp64_scores():
         mask = np.zeros(50000, bool)
         mask[sel[r]] = True
         assert ref[r][mask].min() >= ref[r][~mask].max() - 2 * tol[r]
+
+
+def test_sparse_replay_with_selection():
+    """c5's indices produced by the selection instead of seeded: the global and
+    the per-shard-candidate modes give identical indices, equal to the
+    oracle's top-k of the GPU scores, and the sparse replay over them matches
+    the oracle over the same indices."""
+    import torch
+    from paper_2607_14952_amd import configs
+    from paper_2607_14952_amd.dsa import DsaSelect
+    cfg = configs.C5.scaled(name="c5_small_dsa", prefix_len=16384, resp_len=40, topk=300,
+                            index_heads=32)
+    h = inputs.sparse_inputs(cfg)
+    dev = {k: to_device(v) for k, v in h.items()}
+    announce(f"dsa select {cfg.name}")
+    g = DsaSelect(cfg, dev, mode="global")
+    idx = g.run().clone()
+    c = DsaSelect(cfg, dev, mode="candidates", n_shards=8)
+    idx_c = c.run()
+    torch.cuda.synchronize()
+    assert np.array_equal(idx.cpu().numpy(), idx_c.cpu().numpy())
+    sc = g.scores[:, :cfg.prefix_len].cpu().numpy().astype(np.float64)
+    want = O.topk_select(sc, cfg.topk)
+    assert np.array_equal(idx.cpu().numpy(), want)
+    # sparse replay over the selected indices vs the oracle over the same indices
+    h_sel = dict(h, idx=idx.cpu().numpy())
+    from tests.test_gpu_sparse import run as sparse_run
+    sparse_run(cfg, h_sel)
