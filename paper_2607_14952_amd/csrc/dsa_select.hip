@@ -3,16 +3,18 @@
 //
 // Score kernel.  I[t, s] = sum_j w[t, j] ReLU(<q[t, j], k_s>) with H index
 // heads of width 128 and one index key per position (shared by the heads).
-// Workgroup = 4 waves = 32 tokens x a chunk of 8,192 positions; wave w holds
-// the queries of heads w H/4 .. (w+1) H/4 - 1 for the 32 tokens in registers.
+// Workgroup = 8 waves (4 for 8 or 24 heads) = 32 tokens x a chunk of 8,192
+// positions; wave w holds the queries of its H/8 (H/4) heads for the 32 tokens
+// in registers, and two waves share each SIMD.
 // Index-key tiles of 32 positions (8 KiB) stream by direct loads into a
 // four-slot LDS ring, two tiles ahead; the key operand of a tile is read once
 // per wave and reused by all of its heads.  Per tile a wave forms S^T = K Q^T
 // for each of its heads (8 MFMAs 32x32x16 over the 128-wide head, two heads'
 // chains interleaved), folds w ReLU(S) into a partial sum, and writes the
-// partial tile to LDS; after the tile barrier wave w adds the four partials of
-// tokens 8w .. 8w+7 and stores those rows of I (fp32).  Partials are double
-// buffered, so one barrier per tile serves the ring and the exchange.
+// partial tile to LDS; after the tile barrier each wave adds the waves'
+// partials for its share of the 32 token rows and stores those rows of I
+// (fp32).  Partials are double buffered, so one barrier per tile serves the
+// ring and the exchange.
 //
 // Top-k kernel.  One workgroup per row: three histogram passes over an
 // order-preserving 32-bit key of the fp32 scores (11, 11 and 10 bits) find the
@@ -40,15 +42,17 @@ constexpr int kIKAhead = 3;               // key operand reads in flight
 // 16 rows a 16-lane phase reads at one logical chunk hit 16 distinct bank groups.
 __device__ __forceinline__ int ikey_off(int r, int c) { return r * kIRow + ((c ^ (r & 15)) << 4); }
 
-// Direct loads of one key tile: wave w issues instructions i = 0, 1, each
-// 1 KiB = 4 rows; lane l writes LDS row 4(2w+i) + l/16, physical chunk l%16,
-// which holds logical chunk (l%16) ^ (row & 15).
+// Direct loads of one key tile by kWaves waves: wave w issues kFI = 8 /
+// kWaves instructions i, each 1 KiB = 4 rows; lane l writes LDS row
+// 4(kFI w + i) + l/16, physical chunk l%16, which holds logical chunk
+// (l%16) ^ (row & 15).
+template <int kFI>
 struct IKeyFetch {
-  int lds_row[2], lane_row[2], lane_off[2];
+  int lds_row[kFI], lane_row[kFI], lane_off[kFI];
   __device__ __forceinline__ void init(int lane, int w) {
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      lds_row[i] = 4 * (2 * w + i);
+    for (int i = 0; i < kFI; ++i) {
+      lds_row[i] = 4 * (kFI * w + i);
       lane_row[i] = lds_row[i] + (lane >> 4);
       lane_off[i] = ((lane & 15) ^ (lane_row[i] & 15)) << 4;
     }
@@ -67,9 +71,11 @@ struct IKeyFetch {
 // stored at chunk ^ (token & 7).
 __device__ __forceinline__ int xoff(int tok, int c) { return tok * 128 + ((c ^ (tok & 7)) << 4); }
 
-template <int kHPW>   // heads per wave (H / 4), even
-__global__ __launch_bounds__(256, 1) void dsa_score_kernel(DsaArgs a) {
-  __shared__ __attribute__((aligned(1024))) char smem[kISlots * kITile + 2 * 4 * kXWave];
+template <int kHPW, int kWaves>   // heads per wave (H / kWaves, even), waves (4 or 8)
+__global__ __launch_bounds__(64 * kWaves, 1) void dsa_score_kernel(DsaArgs a) {
+  constexpr int kFI = 8 / kWaves;          // direct loads per wave per tile
+  constexpr int kTPW = 32 / kWaves;        // output token rows per wave in the exchange
+  __shared__ __attribute__((aligned(1024))) char smem[kISlots * kITile + 2 * kWaves * kXWave];
   char* xbase = smem + kISlots * kITile;
   const int tid = threadIdx.x, lane = tid & 63;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -100,7 +106,7 @@ __global__ __launch_bounds__(256, 1) void dsa_score_kernel(DsaArgs a) {
     wv[j] = row_ok ? a.w[(int64_t)tok * a.n_heads + head] : 0.f;
   }
 
-  IKeyFetch f;
+  IKeyFetch<kFI> f;
   f.init(lane, w);
   PageLookup pl;
   pl.init(a.page_table, a.log2_page);
@@ -115,8 +121,8 @@ __global__ __launch_bounds__(256, 1) void dsa_score_kernel(DsaArgs a) {
     const int64_t t0 = tile0(i);
     const auto r = rsrc_of(phys_pos_uniform(a.page_table, t0, a.log2_page));
     const int nv = (int)min(c1 - t0, (int64_t)32);
-    f.issue(smem + i * kITile, r, 0, nv);
-    f.issue(smem + i * kITile, r, 1, nv);
+#pragma unroll
+    for (int fi = 0; fi < kFI; ++fi) f.issue(smem + i * kITile, r, fi, nv);
   }
   int32_t pe = pl.load(tile0(kIAhead));
 
@@ -126,7 +132,7 @@ __global__ __launch_bounds__(256, 1) void dsa_score_kernel(DsaArgs a) {
   for (int t = 0; t < n_tiles; ++t) {
     const char* __restrict__ kt = smem + (t % kISlots) * kITile;
     char* __restrict__ next = smem + ((t + kIAhead) % kISlots) * kITile;
-    char* __restrict__ xw = xbase + ((t & 1) * 4 + w) * kXWave;
+    char* __restrict__ xw = xbase + ((t & 1) * kWaves + w) * kXWave;
     const int64_t t0n = tile0(t + kIAhead);
     const int64_t prow_next = pl.row(pe, t0n);
     pe = pl.load(tile0(t + kIAhead + 1));
@@ -151,7 +157,7 @@ __global__ __launch_bounds__(256, 1) void dsa_score_kernel(DsaArgs a) {
               *reinterpret_cast<const bf16x8*>(kt + ikey_off(l32, 2 * (ks + kIKAhead) + hh));
         s0 = mfma32(kreg[ks], qreg[j][ks], s0);
         s1 = mfma32(kreg[ks], qreg[j + 1][ks], s1);
-        if (j == 0 && ks < 2) f.issue(next, rn, ks, nvn);
+        if (j == 0 && ks < kFI) f.issue(next, rn, ks, nvn);
         mfma_fence();
       }
 #pragma unroll
@@ -166,16 +172,17 @@ __global__ __launch_bounds__(256, 1) void dsa_score_kernel(DsaArgs a) {
       f32x4 v = {part[4 * q], part[4 * q + 1], part[4 * q + 2], part[4 * q + 3]};
       *reinterpret_cast<f32x4*>(xw + xoff(l32, 2 * q + hh)) = v;
     }
-    wait_newest_stage<2>();
+    wait_newest_stage<kFI>();
     __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0): the partial tile is in LDS
     tile_barrier();
-    // wave w: tokens 8w + lane/8, positions 4 (lane%8) .. +3 of this tile
-    {
-      const int rt = 8 * w + (lane >> 3), c = lane & 7;
-      const char* xb = xbase + (t & 1) * 4 * kXWave;
+    // wave w: tokens kTPW w + lane/8, positions 4 (lane%8) .. +3 of this tile
+    if ((lane >> 3) < kTPW) {
+      const int rt = kTPW * w + (lane >> 3), c = lane & 7;
+      const char* xb = xbase + (t & 1) * kWaves * kXWave;
       f32x4 sum = *reinterpret_cast<const f32x4*>(xb + xoff(rt, c));
 #pragma unroll
-      for (int v = 1; v < 4; ++v) sum += *reinterpret_cast<const f32x4*>(xb + v * kXWave + xoff(rt, c));
+      for (int v = 1; v < kWaves; ++v)
+        sum += *reinterpret_cast<const f32x4*>(xb + v * kXWave + xoff(rt, c));
       const int otok = tok0 + rt;
       const int64_t pos = c0 + (int64_t)t * 32 + 4 * c;
       if (otok < a.n_q) {
@@ -350,11 +357,12 @@ __global__ __launch_bounds__(kKThreads) void topk_kernel(TopkArgs a) {
 hipError_t launch_dsa_scores(const DsaArgs& a, hipStream_t stream) {
   const unsigned chunks = (unsigned)((a.pos_end - a.pos_begin + kIChunk - 1) / kIChunk);
   const dim3 grid(chunks, (unsigned)((a.n_q + 31) / 32));
+  // 16 and 32 heads: 8 waves (two per SIMD, 2 or 4 heads each); 8 and 24: 4 waves
   switch (a.n_heads) {
-    case 8: hipLaunchKernelGGL(dsa_score_kernel<2>, grid, dim3(256), 0, stream, a); break;
-    case 16: hipLaunchKernelGGL(dsa_score_kernel<4>, grid, dim3(256), 0, stream, a); break;
-    case 24: hipLaunchKernelGGL(dsa_score_kernel<6>, grid, dim3(256), 0, stream, a); break;
-    case 32: hipLaunchKernelGGL(dsa_score_kernel<8>, grid, dim3(256), 0, stream, a); break;
+    case 8: hipLaunchKernelGGL((dsa_score_kernel<2, 4>), grid, dim3(256), 0, stream, a); break;
+    case 16: hipLaunchKernelGGL((dsa_score_kernel<2, 8>), grid, dim3(512), 0, stream, a); break;
+    case 24: hipLaunchKernelGGL((dsa_score_kernel<6, 4>), grid, dim3(256), 0, stream, a); break;
+    case 32: hipLaunchKernelGGL((dsa_score_kernel<4, 8>), grid, dim3(512), 0, stream, a); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
