@@ -16,13 +16,17 @@
 // (fp32).  Partials are double buffered, so one barrier per tile serves the
 // ring and the exchange.
 //
-// Top-k kernel.  One workgroup per row: three histogram passes over an
-// order-preserving 32-bit key of the fp32 scores (11, 11 and 10 bits) find the
-// exact k-th largest key T and the count of keys above it; a collection pass
-// then keeps every key above T and the first k - above keys equal to T in
-// position order (lower position first), writing positions in ascending
-// order.  Each of the 8 waves owns a contiguous segment of the row, so the
-// order survives: wave totals are scanned once between two passes.
+// Top-k kernel.  One workgroup per row.  A histogram of the top 12 bits of an
+// order-preserving 32-bit key of the fp32 scores finds the bin holding the
+// k-th largest key.  When that bin holds at most 4,096 keys (the usual case),
+// one more pass over the row gathers them into LDS and counts the keys above
+// the bin, and the exact k-th largest key T is found among the gathered keys
+// (two 10-bit digits in LDS); otherwise two more histogram passes over the row
+// find it and a counting pass follows.  A last pass keeps every key above T
+// and the first k - above keys equal to T in position order (lower position
+// first), writing positions in ascending order: each of the 8 waves owns a
+// contiguous segment of the row, and per-segment counts set its output base.
+// The row is read three times (five when the fallback runs).
 #include "ls_internal.h"
 #include "mfma_common.h"
 
@@ -203,17 +207,50 @@ __global__ __launch_bounds__(64 * kWaves, 1) void dsa_score_kernel(DsaArgs a) {
 // ---------------------------------------------------------------- top-k
 constexpr int kKThreads = 512;
 constexpr int kKWaves = kKThreads / 64;
-constexpr int kKUnroll = 8;   // independent loads in flight per thread
+constexpr int kKUnroll = 8;    // independent loads in flight per thread
+constexpr int kKCap = 4096;    // LDS candidates of the first digit's threshold bin
 
 __device__ __forceinline__ uint32_t okey(float x) {
   const uint32_t u = __float_as_uint(x);
   return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
 }
 
+struct TopkShared {
+  uint32_t hist[4096];
+  uint32_t cand_key[kKCap];
+  int32_t cand_idx[kKCap];
+  uint32_t wave_gt[kKWaves], wave_eq[kKWaves];
+  uint32_t bin, above, count;
+};
+
+// Wave 0: the bin b of hist[0 .. nbins) holding the need-th largest (counting
+// from the top) and the number of keys in bins above it.  need >= 1 and the
+// histogram holds at least need keys.
+__device__ __forceinline__ void find_crossing(TopkShared& sh, int nbins, uint32_t need, int lane) {
+  const int per = nbins / 64;
+  uint32_t mine = 0;
+  for (int b = 0; b < per; ++b) mine += sh.hist[lane * per + b];
+  uint32_t incl = mine;   // keys in this lane's bins and above
+#pragma unroll
+  for (int d = 1; d < 64; d <<= 1) {
+    const uint32_t o = __shfl_down(incl, d);
+    if (lane + d < 64) incl += o;
+  }
+  const uint32_t excl = incl - mine;
+  if (excl < need && need <= incl) {
+    uint32_t acc = excl;
+    int b = lane * per + per - 1;
+    for (; b > lane * per; --b) {
+      if (acc + sh.hist[b] >= need) break;
+      acc += sh.hist[b];
+    }
+    sh.bin = (uint32_t)b;
+    sh.above = acc;
+  }
+}
+
 __global__ __launch_bounds__(kKThreads) void topk_kernel(TopkArgs a) {
-  __shared__ uint32_t hist[2048];
-  __shared__ uint32_t wave_gt[kKWaves], wave_eq[kKWaves];
-  __shared__ uint32_t sh_bin, sh_above;
+  __shared__ TopkShared sh;
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   const int64_t row = blockIdx.x;
   const float* x = a.scores + row * a.ld;
@@ -229,18 +266,15 @@ __global__ __launch_bounds__(kKThreads) void topk_kernel(TopkArgs a) {
     }
     return;
   }
+  // wave v owns the contiguous segment [lo, hi) in the gather and write passes
+  const int64_t seg = ((a.n + kKWaves - 1) / kKWaves + 63) / 64 * 64;
+  const int64_t lo = (int64_t)wv * seg, hi = min(a.n, lo + seg);
+  const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
 
-  // exact k-th largest key: 11 + 11 + 10 bits
-  uint32_t prefix = 0, above = 0;
-#pragma unroll 1
-  for (int pass = 0; pass < 3; ++pass) {
-    const int shift = pass == 0 ? 21 : (pass == 1 ? 10 : 0);
-    const int nbins = pass == 2 ? 1024 : 2048;
-    for (int b = tid; b < nbins; b += kKThreads) hist[b] = 0;
-    if (tid == 0) {
-      sh_bin = 0;
-      sh_above = above;
-    }
+  // histogram of a digit of the keys whose higher bits equal `prefix`
+  auto histogram = [&](int shift, int bits, int pbits, uint32_t prefix) {
+    const int nbins = 1 << bits;
+    for (int b = tid; b < nbins; b += kKThreads) sh.hist[b] = 0;
     __syncthreads();
     for (int64_t i0 = tid; i0 < a.n; i0 += kKUnroll * kKThreads) {
       float v[kKUnroll];
@@ -251,77 +285,130 @@ __global__ __launch_bounds__(kKThreads) void topk_kernel(TopkArgs a) {
       }
 #pragma unroll
       for (int u = 0; u < kKUnroll; ++u) {
-        const int64_t i = i0 + (int64_t)u * kKThreads;
         const uint32_t key = okey(v[u]);
-        const bool in = i < a.n && (pass == 0 || (key >> (shift + (pass == 1 ? 11 : 10))) == prefix);
-        if (in) atomicAdd(&hist[(key >> shift) & (nbins - 1)], 1u);
+        const bool in = i0 + (int64_t)u * kKThreads < a.n &&
+                        (pbits == 0 || (key >> (shift + bits)) == prefix);
+        if (in) atomicAdd(&sh.hist[(key >> shift) & (nbins - 1)], 1u);
       }
     }
     __syncthreads();
-    if (wv == 0) {
-      // lane owns bins [lane*per, (lane+1)*per); scan from the top
-      const int per = nbins / 64;
-      uint32_t mine = 0;
-      for (int b = 0; b < per; ++b) mine += hist[lane * per + b];
-      // suffix sum over lanes: total of lanes > lane
-      uint32_t incl = mine;
-#pragma unroll
-      for (int d = 1; d < 64; d <<= 1) {
-        const uint32_t o = __shfl_down(incl, d);
-        if (lane + d < 64) incl += o;
-      }
-      const uint32_t excl = incl - mine;   // keys in bins of higher lanes
-      const uint32_t need = (uint32_t)a.k - above;
-      // the crossing lane: excl < need <= incl
-      if (excl < need && need <= incl) {
-        uint32_t acc = excl;
-        int b = lane * per + per - 1;
-        for (; b > lane * per; --b) {
-          if (acc + hist[b] >= need) break;
-          acc += hist[b];
-        }
-        sh_bin = (uint32_t)b;
-        sh_above = above + acc;
-      }
+  };
+  auto crossing = [&](int nbins, uint32_t need) {
+    if (tid == 0) {
+      sh.bin = 0;
+      sh.above = 0;
     }
     __syncthreads();
-    prefix = (prefix << (pass == 2 ? 10 : 11)) | sh_bin;
-    above = sh_above;
+    if (wv == 0) find_crossing(sh, nbins, need, lane);
     __syncthreads();
-  }
-  const uint32_t T = prefix;
-  const uint32_t need_eq = (uint32_t)a.k - above;   // keys equal to T to keep, lowest first
+  };
 
-  // collection: wave v owns the contiguous segment [lo, hi)
-  const int64_t seg = ((a.n + kKWaves - 1) / kKWaves + 63) / 64 * 64;
-  const int64_t lo = (int64_t)wv * seg, hi = min(a.n, lo + seg);
-  const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
-  uint32_t n_gt = 0, n_eq = 0;
-  for (int64_t i0 = lo; i0 < hi; i0 += 64 * kKUnroll) {
-    float v[kKUnroll];
+  // first digit: key bits 31..20
+  histogram(20, 12, 0, 0);
+  crossing(4096, (uint32_t)a.k);
+  const uint32_t b1 = sh.bin, above1 = sh.above, in_bin = sh.hist[b1];
+  uint32_t T, gt_total;
+  if (in_bin <= (uint32_t)kKCap) {
+    // gather the bin's keys into LDS (with their columns) and count, per wave
+    // segment, the keys above the bin
+    if (tid == 0) sh.count = 0;
+    if (tid < kKWaves) sh.wave_gt[tid] = sh.wave_eq[tid] = 0;
+    __syncthreads();
+    uint32_t n_above = 0;
+    for (int64_t i0 = lo; i0 < hi; i0 += 64 * kKUnroll) {
+      float v[kKUnroll];
 #pragma unroll
-    for (int u = 0; u < kKUnroll; ++u) {
-      const int64_t i = i0 + 64 * u + lane;
-      v[u] = i < hi ? x[i] : 0.f;
-    }
+      for (int u = 0; u < kKUnroll; ++u) {
+        const int64_t i = i0 + 64 * u + lane;
+        v[u] = i < hi ? x[i] : 0.f;
+      }
 #pragma unroll
-    for (int u = 0; u < kKUnroll; ++u) {
-      const bool ok = i0 + 64 * u + lane < hi;
-      const uint32_t key = okey(v[u]);
-      n_gt += __popcll(__ballot(ok && key > T));
-      n_eq += __popcll(__ballot(ok && key == T));
+      for (int u = 0; u < kKUnroll; ++u) {
+        const int64_t i = i0 + 64 * u + lane;
+        const uint32_t key = okey(v[u]);
+        const bool ok = i < hi;
+        n_above += __popcll(__ballot(ok && (key >> 20) > b1));
+        const bool in = ok && (key >> 20) == b1;
+        const uint64_t inm = __ballot(in);
+        if (inm) {
+          uint32_t base = 0;
+          if (lane == 0) base = atomicAdd(&sh.count, (uint32_t)__popcll(inm));
+          base = __shfl(base, 0);
+          const uint32_t slot = base + (uint32_t)__popcll(inm & below);
+          if (in && slot < (uint32_t)kKCap) {
+            sh.cand_key[slot] = key;
+            sh.cand_idx[slot] = (int32_t)i;
+          }
+        }
+      }
     }
+    if (lane == 0) atomicAdd(&sh.wave_gt[wv], n_above);
+    __syncthreads();
+    const uint32_t nc = min(sh.count, (uint32_t)kKCap);
+    // the remaining 20 bits among the candidates: 10 + 10
+    for (int b = tid; b < 1024; b += kKThreads) sh.hist[b] = 0;
+    __syncthreads();
+    for (uint32_t c = tid; c < nc; c += kKThreads) atomicAdd(&sh.hist[(sh.cand_key[c] >> 10) & 1023], 1u);
+    __syncthreads();
+    crossing(1024, (uint32_t)a.k - above1);
+    const uint32_t b2 = sh.bin, above2 = sh.above;
+    for (int b = tid; b < 1024; b += kKThreads) sh.hist[b] = 0;
+    __syncthreads();
+    for (uint32_t c = tid; c < nc; c += kKThreads) {
+      const uint32_t key = sh.cand_key[c];
+      if (((key >> 10) & 1023) == b2) atomicAdd(&sh.hist[key & 1023], 1u);
+    }
+    __syncthreads();
+    crossing(1024, (uint32_t)a.k - above1 - above2);
+    T = (b1 << 20) | (b2 << 10) | sh.bin;
+    gt_total = above1 + above2 + sh.above;
+    // per wave segment: candidates above T and equal to T
+    for (uint32_t c = tid; c < nc; c += kKThreads) {
+      const uint32_t key = sh.cand_key[c];
+      const int w = (int)(sh.cand_idx[c] / seg);
+      if (key > T) atomicAdd(&sh.wave_gt[w], 1u);
+      else if (key == T) atomicAdd(&sh.wave_eq[w], 1u);
+    }
+    __syncthreads();
+  } else {
+    // many keys share the first digit: two more digits over the row, then
+    // count, per wave segment, the keys above and equal to T
+    histogram(10, 10, 12, b1);
+    crossing(1024, (uint32_t)a.k - above1);
+    const uint32_t b2 = sh.bin, above2 = sh.above;
+    histogram(0, 10, 22, (b1 << 10) | b2);
+    crossing(1024, (uint32_t)a.k - above1 - above2);
+    T = (b1 << 20) | (b2 << 10) | sh.bin;
+    gt_total = above1 + above2 + sh.above;
+    uint32_t n_gt = 0, n_eq = 0;
+    for (int64_t i0 = lo; i0 < hi; i0 += 64 * kKUnroll) {
+      float v[kKUnroll];
+#pragma unroll
+      for (int u = 0; u < kKUnroll; ++u) {
+        const int64_t i = i0 + 64 * u + lane;
+        v[u] = i < hi ? x[i] : 0.f;
+      }
+#pragma unroll
+      for (int u = 0; u < kKUnroll; ++u) {
+        const bool ok = i0 + 64 * u + lane < hi;
+        const uint32_t key = okey(v[u]);
+        n_gt += __popcll(__ballot(ok && key > T));
+        n_eq += __popcll(__ballot(ok && key == T));
+      }
+    }
+    if (lane == 0) {
+      sh.wave_gt[wv] = n_gt;
+      sh.wave_eq[wv] = n_eq;
+    }
+    __syncthreads();
   }
-  if (lane == 0) {
-    wave_gt[wv] = n_gt;
-    wave_eq[wv] = n_eq;
-  }
-  __syncthreads();
+  const uint32_t need_eq = (uint32_t)a.k - gt_total;   // keys equal to T to keep, lowest first
+
   uint32_t base = 0, eq_before = 0;
   for (int v = 0; v < wv; ++v) {
-    const uint32_t take = eq_before >= need_eq ? 0u : min(wave_eq[v], need_eq - eq_before);
-    base += wave_gt[v] + take;
-    eq_before += wave_eq[v];
+    const uint32_t take = eq_before >= need_eq ? 0u : min(sh.wave_eq[v], need_eq - eq_before);
+    base += sh.wave_gt[v] + take;
+    eq_before += sh.wave_eq[v];
   }
   uint32_t run_sel = 0, run_eq = 0;
   for (int64_t i0 = lo; i0 < hi; i0 += 64 * kKUnroll) {

@@ -88,6 +88,24 @@ def test_topk_exact_on_gpu_scores(k, quant):
     assert np.array_equal(host(val), np.take_along_axis(s_host, want, axis=1))
 
 
+def test_topk_many_ties_fallback():
+    """More than 4,096 keys in the threshold's 12-bit bin (here ~20,000 equal
+    scores) take the kernel's full-row radix path; the result still follows the
+    rule exactly (lower positions first among the equal scores)."""
+    import torch
+    g = torch.Generator(device="cuda").manual_seed(7)
+    sc = torch.zeros((6, 24000), device="cuda")
+    hi = torch.randint(0, 24000, (6, 300), device="cuda", generator=g)
+    sc.scatter_(1, hi, torch.rand((6, 300), device="cuda", generator=g) + 1.0)
+    sc[:, 5000:5010] = -1.0
+    for k in (500, 2048, 23995):
+        announce(f"topk ties k={k}")
+        pos, _ = B.topk_select(sc, k)
+        torch.cuda.synchronize()
+        want = O.topk_select(host(sc), k)
+        assert np.array_equal(host(pos), want), f"k={k}"
+
+
 def test_topk_fewer_than_k_and_offsets():
     import torch
     sc = torch.tensor([[1.0, 3.0, 2.0, 3.0, -1.0], [0.0, 0.0, 0.0, 0.0, 0.0]], device="cuda")
