@@ -32,7 +32,10 @@ constexpr int kQBM = 128;
 constexpr int kQBN = kTileKeys;                   // 32
 constexpr int kRowBytes = kD * 2;                 // 512 B: one key row
 constexpr int kQStage = 2 * kTileBytes;           // K tile + V tile (row-major, swizzled)
-constexpr int kQAhead = 2;                        // tiles in flight beyond the one consumed
+#ifndef LS_DQ_AHEAD
+#define LS_DQ_AHEAD 2
+#endif
+constexpr int kQAhead = LS_DQ_AHEAD;              // tiles in flight beyond the one consumed
 constexpr int kQSlots = kQAhead + 2;
 
 // Operand reads run a fixed number of MFMAs ahead of their use (see mfma_fence).
@@ -250,7 +253,7 @@ __global__ __launch_bounds__(256, 1) void bwd_dq_bf16_d256_kernel(BwdArgs a) {
     dq_step<kPerKey, true>(a, smem + kQAhead * kQStage, smem, smem, kf, vf, pl, pe, tile0(kQAhead),
                            tile0(kQAhead + 1), k_hi, k_lo, kb, k_all, my_lim, qreg, dreg, to, hh,
                            lse2, delta, acc, s_prev, dp_prev);
-    wait_fetch_but_newest_stage();
+    wait_vmcnt<(kQAhead - 1) * 8>();
     tile_barrier();
   }
   for (int t = 1; t < n_tiles; ++t) {
@@ -260,7 +263,7 @@ __global__ __launch_bounds__(256, 1) void bwd_dq_bf16_d256_kernel(BwdArgs a) {
                             kf, vf, pl, pe, tile0(t + kQAhead), tile0(t + kQAhead + 1), k_hi, t0,
                             kb, k_all, my_lim, qreg, dreg, to, hh, lse2, delta, acc, s_prev,
                             dp_prev);
-    wait_fetch_but_newest_stage();
+    wait_vmcnt<(kQAhead - 1) * 8>();
     tile_barrier();
   }
   {

@@ -33,8 +33,13 @@ namespace {
 constexpr int kD = 256;
 constexpr int kBN = kTileKeys;              // 32
 constexpr int kStage = 2 * kTileBytes;      // K tile + V tile
-constexpr int kAhead = 2;                   // tiles in flight beyond the one consumed
-constexpr int kSlots = kAhead + 2;          // + the tile being scored + the V of the previous one
+#ifndef LS_FWD_AHEAD8
+#define LS_FWD_AHEAD8 3
+#endif
+// Tiles in flight beyond the one consumed, and ring slots: + the tile being
+// scored, + (one wave per SIMD, pipelined across tiles) the V of the previous one.
+template <int kWaves> constexpr int kAheadOf = kWaves == 4 ? 2 : LS_FWD_AHEAD8;
+template <int kWaves> constexpr int kSlotsOf = kAheadOf<kWaves> + (kWaves == 4 ? 2 : 1);
 
 // Operand reads run a fixed number of MFMAs ahead of their use (see mfma_fence):
 // K operand reads in flight (16-byte reads) and V operands in flight (two
@@ -205,6 +210,7 @@ __device__ __forceinline__ void step(const FwdArgs& a, char* __restrict__ next,
 // share each SIMD (one's VALU and LDS work overlaps the other's MFMAs).
 template <bool kPerKey, int kWaves>
 __global__ __launch_bounds__(64 * kWaves, 1) void fwd_bf16_d256_kernel(FwdArgs a) {
+  constexpr int kAhead = kAheadOf<kWaves>, kSlots = kSlotsOf<kWaves>;
   __shared__ __attribute__((aligned(1024))) char smem[kSlots * kStage];
   constexpr int kBM = 32 * kWaves;
   constexpr int kInstr = 16 / kWaves;   // direct-load instructions per wave per 16 KiB tile
@@ -304,7 +310,7 @@ __global__ __launch_bounds__(64 * kWaves, 1) void fwd_bf16_d256_kernel(FwdArgs a
     step<kPerKey, true, kOverlap, kInstr, kAK, kAV>(
         a, smem + kAhead * kStage, smem, smem + kTileBytes, kf, vf, pl, pe, tile0(kAhead),
         tile0(kAhead + 1), k_hi, k_lo, k_lo, kb, k_all, lim_rel, qreg, to, hh, oacc, s_prev, m_run, l_run);
-    wait_newest_stage<2 * kInstr>();
+    wait_vmcnt<(kAhead - 1) * 2 * kInstr>();
     tile_barrier();
     t = 1;
   }
@@ -312,10 +318,10 @@ __global__ __launch_bounds__(64 * kWaves, 1) void fwd_bf16_d256_kernel(FwdArgs a
     const int64_t t0 = k_lo + (int64_t)t * kBN;
     step<kPerKey, false, kOverlap, kInstr, kAK, kAV>(
         a, smem + ((t + kAhead) % kSlots) * kStage, smem + (t % kSlots) * kStage,
-        smem + ((t - 1) % kSlots) * kStage + kTileBytes, kf, vf, pl, pe, tile0(t + kAhead),
+        smem + ((t + kSlots - 1) % kSlots) * kStage + kTileBytes, kf, vf, pl, pe, tile0(t + kAhead),
         tile0(t + kAhead + 1), k_hi, t0, k_lo, kb, k_all, lim_rel, qreg, to, hh, oacc, s_prev, m_run,
         l_run);
-    wait_newest_stage<2 * kInstr>();
+    wait_vmcnt<(kAhead - 1) * 2 * kInstr>();
     tile_barrier();
   }
   if (kOverlap) {

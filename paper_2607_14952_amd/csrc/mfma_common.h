@@ -355,6 +355,15 @@ __device__ __forceinline__ void wait_newest_stage() {
   __builtin_amdgcn_s_waitcnt(0x0F70 | kN);
 }
 
+// Wait until at most kN vector-memory operations of this wave are in flight
+// (0 <= kN < 64: the count's low four bits sit in bits 3:0, the high two in
+// bits 15:14; LDS and export counts are left alone).
+template <int kN>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(kN >= 0 && kN < 64, "vmcnt immediate");
+  __builtin_amdgcn_s_waitcnt(0x0F70 | (kN & 15) | ((kN >> 4) << 14));
+}
+
 // Workgroup barrier without the release/acquire fence of __syncthreads: that
 // fence counts the direct loads as LDS writes and would wait for every one in
 // flight.  The empty asm statements keep the compiler from moving memory
