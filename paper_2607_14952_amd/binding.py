@@ -342,7 +342,7 @@ def dsa_index_scores(q_index, w_index, k_index_pool, page_table, *, pos_begin: i
     n_q, H, d = q_index.shape
     n = pos_end - pos_begin
     if scores is None:
-        scores = torch.empty((n_q, max(n, 1) + (-n) % 4), dtype=torch.float32,
+        scores = torch.empty((n_q, max(4, n + (-n) % 4)), dtype=torch.float32,
                              device=q_index.device)
     p = DsaParams(q_index.data_ptr(), w_index.data_ptr(), k_index_pool.data_ptr(),
                   page_table.data_ptr(), k_index_pool.shape[0], page_table.shape[0], n_q, H, d,

@@ -42,12 +42,18 @@ constexpr int kQSlots = kQAhead + 2;
 constexpr int kSDAhead = 2;   // steps of (K row, V row) reads in flight
 constexpr int kKTAhead = 4;   // transposed K operands in flight (two reads each)
 
+#ifndef LS_DQ_KT_EARLY
+#define LS_DQ_KT_EARLY 1
+#endif
+
 // S^T = K Q^T and dP^T = V dO^T for one 32-key tile.  After step ks < 8,
-// load(ks) issues one instruction of the next stage's direct loads.
-template <typename Load, typename Valu>
+// load(ks) issues one instruction of the next stage's direct loads; after the
+// last kKTAhead steps, late(i) issues the i-th operand read of the dq product
+// that follows.
+template <typename Load, typename Valu, typename Late>
 __device__ __forceinline__ void scores_dp(const char* Ks, const char* Vs, const bf16x8* qreg,
                                           const bf16x8* dreg, const TileOffsets& o, f32x16& s,
-                                          f32x16& dp, Load&& load, Valu&& valu) {
+                                          f32x16& dp, Load&& load, Valu&& valu, Late&& late) {
   bf16x8 kr[16], vr[16];
 #pragma unroll
   for (int i = 0; i < kSDAhead; ++i) {
@@ -67,6 +73,7 @@ __device__ __forceinline__ void scores_dp(const char* Ks, const char* Vs, const 
     dp = mfma32(vr[ks], dreg[ks], dp);
     if (ks < 8) load(ks);
     valu(ks);
+    if (ks >= 16 - kKTAhead) late(ks - (16 - kKTAhead));
     mfma_fence();
   }
 }
@@ -74,14 +81,17 @@ __device__ __forceinline__ void scores_dp(const char* Ks, const char* Vs, const 
 // dq^T += K^T dS^T for one 32-key tile; dS register block kk holds keys
 // 16kk + {4h..4h+3, 8+4h..8+4h+3}, matched by the transposed K reads.
 // Operand i is dims block i/2, key half i%2.
+__device__ __forceinline__ bf16x8 dq_kt(const char* Ks, const TileOffsets& o, int i) {
+  return (i & 1) ? tile_col8(Ks, o, i >> 1, 16, 24) : tile_col8(Ks, o, i >> 1, 0, 8);
+}
+// kt0: the first kKTAhead operands, already read (or null: read them here).
 __device__ __forceinline__ void dq_update(const char* Ks, const bf16x8& d0, const bf16x8& d1,
-                                          f32x16* acc, const TileOffsets& o) {
+                                          f32x16* acc, const TileOffsets& o,
+                                          const bf16x8* kt0 = nullptr) {
   bf16x8 kt[16];
-  auto read = [&](int i) {
-    return (i & 1) ? tile_col8(Ks, o, i >> 1, 16, 24) : tile_col8(Ks, o, i >> 1, 0, 8);
-  };
+  auto read = [&](int i) { return dq_kt(Ks, o, i); };
 #pragma unroll
-  for (int i = 0; i < kKTAhead; ++i) kt[i] = read(i);
+  for (int i = 0; i < kKTAhead; ++i) kt[i] = kt0 ? kt0[i] : read(i);
 #pragma unroll
   for (int i = 0; i < 16; ++i) {
     if (i + kKTAhead < 16) kt[i + kKTAhead] = read(i + kKTAhead);
@@ -141,10 +151,15 @@ __device__ __forceinline__ void dq_step(const BwdArgs& a, char* __restrict__ nex
     if (!kFirst) ds.piece(k);
   };
   f32x16 s, dp;
+  constexpr bool kEarly = LS_DQ_KT_EARLY && !kFirst;
+  bf16x8 kt0[kKTAhead];
+  auto late = [&](int i) {
+    if (kEarly) kt0[i] = dq_kt(prev_k, to, i);
+  };
   if (kPerKey) {
     kf.issue_rows(next, a.page_table, a.log2_page, t0_next, k_hi);
     vf.issue_rows(next + kTileBytes, a.page_table, a.log2_page, t0_next, k_hi);
-    scores_dp(cur, cur + kTileBytes, qreg, dreg, to, s, dp, [](int) {}, valu);
+    scores_dp(cur, cur + kTileBytes, qreg, dreg, to, s, dp, [](int) {}, valu, late);
   } else {
     const int64_t prow_next = pl.row(pe, t0_next);
     pe = pl.load(t0_after);
@@ -154,10 +169,10 @@ __device__ __forceinline__ void dq_step(const BwdArgs& a, char* __restrict__ nex
     scores_dp(cur, cur + kTileBytes, qreg, dreg, to, s, dp, [&](int i) {
       if (i < 4) kf.issue_one(next, rk, i, nv);
       else vf.issue_one(next + kTileBytes, rv, i - 4, nv);
-    }, valu);
+    }, valu, late);
   }
   if (t0 < kb || t0 + kQBN > k_all) mask_keys(s, t0, kb, my_lim, hh);
-  if (!kFirst) dq_update(prev_k, ds.d0, ds.d1, acc, to);
+  if (!kFirst) dq_update(prev_k, ds.d0, ds.d1, acc, to, kEarly ? kt0 : nullptr);
   s_prev = s;
   dp_prev = dp;
 }
@@ -169,10 +184,15 @@ __global__ __launch_bounds__(256, 1) void bwd_dq_bf16_d256_kernel(BwdArgs a) {
   const int tid = threadIdx.x, lane = tid & 63;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave-uniform (scalar)
   const int l32 = lane & 31, hh = lane >> 5;
-  const int g = blockIdx.y;
+#if LS_XCD_MAP
+  const WorkItem wi = xcd_work_item();
+#else
+  const WorkItem wi{(int)blockIdx.x, (int)blockIdx.y, (int)blockIdx.z};
+#endif
+  const int g = wi.y;
   const int lg = a.log2_group;
   const int rows_total = a.n_q << lg;
-  const int row0 = blockIdx.x * kQBM;
+  const int row0 = wi.x * kQBM;
   const int prow = row0 + w * 32 + l32;
   const bool row_ok = prow < rows_total;
   const int tok = prow >> lg;
@@ -434,7 +454,7 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_bf16_d256_kernel(BwdArgs a, i
     __builtin_amdgcn_sched_barrier(0);
     f32x16 s, dp;
     scores_dp(cur, cur + kTileBytes, kreg, vreg, to, s, dp,
-              [&](int i) { fetch(next, row_next, i); }, [](int) {});
+              [&](int i) { fetch(next, row_next, i); }, [](int) {}, [](int) {});
     const float* st = reinterpret_cast<const float*>(cur + 2 * kTileBytes + kRStat * w);
     const int row0 = row_lo + 32 * t;
     const bool edge = a.q_pos0 + (row0 >> lg) < jw + 31 || row0 + 32 > rows_total;

@@ -220,10 +220,15 @@ __global__ __launch_bounds__(64 * kWaves, 1) void fwd_bf16_d256_kernel(FwdArgs a
   const int tid = threadIdx.x, lane = tid & 63;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave-uniform (scalar)
   const int l32 = lane & 31, hh = lane >> 5;
-  const int g = blockIdx.y, sp = blockIdx.z;
+#if LS_XCD_MAP
+  const WorkItem wi = xcd_work_item();
+#else
+  const WorkItem wi{(int)blockIdx.x, (int)blockIdx.y, (int)blockIdx.z};
+#endif
+  const int g = wi.y, sp = wi.z;
   const int lg = a.log2_group;
   const int rows_total = a.n_q << lg;
-  const int row0 = blockIdx.x * kBM;
+  const int row0 = wi.x * kBM;
   const int prow = row0 + w * 32 + l32;
   const bool row_ok = prow < rows_total;
   const int tok = prow >> lg;

@@ -2,6 +2,11 @@
 // the response-replay attention library.  Not part of the public ABI.
 #pragma once
 
+// Workgroups that share K/V tiles are mapped onto one XCD (see xcd_work_item).
+#ifndef LS_XCD_MAP
+#define LS_XCD_MAP 1
+#endif
+
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 

@@ -340,6 +340,27 @@ struct TileFetchN {
 };
 using TileFetch = TileFetchN<4>;
 
+// Work item of this workgroup.  Workgroups are dealt to the 8 XCDs round-robin
+// by linear id (XCD = id % 8), and each XCD has its own L2.  This mapping gives
+// each XCD one contiguous range of the x-fastest work order, so workgroups that
+// differ only in x (row tiles reading the same K/V of one head and key range)
+// run on one XCD and share its L2 instead of every XCD fetching every tile.
+struct WorkItem {
+  int x, y, z;
+};
+__device__ __forceinline__ WorkItem xcd_work_item() {
+  const uint32_t nx = gridDim.x, ny = gridDim.y, nz = gridDim.z;
+  const uint32_t n = nx * ny * nz;
+  const uint32_t id = blockIdx.x + nx * (blockIdx.y + ny * blockIdx.z);
+  const uint32_t xcd = id % 8, slot = id / 8, q = n / 8, r = n % 8;
+  const uint32_t w = xcd * q + min(xcd, r) + slot;   // XCD xcd's range starts at xcd q + min(xcd, r)
+  WorkItem it;
+  it.x = (int)(w % nx);
+  it.y = (int)((w / nx) % ny);
+  it.z = (int)(w / (nx * ny));
+  return it;
+}
+
 // Wait for this wave's direct loads (vmcnt = 0).
 __device__ __forceinline__ void wait_fetch() { __builtin_amdgcn_s_waitcnt(0x0F70); }
 
