@@ -3,9 +3,11 @@
 //
 // Score kernel.  I[t, s] = sum_j w[t, j] ReLU(<q[t, j], k_s>) with H index
 // heads of width 128 and one index key per position (shared by the heads).
-// Workgroup = 8 waves (4 for 8 or 24 heads) = 32 tokens x a chunk of 8,192
+// Workgroup = 8 waves (4 for 8 or 24 heads) = 32 tokens x a chunk of 16,384
 // positions; wave w holds the queries of its H/8 (H/4) heads for the 32 tokens
-// in registers, and two waves share each SIMD.
+// in registers, and two waves share each SIMD.  The token blocks of a chunk
+// are consecutive work items mapped onto one XCD, so its keys are read once
+// into that XCD's L2.
 // Index-key tiles of 32 positions (8 KiB) stream by direct loads into a
 // four-slot LDS ring, two tiles ahead; the key operand of a tile is read once
 // per wave and reused by all of its heads.  Per tile a wave forms S^T = K Q^T
@@ -38,7 +40,10 @@ constexpr int kIRow = kID * 2;            // bytes per index key
 constexpr int kITile = 32 * kIRow;        // 32 positions: 8 KiB
 constexpr int kIAhead = 2;
 constexpr int kISlots = kIAhead + 2;
-constexpr int kIChunk = 8192;             // positions per workgroup
+#ifndef LS_DSA_CHUNK
+#define LS_DSA_CHUNK 16384
+#endif
+constexpr int kIChunk = LS_DSA_CHUNK;     // positions per workgroup
 constexpr int kXWave = 32 * 32 * 4;       // one wave's partial tile (fp32)
 constexpr int kIKAhead = 3;               // key operand reads in flight
 
@@ -84,10 +89,17 @@ __global__ __launch_bounds__(64 * kWaves, 1) void dsa_score_kernel(DsaArgs a) {
   const int tid = threadIdx.x, lane = tid & 63;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int l32 = lane & 31, hh = lane >> 5;
-  const int tok0 = blockIdx.y * 32;
+  // grid x = token blocks (fastest), y = position chunks: the workgroups of one
+  // chunk read the same keys and land on one XCD together
+#if LS_XCD_MAP
+  const WorkItem wi = xcd_work_item();
+#else
+  const WorkItem wi{(int)blockIdx.x, (int)blockIdx.y, (int)blockIdx.z};
+#endif
+  const int tok0 = wi.x * 32;
   const int tok = tok0 + l32;
   const bool row_ok = tok < a.n_q;
-  const int64_t c0 = a.pos_begin + (int64_t)blockIdx.x * kIChunk;   // multiple of 32
+  const int64_t c0 = a.pos_begin + (int64_t)wi.y * kIChunk;   // multiple of 32
   const int64_t c1 = min(a.pos_end, c0 + kIChunk);
   const int n_tiles = (int)((c1 - c0 + 31) / 32);
 
@@ -443,7 +455,7 @@ __global__ __launch_bounds__(kKThreads) void topk_kernel(TopkArgs a) {
 
 hipError_t launch_dsa_scores(const DsaArgs& a, hipStream_t stream) {
   const unsigned chunks = (unsigned)((a.pos_end - a.pos_begin + kIChunk - 1) / kIChunk);
-  const dim3 grid(chunks, (unsigned)((a.n_q + 31) / 32));
+  const dim3 grid((unsigned)((a.n_q + 31) / 32), chunks);
   // 16 and 32 heads: 8 waves (two per SIMD, 2 or 4 heads each); 8 and 24: 4 waves
   switch (a.n_heads) {
     case 8: hipLaunchKernelGGL((dsa_score_kernel<2, 4>), grid, dim3(256), 0, stream, a); break;
