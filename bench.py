@@ -135,7 +135,7 @@ def bf16_numerator_cost(step, stream, reps=20):
             "lse_identical": bool(torch.equal(l16, l32))}
 
 
-def page_streaming(cfg, dev, rows=16, n_splits=128):
+def page_streaming(cfg, dev, rows=16, n_splits=256):
     """The split forward over the whole prefix with only `rows` query rows: an
     HBM-bound pass that reads every K and V row of the prefix once."""
     from paper_2607_14952_amd import binding as B

@@ -90,23 +90,42 @@ __global__ __launch_bounds__(256) void merge_kernel(const float* __restrict__ ou
   const int64_t lse_off = (int64_t)head * n_q + row;
   const int64_t part_lse = rows, part_out = rows * dv4 * 4;
 
+  // parts are read kU at a time so that their loads are in flight together
+  constexpr int kU = 8;
   float m = -INFINITY;
-  for (int s = 0; s < n_splits; ++s) m = fmaxf(m, lse_part[s * part_lse + lse_off]);
+  for (int s0 = 0; s0 < n_splits; s0 += kU) {
+    float l[kU];
+#pragma unroll
+    for (int u = 0; u < kU; ++u)
+      l[u] = s0 + u < n_splits ? lse_part[(int64_t)(s0 + u) * part_lse + lse_off] : -INFINITY;
+#pragma unroll
+    for (int u = 0; u < kU; ++u) m = fmaxf(m, l[u]);
+  }
   f32x4 acc = {0.f, 0.f, 0.f, 0.f};
   float a = 0.f;
   if (m != -INFINITY) {
     const float m2 = m * kLog2e;
     const f32x4* src = reinterpret_cast<const f32x4*>(out_part) + rh * dv4 + d4;
-    for (int s = 0; s < n_splits; ++s) {
-      const float l = lse_part[s * part_lse + lse_off];
-      const float w = __builtin_amdgcn_exp2f(fmaf(l, kLog2e, -m2));   // 0 for l = -inf
-      a += w;
-      const f32x4 o = src[s * (part_out / 4)];
-      if (BF16_NUM) {
+    for (int s0 = 0; s0 < n_splits; s0 += kU) {
+      float l[kU];
+      f32x4 o[kU];
 #pragma unroll
-        for (int e = 0; e < 4; ++e) acc[e] = round_bf16(acc[e] + round_bf16(w * o[e]));
-      } else {
-        acc += w * o;
+      for (int u = 0; u < kU; ++u) {
+        const bool in = s0 + u < n_splits;
+        l[u] = in ? lse_part[(int64_t)(s0 + u) * part_lse + lse_off] : -INFINITY;
+        o[u] = in ? src[(int64_t)(s0 + u) * (part_out / 4)] : f32x4{0.f, 0.f, 0.f, 0.f};
+      }
+#pragma unroll
+      for (int u = 0; u < kU; ++u) {
+        if (s0 + u >= n_splits) break;
+        const float w = __builtin_amdgcn_exp2f(fmaf(l[u], kLog2e, -m2));   // 0 for l = -inf
+        a += w;
+        if (BF16_NUM) {
+#pragma unroll
+          for (int e = 0; e < 4; ++e) acc[e] = round_bf16(acc[e] + round_bf16(w * o[u][e]));
+        } else {
+          acc += w * o[u];
+        }
       }
     }
     acc *= 1.0f / a;
