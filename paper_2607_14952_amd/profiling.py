@@ -2,6 +2,7 @@
 
 Usage:
   python -m paper_2607_14952_amd.profiling stats <rocprof dir> <out.md> --command "..."
+  python -m paper_2607_14952_amd.profiling util <rocprof --pmc dir> <out.md> --command "..."
   python -m paper_2607_14952_amd.profiling traffic <FETCH_SIZE dir> <WRITE_SIZE dir> <out.json>
          --calib-bytes N --command "..."
 
@@ -121,6 +122,65 @@ def counter_per_dispatch(directory: str, counter: str):
     return out
 
 
+UTIL_COUNTERS = ["SQ_INSTS_VALU_MFMA_MOPS_BF16", "SQ_VALU_MFMA_BUSY_CYCLES", "GRBM_GUI_ACTIVE",
+                 "SQ_BUSY_CYCLES", "SQ_LDS_IDX_ACTIVE", "SQ_LDS_BANK_CONFLICT"]
+N_XCD, N_CU, N_SIMD = 8, 256, 1024
+
+
+def write_util_md(directory: str, out_path: str, command: str, title: str,
+                  min_ms: float = 1.0) -> None:
+    """Per kernel (median over its dispatches longer than min_ms): the clock
+    (GRBM_GUI_ACTIVE, one count per XCD, over the dispatch time), MFMA-busy
+    share of SIMD cycles, executed bf16 MFMA work (MOPS x 512 flop) and its
+    rate, LDS-active and bank-conflict shares of CU cycles."""
+    files = _find(directory, "counter_collection.csv")
+    if not files:
+        raise FileNotFoundError(f"no counter_collection.csv under {directory}")
+    disp = defaultdict(dict)
+    meta = {}
+    with open(files[0]) as f:
+        for row in csv.DictReader(f):
+            d = _col(row, "Dispatch_Id", "DispatchId", "Correlation_Id")
+            c = _col(row, "Counter_Name", "CounterName")
+            disp[d][c] = disp[d].get(c, 0.0) + float(_col(row, "Counter_Value", "CounterValue"))
+            ns = int(_col(row, "End_Timestamp", "EndTimestamp")) - int(
+                _col(row, "Start_Timestamp", "StartTimestamp"))
+            meta[d] = (_col(row, "Kernel_Name", "KernelName", "Name"), ns)
+    per = defaultdict(list)
+    for d, c in disp.items():
+        name, ns = meta[d]
+        if ns / 1e6 >= min_ms and "GRBM_GUI_ACTIVE" in c:
+            per[name].append((ns, c))
+    lines = [f"# {title}", "", "Command (run from the repository root on one MI355X):", "",
+             "```", command, "```", "",
+             f"Kernel sources: `{source_hash()}` (sha256/16 of `paper_2607_14952_amd/csrc`).", "",
+             "Per kernel, the dispatch with the median duration among those longer than "
+             f"{min_ms} ms. The clock is GRBM_GUI_ACTIVE / {N_XCD} XCDs / duration. MFMA busy is "
+             f"SQ_VALU_MFMA_BUSY_CYCLES / ({N_SIMD} SIMDs x GUI cycles). Executed bf16 work is "
+             "SQ_INSTS_VALU_MFMA_MOPS_BF16 x 512 flop. LDS active and bank conflict are "
+             f"SQ_LDS_IDX_ACTIVE and SQ_LDS_BANK_CONFLICT / ({N_CU} CUs x GUI cycles). The "
+             "2.5 PFLOP/s peak assumes 2.4 GHz; 'peak at clock' scales it to the measured clock.",
+             "", "| kernel | dispatches | ms | clock GHz | MFMA busy % | executed TFLOP | "
+             "executed TFLOP/s | % of peak at clock | LDS active % | bank conflict % |",
+             "|---|---:|---:|---:|---:|---:|---:|---:|---:|---:|"]
+    for name, lst in sorted(per.items(), key=lambda kv: -sum(ns for ns, _ in kv[1])):
+        lst.sort(key=lambda t: t[0])
+        ns, c = lst[len(lst) // 2]
+        gui = c["GRBM_GUI_ACTIVE"] / N_XCD
+        clk = gui / ns
+        busy = 100 * c.get("SQ_VALU_MFMA_BUSY_CYCLES", 0) / (N_SIMD * gui)
+        fl = c.get("SQ_INSTS_VALU_MFMA_MOPS_BF16", 0) * 512
+        rate = fl / (ns * 1e-9) / 1e12
+        peak_clk = 2500.0 * clk / 2.4
+        lds = 100 * c.get("SQ_LDS_IDX_ACTIVE", 0) / (N_CU * gui)
+        bank = 100 * c.get("SQ_LDS_BANK_CONFLICT", 0) / (N_CU * gui)
+        lines.append(f"| `{name[:90]}` | {len(lst)} | {ns / 1e6:.3f} | {clk:.2f} | {busy:.1f} | "
+                     f"{fl / 1e12:.2f} | {rate:.0f} | {100 * rate / peak_clk:.1f} | {lds:.1f} | "
+                     f"{bank:.2f} |")
+    with open(out_path, "w") as f:
+        f.write("\n".join(lines) + "\n")
+
+
 def write_traffic(fetch_dir: str, write_dir: str, out_path: str, calib_bytes: int,
                   command: str) -> dict:
     fetch = counter_per_dispatch(fetch_dir, "FETCH_SIZE")
@@ -182,6 +242,11 @@ def main():
     a.add_argument("out")
     a.add_argument("--command", required=True)
     a.add_argument("--title", default="rocprofv3 kernel statistics")
+    u = sub.add_parser("util")
+    u.add_argument("directory")
+    u.add_argument("out")
+    u.add_argument("--command", required=True)
+    u.add_argument("--title", default="rocprofv3 MFMA and LDS utilization")
     b = sub.add_parser("traffic")
     b.add_argument("fetch_dir")
     b.add_argument("write_dir")
@@ -191,6 +256,8 @@ def main():
     args = ap.parse_args()
     if args.cmd == "stats":
         write_stats_md(args.directory, args.out, args.command, args.title)
+    elif args.cmd == "util":
+        write_util_md(args.directory, args.out, args.command, args.title)
     else:
         write_traffic(args.fetch_dir, args.write_dir, args.out, args.calib_bytes, args.command)
 
