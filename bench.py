@@ -387,8 +387,8 @@ def run_capture(cfg, args):
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=5)
-    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--config", default="c3")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-rows", type=int, default=96)
@@ -538,7 +538,9 @@ def main():
         "roofline": roofline,
         "phases_ms": {"fwd_splits": round(fwd_avg, 3), "merge": round(avg(merge_ms), 3),
                       "bwd_ranges": [round(avg([b[r] for b in bwd_ms]), 3) for r in range(n_r)],
-                      "step_events": round(avg(step_ms), 3)},
+                      "step_events": round(avg(step_ms), 3),
+                      "step_events_median": round(sorted(step_ms)[len(step_ms) // 2], 3),
+                      "step_events_min": round(min(step_ms), 3)},
         "fwd_tflops": round(fwd_tf, 2),
         "dq_tflops": round(dq_tf, 2),
         "merge_gbs": round(merge_bytes / (avg(merge_ms) * 1e-3) / 1e9, 1),
