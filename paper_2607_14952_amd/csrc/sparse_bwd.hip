@@ -31,7 +31,7 @@ constexpr int kBSlots = 3;   // ring slots: tile t is consumed in iteration t, t
 // distinct ring slots (restrict: no wait for the loads before reading `tile`).
 __device__ __forceinline__ void ds_tile(const SparseArgs& a, char* __restrict__ next,
                                         const char* __restrict__ tile, const SFetch& f,
-                                        __amdgpu_buffer_rsrc_t pool, const int32_t* pr, int w,
+                                        __amdgpu_buffer_rsrc_t pool, int32_t pr, int w,
                                         const bf16x8* qreg, const bf16x8* dreg, const SOffsets& so,
                                         int T, int n_t, int hh, float lse2, float delta,
                                         __bf16* ds_row) {
@@ -69,24 +69,22 @@ __device__ __forceinline__ void ds_tile(const SparseArgs& a, char* __restrict__ 
   f.issue(next, pool, pr, w);
 }
 
-// One dq tile: dq^T += C^T dS^T over the 9 column blocks of this wave's half,
-// the next stage's direct loads spread over the first nine MFMAs (restrict:
-// see ds_tile).
+// One dq tile: dq^T += C^T dS^T over all 18 column blocks, the next stage's
+// direct loads spread over the first nine MFMAs (restrict: see ds_tile).
 __device__ __forceinline__ void dq_tile(char* __restrict__ next, const char* __restrict__ tile,
                                         const SFetch& f, __amdgpu_buffer_rsrc_t pool,
-                                        const int32_t* pr, int w, int half, const bf16x8* d,
-                                        const SOffsets& so, f32x16* acc) {
-  bf16x8 kt[18];
+                                        int32_t pr, int w, const bf16x8* d, const SOffsets& so,
+                                        f32x16* acc) {
+  bf16x8 kt[36];
   auto read = [&](int i) {
-    const int db = 9 * half + (i >> 1);
-    return (i & 1) ? s_col8(tile, so, db, 16, 24) : s_col8(tile, so, db, 0, 8);
+    return (i & 1) ? s_col8(tile, so, i >> 1, 16, 24) : s_col8(tile, so, i >> 1, 0, 8);
   };
 #pragma unroll
   for (int i = 0; i < kSVAhead; ++i) kt[i] = read(i);
   mfma_fence();
 #pragma unroll
-  for (int i = 0; i < 18; ++i) {
-    if (i + kSVAhead < 18) kt[i + kSVAhead] = read(i + kSVAhead);
+  for (int i = 0; i < 36; ++i) {
+    if (i + kSVAhead < 36) kt[i + kSVAhead] = read(i + kSVAhead);
     acc[i >> 1] = mfma32(kt[i], d[i & 1], acc[i >> 1]);
     if (i < 9) f.issue_one(next, pool, pr, w, i);
     mfma_fence();
@@ -95,13 +93,14 @@ __device__ __forceinline__ void dq_tile(char* __restrict__ next, const char* __r
 
 // ---------------------------------------------------------------- backward, phase 1
 // dS[t][head][k] = P (dP - Delta) in bf16, P = exp2(s*c - lse2), dP = dO . v_k.
-// Workgroup = 4 waves = one token x 128 heads (wave w: heads 32w .. +31).
+// Workgroup = 4 waves = one token x 128 heads (wave w: heads 32w .. +31);
+// tokens with more keys go first.
 __global__ __launch_bounds__(256, 1) void sparse_ds_kernel(SparseArgs a) {
   __shared__ __attribute__((aligned(1024))) char smem[kBSlots * kTile];
   const int tid = threadIdx.x, lane = tid & 63;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int l32 = lane & 31, hh = lane >> 5;
-  const int t = blockIdx.x;
+  const int t = a.n_q - 1 - (int)blockIdx.x;
   const int head = blockIdx.y * 128 + w * 32 + l32;
   const int n_t = a.topk + (int)a.window0 + t + 1;
   const int n_tiles = (n_t + kKeys - 1) / kKeys;
@@ -112,12 +111,12 @@ __global__ __launch_bounds__(256, 1) void sparse_ds_kernel(SparseArgs a) {
   SFetch f;
   f.init(lane, w);
   const SOffsets so = s_offsets(lane);
-  int32_t pr[9], pn[9];
-  f.rows_of(phys_t, 0, pr);
-  f.issue(smem, pool, pr, w);
-  f.rows_of(phys_t, clamp(1), pr);
-  f.issue(smem + kTile, pool, pr, w);
-  f.rows_of(phys_t, clamp(2), pr);
+  // the row lists of the first three tiles load before any tile does, so
+  // the waits for them do not order the first two stages
+  const int32_t r0 = f.rows_of(phys_t, 0, lane), r1 = f.rows_of(phys_t, clamp(1), lane);
+  int32_t pr = f.rows_of(phys_t, clamp(2), lane), pn;
+  f.issue(smem, pool, r0, w);
+  f.issue(smem + kTile, pool, r1, w);
 
   bf16x8 qreg[36], dreg[32];
   {
@@ -136,12 +135,11 @@ __global__ __launch_bounds__(256, 1) void sparse_ds_kernel(SparseArgs a) {
   tile_barrier();
 
   for (int T = 0; T < n_tiles; ++T) {
-    f.rows_of(phys_t, clamp(T + 3), pn);
+    pn = f.rows_of(phys_t, clamp(T + 3), lane);
     __builtin_amdgcn_sched_barrier(0);   // row indices load ahead of this stage's direct loads
     ds_tile(a, smem + ((T + 2) % kBSlots) * kTile, smem + (T % kBSlots) * kTile, f, pool, pr, w,
             qreg, dreg, so, T, n_t, hh, lse2, delta, ds_row);
-#pragma unroll
-    for (int i = 0; i < 9; ++i) pr[i] = pn[i];
+    pr = pn;
     __builtin_amdgcn_s_waitcnt(0x0F79);   // vmcnt(9): only this iteration's stage may be in flight
     tile_barrier();
   }
@@ -150,18 +148,15 @@ __global__ __launch_bounds__(256, 1) void sparse_ds_kernel(SparseArgs a) {
 
 // ---------------------------------------------------------------- backward, phase 2
 // dq[t][head][d] (+)= scale * sum_k dS[t][head][k] c_k[d].  Workgroup = 4 waves
-// = 64 heads of one token (token_and_half); wave w = 2 * half + g owns heads
-// 32g .. 32g+31 of the workgroup and columns 288 * half .. +287.
+// = all 128 heads of one token (wave w: heads 32w .. +31, all 576 columns), so
+// each gathered row is fetched once per token; tokens with more keys go first.
 __global__ __launch_bounds__(256, 1) void sparse_dq_kernel(SparseArgs a) {
   __shared__ __attribute__((aligned(1024))) char smem[kBSlots * kTile];
   const int tid = threadIdx.x, lane = tid & 63;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int l32 = lane & 31, hh = lane >> 5;
-  const int g = w & 1, half = w >> 1;
-  int t, hs;
-  token_and_half(blockIdx.x, t, hs);
-  if (t >= a.n_q) return;
-  const int head = blockIdx.y * 128 + hs * 64 + g * 32 + l32;
+  const int t = a.n_q - 1 - (int)blockIdx.x;
+  const int head = blockIdx.y * 128 + w * 32 + l32;
   const int n_t = a.topk + (int)a.window0 + t + 1;
   const int n_tiles = (n_t + kKeys - 1) / kKeys;
   const __amdgpu_buffer_rsrc_t phys_t = phys_rsrc(a, t);
@@ -184,28 +179,27 @@ __global__ __launch_bounds__(256, 1) void sparse_dq_kernel(SparseArgs a) {
   SFetch f;
   f.init(lane, w);
   const SOffsets so = s_offsets(lane);
-  int32_t pr[9], pn[9];
-  f.rows_of(phys_t, 0, pr);
-  f.issue(smem, pool, pr, w);
-  f.rows_of(phys_t, clamp(1), pr);
-  f.issue(smem + kTile, pool, pr, w);
-  f.rows_of(phys_t, clamp(2), pr);
+  // the row lists of the first three tiles load before any tile does, so
+  // the waits for them do not order the first two stages
+  const int32_t r0 = f.rows_of(phys_t, 0, lane), r1 = f.rows_of(phys_t, clamp(1), lane);
+  int32_t pr = f.rows_of(phys_t, clamp(2), lane), pn;
+  f.issue(smem, pool, r0, w);
+  f.issue(smem + kTile, pool, r1, w);
   bf16x8 d[2], dn[2];
   load_ds(0, d);
-  f32x16 acc[9];
+  f32x16 acc[18];
 #pragma unroll
-  for (int i = 0; i < 9; ++i) acc[i] = zero16();
+  for (int i = 0; i < 18; ++i) acc[i] = zero16();
   wait_fetch();
   tile_barrier();
 
   for (int T = 0; T < n_tiles; ++T) {
     load_ds(clamp(T + 1), dn);
-    f.rows_of(phys_t, clamp(T + 3), pn);
+    pn = f.rows_of(phys_t, clamp(T + 3), lane);
     __builtin_amdgcn_sched_barrier(0);   // both load ahead of this stage's direct loads
-    dq_tile(smem + ((T + 2) % kBSlots) * kTile, smem + (T % kBSlots) * kTile, f, pool, pr, w, half,
-            d, so, acc);
-#pragma unroll
-    for (int i = 0; i < 9; ++i) pr[i] = pn[i];
+    dq_tile(smem + ((T + 2) % kBSlots) * kTile, smem + (T % kBSlots) * kTile, f, pool, pr, w, d,
+            so, acc);
+    pr = pn;
     d[0] = dn[0];
     d[1] = dn[1];
     __builtin_amdgcn_s_waitcnt(0x0F79);   // vmcnt(9): only this iteration's stage may be in flight
@@ -213,9 +207,9 @@ __global__ __launch_bounds__(256, 1) void sparse_dq_kernel(SparseArgs a) {
   }
   wait_fetch();
 
-  float* dq = a.dq + ((int64_t)t * a.n_heads + head) * kDk + 288 * half;
+  float* dq = a.dq + ((int64_t)t * a.n_heads + head) * kDk;
 #pragma unroll
-  for (int db = 0; db < 9; ++db) {
+  for (int db = 0; db < 18; ++db) {
 #pragma unroll
     for (int q4 = 0; q4 < 4; ++q4) {
       f32x4* dst = reinterpret_cast<f32x4*>(dq + 32 * db + 8 * q4 + 4 * hh);
@@ -242,8 +236,8 @@ hipError_t launch_sparse_bwd(const SparseArgs& a, hipStream_t stream) {
   hipLaunchKernelGGL(sparse_ds_kernel, dim3(a.n_q, a.n_heads / 128), dim3(256), 0, stream, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(sparse_dq_kernel, dim3(token_half_blocks(a.n_q), a.n_heads / 128), dim3(256),
-                     0, stream, a);
+  hipLaunchKernelGGL(sparse_dq_kernel, dim3((unsigned)a.n_q, a.n_heads / 128), dim3(256), 0, stream,
+                     a);
   return hipGetLastError();
 }
 

@@ -40,36 +40,35 @@ constexpr int kChunks = kRow / 16;            // 72
 // 4 chunks cover all 16 bank groups).
 __host__ __device__ inline int s_swz(int k) { return (((k >> 1) & 1) << 2) | ((k >> 2) & 3); }
 
-// Lane-constant LDS offsets: row operand row_off[ks & 3] + 128 * (ks >> 2);
-// transposed operand col_off[(r >> 3) & 1][db & 1] + 128 * (db >> 1) + kRow * r
-// for a row-group start r (a multiple of 8).
+// Lane-constant LDS offsets, one register each: the swizzle only flips bits
+// that the compile-time operand index selects, so the row operand of step ks
+// sits at row_off(ks & 3) + 128 * (ks >> 2) with row_off(q) = row0 ^ 32q, and
+// the transposed operand of column block db and row-group start r (a multiple
+// of 8) at col_off(r >> 3 & 1, db & 1) + 128 * (db >> 1) + kRow * r with
+// col_off(par, d) = col0[par] ^ 64d.
 struct SOffsets {
-  int row_off[4];
-  int col_off[2][2];
+  int row0;
+  int col0[2];
+  __host__ __device__ inline int row_off(int q) const { return row0 ^ (32 * q); }
+  __host__ __device__ inline int col_off(int par, int d) const { return col0[par] ^ (64 * d); }
 };
 
 __host__ __device__ inline SOffsets s_offsets(int lane) {
   SOffsets o;
   const int l32 = lane & 31, h = lane >> 5;
-  const int sw = s_swz(l32);
-#pragma unroll
-  for (int q = 0; q < 4; ++q) o.row_off[q] = l32 * kRow + (((2 * q + h) ^ sw) << 4);
+  o.row0 = l32 * kRow + ((h ^ s_swz(l32)) << 4);
   const int s = lane & 15;
   const int x = 2 * ((lane >> 4) & 1) + ((s & 3) >> 1);
   const int row = 4 * h + (s >> 2);
   const int base = row * kRow + ((s & 1) << 3);
 #pragma unroll
-  for (int par = 0; par < 2; ++par) {
-    const int swc = s_swz(row + 8 * par);
-    o.col_off[par][0] = base + ((x ^ swc) << 4);
-    o.col_off[par][1] = base + (((4 + x) ^ swc) << 4);
-  }
+  for (int par = 0; par < 2; ++par) o.col0[par] = base + ((x ^ s_swz(row + 8 * par)) << 4);
   return o;
 }
 
 // Row operand: lane supplies row l32, 16-byte chunk 2*ks + h (ks < 36).
 __device__ __forceinline__ bf16x8 s_row16(const char* tile, const SOffsets& o, int ks) {
-  return *reinterpret_cast<const bf16x8*>(tile + o.row_off[ks & 3] + 128 * (ks >> 2));
+  return *reinterpret_cast<const bf16x8*>(tile + o.row_off(ks & 3) + 128 * (ks >> 2));
 }
 
 // Transposed operand: lane l = 32h + c gets column 32*db + c of rows
@@ -77,9 +76,9 @@ __device__ __forceinline__ bf16x8 s_row16(const char* tile, const SOffsets& o, i
 __device__ __forceinline__ bf16x8 s_col8(const char* tile, const SOffsets& o, int db, int r0, int r1) {
   const char* p = tile + 128 * (db >> 1);
   const i16x4 a = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-      LS_LDS4(p + o.col_off[(r0 >> 3) & 1][db & 1] + r0 * kRow));
+      LS_LDS4(p + o.col_off((r0 >> 3) & 1, db & 1) + r0 * kRow));
   const i16x4 b = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-      LS_LDS4(p + o.col_off[(r1 >> 3) & 1][db & 1] + r1 * kRow));
+      LS_LDS4(p + o.col_off((r1 >> 3) & 1, db & 1) + r1 * kRow));
   return __builtin_bit_cast(bf16x8, __builtin_shufflevector(a, b, 0, 1, 2, 3, 4, 5, 6, 7));
 }
 
@@ -98,45 +97,75 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t phys_rsrc(const SparseArgs& a,
 
 // Direct loads of one 36 KiB tile by 4 waves (9 x 1 KiB each): lane l of
 // instruction i of wave w carries LDS chunk q = (9w + i) * 64 + l, i.e. row
-// q / 72 and physical chunk q % 72 (logical chunk permuted by s_swz).  Row and
-// chunk offsets are recomputed per instruction (a few integer ops) rather than
-// kept in registers.
+// q / 72 and physical chunk q % 72 (logical chunk permuted by s_swz).  The 64
+// chunks of one instruction lie in two consecutive rows, the first of which
+// (first_row) is the same for every lane, so one register holding the tile's
+// 32 physical rows (lane k: key row k) serves all nine instructions through
+// two lane reads and a select.  Row and chunk offsets are recomputed per
+// instruction (a few integer ops) rather than kept in registers.
 struct SFetch {
   int q0;   // (9w) * 64 + lane
   __host__ __device__ inline void init(int lane, int w) { q0 = 9 * w * 64 + lane; }
-  __host__ __device__ inline int row(int i) const { return (q0 + 64 * i) / kChunks; }
+  // (q0 passes through an empty asm so that the per-instruction offsets are
+  // recomputed where they are used instead of being hoisted out of the tile
+  // loop as 18 loop-invariant registers)
+  __host__ __device__ inline int qi(int i) const {
+    int q = q0;
+#if defined(__HIP_DEVICE_COMPILE__)
+    asm volatile("" : "+v"(q));
+#endif
+    return q + 64 * i;
+  }
+  __host__ __device__ inline int row(int i) const { return qi(i) / kChunks; }
   __host__ __device__ inline int coff(int i) const {
-    const int q = q0 + 64 * i, r = q / kChunks;
+    const int q = qi(i), r = q / kChunks;
     const int c = q - r * kChunks;
     return ((c & ~7) | ((c & 7) ^ s_swz(r))) * 16;
   }
-  // phys rows of this lane's 9 chunks for tile T, read through a buffer
-  // resource over the token's resolved key list (32-bit offsets recomputed per
-  // call instead of nine 64-bit addresses held across the loop)
-  __device__ __forceinline__ void rows_of(__amdgpu_buffer_rsrc_t phys_t, int T, int32_t* pr) const {
-#pragma unroll
-    for (int i = 0; i < 9; ++i)
-      pr[i] = __builtin_amdgcn_raw_buffer_load_b32(phys_t, (T * kKeys + row(i)) * 4, 0, 0);
+  // first key row of instruction i of wave w (its other lanes: the next row)
+  __host__ __device__ static inline int first_row(int w, int i) {
+    return (9 * w * 64 + 64 * i) / kChunks;
   }
-  __device__ __forceinline__ void issue_one(char* tile, __amdgpu_buffer_rsrc_t r, const int32_t* pr,
+  // physical rows of tile T's key rows, read through a buffer resource over
+  // the token's resolved key list: lane k and lane k + 32 hold key row k's
+  __device__ __forceinline__ int32_t rows_of(__amdgpu_buffer_rsrc_t phys_t, int T, int lane) const {
+    return __builtin_amdgcn_raw_buffer_load_b32(phys_t, (T * kKeys + (lane & 31)) * 4, 0, 0);
+  }
+  // w: the wave (uniform)
+  __device__ __forceinline__ void issue_one(char* tile, __amdgpu_buffer_rsrc_t r, int32_t rows,
                                             int w, int i) const {
-    const uint32_t off = (uint32_t)pr[i] * (uint32_t)kRow + (uint32_t)coff(i);
+    const int ra = first_row(w, i);
+    const int pa = __builtin_amdgcn_readlane(rows, ra);
+    const int pb = __builtin_amdgcn_readlane(rows, min(ra + 1, kKeys - 1));
+    const int q = qi(i), rw = q / kChunks;
+    const int c = q - rw * kChunks;
+    const int phys = rw > ra ? pb : pa;
+    const uint32_t off =
+        (uint32_t)phys * (uint32_t)kRow + (uint32_t)(((c & ~7) | ((c & 7) ^ s_swz(rw))) * 16);
     __builtin_amdgcn_raw_ptr_buffer_load_lds(r, LS_LDS(tile + (9 * w + i) * 1024), 16, (int)off, 0,
                                              0, 0);
   }
-  __device__ __forceinline__ void issue(char* tile, __amdgpu_buffer_rsrc_t r, const int32_t* pr,
+  __device__ __forceinline__ void issue(char* tile, __amdgpu_buffer_rsrc_t r, int32_t rows,
                                         int w) const {
 #pragma unroll
-    for (int i = 0; i < 9; ++i) issue_one(tile, r, pr, w, i);
+    for (int i = 0; i < 9; ++i) issue_one(tile, r, rows, w, i);
   }
 };
 
+// Online softmax step over one tile (base 2, scale c folded in) with a lazily
+// moved reference: m_run moves to the tile's row max only when that exceeds it
+// by more than kLazyLog2, so the exponentials stay below 2^kLazyLog2 and most
+// tiles leave the output accumulator unscaled (rescaling 256 accumulator
+// registers per tile would cost more than the tile's MFMAs).  The result is
+// the same softmax: l_run and the output are kept relative to the same m_run,
+// and the log-normalizer is m_run + log2(l_run).
+constexpr float kLazyLog2 = 8.f;
 __device__ __forceinline__ float softmax_step(f32x16& s, float c, float& m_run, float& l_run) {
   float mx = s[0];
 #pragma unroll
   for (int r = 1; r < 16; ++r) mx = fmaxf(mx, s[r]);
-  mx = half_max(mx);
-  const float m_new = fmaxf(m_run, mx * c);
+  mx = half_max(mx) * c;
+  const float m_new = mx > m_run + kLazyLog2 ? mx : m_run;
   const float m_use = m_new == -INFINITY ? 0.f : m_new;
   const float alpha = __builtin_amdgcn_exp2f(m_run - m_use);
   float psum = 0.f;
@@ -149,18 +178,6 @@ __device__ __forceinline__ float softmax_step(f32x16& s, float c, float& m_run, 
   m_run = m_new;
   return alpha;
 }
-
-// Workgroups own 64 heads of one token, so two workgroups share every token's
-// gathered rows.  Block b serves token (b / 16) * 8 + b % 8, head half
-// (b / 8) % 2: blocks b and b + 8 hold the two halves of one token, run on the
-// same XCD (blocks are dealt to the 8 XCDs round-robin) and are dispatched
-// back to back, so the second finds the rows in that XCD's L2.  The grid has
-// 16 * ceil(n_q / 8) blocks per 128 heads; blocks past n_q exit.
-__device__ __forceinline__ void token_and_half(int b, int& t, int& hs) {
-  t = (b >> 4) * 8 + (b & 7);
-  hs = (b >> 3) & 1;
-}
-inline unsigned token_half_blocks(int n_q) { return 16u * (unsigned)((n_q + 7) / 8); }
 
 // Operand reads run a fixed number of MFMAs ahead of their use (mfma_fence).
 constexpr int kSKAhead = 4;   // K row reads in flight

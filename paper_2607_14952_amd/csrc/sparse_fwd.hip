@@ -1,13 +1,13 @@
-// Sparse latent replay, forward.  A workgroup of 4 waves owns 64 heads of one
-// token (see token_and_half): wave w = 2 * half + g takes heads 32g .. 32g+31
-// of the workgroup (lane l: head l % 32; scores computed transposed,
-// S^T = C Q^T) and latent columns 288 * half .. +287 of the score
-// contraction.  The two halves of a head group exchange their partial score
-// tiles through LDS and sum them (the same sum in both), run the identical
-// online softmax, and wave half h accumulates output channels 256h .. +255
-// (Eq. dsa-attention over the selected rows plus the response window).
-// Gathered rows stream into a three-slot LDS ring, two tiles ahead; tile t is
-// fully consumed in iteration t.
+// Sparse latent replay, forward.  A workgroup of 4 waves owns all 128 heads of
+// one token: wave w takes heads 32w .. 32w+31 (lane l: head l % 32; scores
+// computed transposed, S^T = C Q^T) over the full 576-wide score contraction
+// and all 512 output channels (Eq. dsa-attention over the selected rows plus
+// the response window).  Each gathered row is fetched once per token, and the
+// waves need no exchange: one barrier per tile serves the ring.  Q (144
+// registers) and the output accumulator (256) stay in registers, one wave per
+// SIMD.  Gathered rows stream into a three-slot LDS ring, two tiles ahead;
+// tile t is fully consumed in iteration t.  Tokens with more keys (later
+// ones: the response window grows with t) are dispatched first.
 #include "sparse_common.h"
 
 namespace ls {
@@ -15,38 +15,16 @@ namespace {
 using namespace sparse;
 
 constexpr int kFSlots = 3;
-constexpr int kXBytes = 64 * 16 * 4;   // one wave's partial score tile
 
-// One tile.  `next` and `tile` are distinct ring slots and `xbuf` is the
-// exchange area; the restrict qualifiers tell the compiler so, which keeps it
-// from waiting for the direct loads before reading `tile`.
+// One tile.  `next` and `tile` are distinct ring slots; the restrict
+// qualifiers tell the compiler so, which keeps it from waiting for the direct
+// loads before reading `tile`.
 __device__ __forceinline__ void fwd_tile(const SparseArgs& a, char* __restrict__ next,
-                                         const char* __restrict__ tile, float* __restrict__ xbuf,
-                                         const SFetch& f, __amdgpu_buffer_rsrc_t pool,
-                                         const int32_t* pr, int w, int half, const bf16x8* qreg,
-                                         const SOffsets& so, int T, int n_t, int hh, int lane,
-                                         f32x16* oacc, float& m_run, float& l_run) {
-  // partial S^T over this wave's 18 contraction steps, the stage's loads in between
-  bf16x8 kr[18];
-#pragma unroll
-  for (int i = 0; i < kSKAhead; ++i) kr[i] = s_row16(tile, so, 18 * half + i);
-  mfma_fence();
-  f32x16 s = zero16();
-#pragma unroll
-  for (int ks = 0; ks < 18; ++ks) {
-    if (ks + kSKAhead < 18) kr[ks + kSKAhead] = s_row16(tile, so, 18 * half + ks + kSKAhead);
-    s = mfma32(kr[ks], qreg[ks], s);
-    if (ks < 9) f.issue_one(next, pool, pr, w, ks);
-    mfma_fence();
-  }
-  float* xmine = xbuf + w * (kXBytes / 4);
-  const float* xpeer = xbuf + (w ^ 2) * (kXBytes / 4);
-#pragma unroll
-  for (int r = 0; r < 16; ++r) xmine[r * 64 + lane] = s[r];
-  __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0): this wave's partial is in LDS
-  tile_barrier();
-#pragma unroll
-  for (int r = 0; r < 16; ++r) s[r] += xpeer[r * 64 + lane];
+                                         const char* __restrict__ tile, const SFetch& f,
+                                         __amdgpu_buffer_rsrc_t pool, int32_t pr, int w,
+                                         const bf16x8* qreg, const SOffsets& so, int T, int n_t,
+                                         int hh, f32x16* oacc, float& m_run, float& l_run) {
+  f32x16 s = s_scores(tile, qreg, so, [&](int i) { f.issue_one(next, pool, pr, w, i); });
   if ((T + 1) * kKeys > n_t) {
 #pragma unroll
     for (int r = 0; r < 16; ++r)
@@ -56,22 +34,18 @@ __device__ __forceinline__ void fwd_tile(const SparseArgs& a, char* __restrict__
   // (l_run < 0 never holds; it keeps the exponentials ahead of this branch)
   if (__any(alpha != 1.f || l_run < 0.f)) {
 #pragma unroll
-    for (int i = 0; i < 8; ++i) oacc[i] *= alpha;
+    for (int i = 0; i < 16; ++i) oacc[i] *= alpha;
   }
-  s_pv<8>(tile, pack8(s, 0), pack8(s, 1), oacc, so, 8 * half);
+  s_pv<16>(tile, pack8(s, 0), pack8(s, 1), oacc, so, 0);
 }
 
 __global__ __launch_bounds__(256, 1) void sparse_fwd_kernel(SparseArgs a) {
-  __shared__ __attribute__((aligned(1024))) char smem[kFSlots * kTile + 4 * kXBytes];
-  float* xbuf = reinterpret_cast<float*>(smem + kFSlots * kTile);
+  __shared__ __attribute__((aligned(1024))) char smem[kFSlots * kTile];
   const int tid = threadIdx.x, lane = tid & 63;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int l32 = lane & 31, hh = lane >> 5;
-  const int g = w & 1, half = w >> 1;
-  int t, hs;
-  token_and_half(blockIdx.x, t, hs);
-  if (t >= a.n_q) return;
-  const int head = blockIdx.y * 128 + hs * 64 + g * 32 + l32;
+  const int t = a.n_q - 1 - (int)blockIdx.x;
+  const int head = blockIdx.y * 128 + w * 32 + l32;
   const int n_t = a.topk + (int)a.window0 + t + 1;
   const int n_tiles = (n_t + kKeys - 1) / kKeys;
   const __amdgpu_buffer_rsrc_t phys_t = phys_rsrc(a, t);
@@ -83,34 +57,33 @@ __global__ __launch_bounds__(256, 1) void sparse_fwd_kernel(SparseArgs a) {
   SFetch f;
   f.init(lane, w);
   const SOffsets so = s_offsets(lane);
-  int32_t pr[9], pn[9];
-  f.rows_of(phys_t, 0, pr);
-  f.issue(smem, pool, pr, w);
-  f.rows_of(phys_t, clamp(1), pr);
-  f.issue(smem + kTile, pool, pr, w);
-  f.rows_of(phys_t, clamp(2), pr);
+  // the row lists of the first three tiles load before any tile does, so
+  // the waits for them do not order the first two stages
+  const int32_t r0 = f.rows_of(phys_t, 0, lane), r1 = f.rows_of(phys_t, clamp(1), lane);
+  int32_t pr = f.rows_of(phys_t, clamp(2), lane), pn;
+  f.issue(smem, pool, r0, w);
+  f.issue(smem + kTile, pool, r1, w);
 
-  bf16x8 qreg[18];   // Q^T operand: q[t][head][288*half + 16*ks + 8*hh .. +7]
+  bf16x8 qreg[36];   // Q^T operand: q[t][head][16*ks + 8*hh .. +7]
   {
-    const __bf16* qrow = static_cast<const __bf16*>(a.q) + ((int64_t)t * a.n_heads + head) * kDk +
-                         288 * half + hh * 8;
+    const __bf16* qrow =
+        static_cast<const __bf16*>(a.q) + ((int64_t)t * a.n_heads + head) * kDk + hh * 8;
 #pragma unroll
-    for (int ks = 0; ks < 18; ++ks) qreg[ks] = *reinterpret_cast<const bf16x8*>(qrow + ks * 16);
+    for (int ks = 0; ks < 36; ++ks) qreg[ks] = *reinterpret_cast<const bf16x8*>(qrow + ks * 16);
   }
-  f32x16 oacc[8];
+  f32x16 oacc[16];
 #pragma unroll
-  for (int i = 0; i < 8; ++i) oacc[i] = zero16();
+  for (int i = 0; i < 16; ++i) oacc[i] = zero16();
   float m_run = -INFINITY, l_run = 0.f;
   wait_fetch();
   tile_barrier();
 
   for (int T = 0; T < n_tiles; ++T) {
-    f.rows_of(phys_t, clamp(T + 3), pn);
+    pn = f.rows_of(phys_t, clamp(T + 3), lane);
     __builtin_amdgcn_sched_barrier(0);   // row indices load ahead of this stage's direct loads
-    fwd_tile(a, smem + ((T + 2) % kFSlots) * kTile, smem + (T % kFSlots) * kTile, xbuf, f, pool,
-             pr, w, half, qreg, so, T, n_t, hh, lane, oacc, m_run, l_run);
-#pragma unroll
-    for (int i = 0; i < 9; ++i) pr[i] = pn[i];
+    fwd_tile(a, smem + ((T + 2) % kFSlots) * kTile, smem + (T % kFSlots) * kTile, f, pool, pr, w,
+             qreg, so, T, n_t, hh, oacc, m_run, l_run);
+    pr = pn;
     __builtin_amdgcn_s_waitcnt(0x0F79);   // vmcnt(9): only this iteration's stage may be in flight
     tile_barrier();
   }
@@ -118,9 +91,9 @@ __global__ __launch_bounds__(256, 1) void sparse_fwd_kernel(SparseArgs a) {
 
   const float l_tot = half_sum(l_run);
   const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
-  float* out = a.out + ((int64_t)t * a.n_heads + head) * kDv + 256 * half;
+  float* out = a.out + ((int64_t)t * a.n_heads + head) * kDv;
 #pragma unroll
-  for (int db = 0; db < 8; ++db) {
+  for (int db = 0; db < 16; ++db) {
 #pragma unroll
     for (int q4 = 0; q4 < 4; ++q4) {
       f32x4 v;
@@ -131,7 +104,7 @@ __global__ __launch_bounds__(256, 1) void sparse_fwd_kernel(SparseArgs a) {
       *reinterpret_cast<f32x4*>(out + 32 * db + 8 * q4 + 4 * hh) = v;
     }
   }
-  if (hh == 0 && half == 0)
+  if (hh == 0)
     a.lse[(int64_t)head * a.n_q + t] =
         l_tot > 0.f ? (m_run + __builtin_amdgcn_logf(l_tot)) * kLn2 : -INFINITY;
 }
@@ -139,8 +112,8 @@ __global__ __launch_bounds__(256, 1) void sparse_fwd_kernel(SparseArgs a) {
 }  // namespace
 
 hipError_t launch_sparse_fwd(const SparseArgs& a, hipStream_t stream) {
-  hipLaunchKernelGGL(sparse_fwd_kernel, dim3(token_half_blocks(a.n_q), a.n_heads / 128), dim3(256),
-                     0, stream, a);
+  hipLaunchKernelGGL(sparse_fwd_kernel, dim3((unsigned)a.n_q, a.n_heads / 128), dim3(256), 0,
+                     stream, a);
   return hipGetLastError();
 }
 

@@ -147,6 +147,10 @@ static void sparse() {
           CHECK(tag[dst / 2 + e] == -1, "sparse fetch writes slot %d twice", dst / 2 + e);
           tag[dst / 2 + e] = f.row(i) * cols + f.coff(i) / 2 + e;
         }
+        CHECK(f.row(i) == SFetch::first_row(w, i) || f.row(i) == SFetch::first_row(w, i) + 1,
+              "sparse fetch row %d outside the two rows of instruction %d of wave %d", f.row(i), i, w);
+        CHECK(SFetch::first_row(w, i) + 1 < kKeys || f.row(i) == SFetch::first_row(w, i),
+              "sparse fetch of wave %d instruction %d needs a row past the tile", w, i);
       }
     }
   for (int v : tag) CHECK(v >= 0, "sparse fetch leaves a slot unwritten");
@@ -156,7 +160,7 @@ static void sparse() {
   for (int ks = 0; ks < 36; ++ks) {
     int off[64];
     for (int l = 0; l < 64; ++l) {
-      off[l] = o[l].row_off[ks & 3] + 128 * (ks >> 2);
+      off[l] = o[l].row_off(ks & 3) + 128 * (ks >> 2);
       const int row = l & 31, c0 = 16 * ks + 8 * (l >> 5);
       for (int e = 0; e < 8; ++e)
         CHECK(tag[off[l] / 2 + e] == row * cols + c0 + e, "sparse row operand ks=%d lane=%d e=%d", ks, l, e);
@@ -166,7 +170,7 @@ static void sparse() {
   for (int db = 0; db < 18; ++db)
     for (int r = 0; r < 32; r += 8) {
       int off[64];
-      for (int l = 0; l < 64; ++l) off[l] = 128 * (db >> 1) + o[l].col_off[(r >> 3) & 1][db & 1] + r * kRow;
+      for (int l = 0; l < 64; ++l) off[l] = 128 * (db >> 1) + o[l].col_off((r >> 3) & 1, db & 1) + r * kRow;
       for (int l = 0; l < 64; ++l)
         for (int j = 0; j < 4; ++j) {
           const int want = (r + 4 * (l >> 5) + j) * cols + 32 * db + (l & 31);
