@@ -209,12 +209,20 @@ def run_blockwise(cfg, args):
         torch.cuda.synchronize()
         log(f"warmup {w + 1}/{args.warmup} done")
     torch.cuda.synchronize()
+    E = lambda: torch.cuda.Event(enable_timing=True)  # noqa: E731
+    evs = [{b: (E(), E()) for b in range(cfg.blocks)} for _ in range(cfg.members)]
     t0 = time.perf_counter()
     for m in range(cfg.members):
-        rep.run_member(members[m])
+        rep.run_member(members[m], block_events=evs[m])
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     value = fl / wall / 1e12
+    blocks = {}
+    for b in range(cfg.blocks):
+        ms = sorted(evs[m][b][0].elapsed_time(evs[m][b][1]) for m in range(cfg.members))
+        bf = sum(block_flops(cfg, b))
+        blocks[str(b)] = {"median_ms": round(ms[len(ms) // 2], 2), "min_ms": round(ms[0], 2),
+                          "tflops_at_median": round(bf / (ms[len(ms) // 2] * 1e-3) / 1e12, 1)}
     print(json.dumps({
         "metric": "replay attention TFLOP/s (fwd+bwd), G blockwise members on a resident prefix",
         "value": round(value, 2), "unit": "TFLOP/s", "n_gpus": 1, "steps": 1,
@@ -225,7 +233,7 @@ def run_blockwise(cfg, args):
                                f"in a {cfg.n_phys_pages}-page pool (sampled, with free pages)",
                    "parallelism": "single-gpu"},
         "frac_of_peak": round(value / PEAK_BF16_TFLOPS, 4), "flop_per_step": fl,
-        "gpu": torch.cuda.get_device_name(0)}), flush=True)
+        "blocks": blocks, "gpu": torch.cuda.get_device_name(0)}), flush=True)
 
 
 def run_sparse(cfg, args):

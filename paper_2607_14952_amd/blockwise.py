@@ -121,12 +121,18 @@ class BlockwiseReplay:
                               dv_resp=self.dv[:kv_end - c.prefix_len], workspace=self.ws,
                               stream=self.stream)
 
-    def run_member(self, resp_dev: dict, keep=None):
-        """append -> blocks in reverse -> pop; returns (dq, dk, dv) of the member."""
+    def run_member(self, resp_dev: dict, keep=None, block_events=None):
+        """append -> blocks in reverse -> pop; returns (dq, dk, dv) of the member.
+        block_events: optional {b: (start, end)} timing events, recorded on the
+        replay's stream around each block."""
         self.prefix.append(resp_dev["k"], resp_dev["v"], stream=self.stream)
         last = self.cfg.blocks - 1
         for b in reversed(range(self.cfg.blocks)):
+            if block_events is not None:
+                block_events[b][0].record(self.stream)
             self.run_block(b, resp_dev["q"], resp_dev["d_out"], keep=keep, first=(b == last))
+            if block_events is not None:
+                block_events[b][1].record(self.stream)
         self.prefix.pop()
         return self.dq, self.dk, self.dv
 

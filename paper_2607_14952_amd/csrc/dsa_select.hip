@@ -227,13 +227,36 @@ __device__ __forceinline__ uint32_t okey(float x) {
   return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
 }
 
+// Sampled-bound path: rows of at least kFMinN keys and k <= kFMaxK, 16-byte
+// aligned.  64 sample blocks of up to 1,024 keys bound the threshold from
+// below; one pass then gathers every key at or above the bound into a
+// per-wave LDS region (in position order), and the selection is resolved
+// there.  A region overflow, or fewer than k keys at or above the bound,
+// falls back to the full-row passes.
+constexpr int64_t kFMinN = 65536;
+constexpr int kFMaxK = 4096;
+constexpr int kFCap = 1536;     // candidates per wave region
+constexpr int kFUnroll = 8;     // 16-byte loads in flight per lane
+
 struct TopkShared {
   uint32_t hist[4096];
-  uint32_t cand_key[kKCap];
-  int32_t cand_idx[kKCap];
-  uint32_t wave_gt[kKWaves], wave_eq[kKWaves];
+  union {
+    struct {
+      uint32_t cand_key[kKCap];
+      int32_t cand_idx[kKCap];
+    };
+    struct {
+      uint32_t wkey[kKWaves][kFCap];
+      int32_t widx[kKWaves][kFCap];
+    };
+  };
+  uint32_t wave_gt[kKWaves], wave_eq[kKWaves], wcount[kKWaves];
   uint32_t bin, above, count;
 };
+
+__device__ __forceinline__ float key_float(uint32_t key) {
+  return __uint_as_float((key & 0x80000000u) ? (key & 0x7FFFFFFFu) : ~key);
+}
 
 // Wave 0: the bin b of hist[0 .. nbins) holding the need-th largest (counting
 // from the top) and the number of keys in bins above it.  need >= 1 and the
@@ -314,6 +337,164 @@ __global__ __launch_bounds__(kKThreads) void topk_kernel(TopkArgs a) {
     if (wv == 0) find_crossing(sh, nbins, need, lane);
     __syncthreads();
   };
+
+  if (a.n >= kFMinN && a.k <= kFMaxK && (reinterpret_cast<uintptr_t>(x) & 15) == 0) {
+    // --- sample: 64 blocks spread over the row, 12-bit histogram
+    const int blk = (int)min<int64_t>(1024, max<int64_t>(256, (a.n / 512) / 256 * 256));
+    for (int b = tid; b < 4096; b += kKThreads) sh.hist[b] = 0;
+    __syncthreads();
+    for (int j = wv; j < 64; j += kKWaves) {
+      const int64_t start = ((int64_t)j * a.n / 64) & ~int64_t(3);
+      for (int c0 = 0; c0 < blk; c0 += 256) {
+        const int64_t i = start + c0 + 4 * lane;
+        if (i + 3 < a.n) {
+          const f32x4 v = *reinterpret_cast<const f32x4*>(x + i);
+#pragma unroll
+          for (int c = 0; c < 4; ++c) atomicAdd(&sh.hist[okey(v[c]) >> 20], 1u);
+        }
+      }
+    }
+    __syncthreads();
+    // samples actually read: blocks whose 4-key groups lie inside the row
+    uint32_t n_s = 0;
+    for (int b = tid; b < 4096; b += kKThreads) n_s += sh.hist[b];
+    n_s = __reduce_add_sync(~0ull, n_s);
+    if (lane == 0) sh.wave_gt[wv] = n_s;
+    __syncthreads();
+    n_s = 0;
+    for (int v = 0; v < kKWaves; ++v) n_s += sh.wave_gt[v];
+    // bound: the bin where the sample count from the top reaches twice the
+    // count expected above the k-th key (at least 16)
+    const double want = 2.0 * (double)a.k * (double)n_s / (double)a.n;
+    const uint32_t need_s = (uint32_t)min<double>((double)n_s, max<double>(16.0, ceil(want)));
+    uint32_t lkey = 0;
+    if (need_s >= 1) {
+      crossing(4096, need_s);
+      lkey = sh.bin << 20;
+    }
+    // --- one pass: wave v gathers its segment's keys >= lkey, in position order
+    const int64_t fseg = ((a.n + kKWaves - 1) / kKWaves + 255) / 256 * 256;
+    const int64_t flo = (int64_t)wv * fseg, fhi = min(a.n, flo + fseg);
+    uint32_t wcount = 0;
+    for (int64_t i0 = flo; i0 < fhi && wcount <= (uint32_t)kFCap; i0 += 256 * kFUnroll) {
+      f32x4 v[kFUnroll];
+#pragma unroll
+      for (int u = 0; u < kFUnroll; ++u) {
+        const int64_t i = i0 + 256 * u + 4 * lane;
+        if (i + 3 < fhi) {
+          v[u] = *reinterpret_cast<const f32x4*>(x + i);
+        } else {
+#pragma unroll
+          for (int c = 0; c < 4; ++c) v[u][c] = i + c < fhi ? x[i + c] : -INFINITY;
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < kFUnroll; ++u) {
+        const int64_t i = i0 + 256 * u + 4 * lane;
+        uint32_t key[4];
+        bool in[4];
+        uint32_t cnt = 0;
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+          key[c] = okey(v[u][c]);
+          in[c] = i + c < fhi && key[c] >= lkey;
+          cnt += in[c] ? 1u : 0u;
+        }
+        // exclusive prefix of the per-lane counts (0..4) over the lanes
+        const uint64_t m0 = __ballot(cnt & 1), m1 = __ballot(cnt & 2), m2 = __ballot(cnt & 4);
+        const uint32_t pre = (uint32_t)(__popcll(m0 & below) + 2 * __popcll(m1 & below) +
+                                        4 * __popcll(m2 & below));
+        uint32_t slot = wcount + pre;
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+          if (in[c]) {
+            if (slot < (uint32_t)kFCap) {
+              sh.wkey[wv][slot] = key[c];
+              sh.widx[wv][slot] = (int32_t)(i + c);
+            }
+            ++slot;
+          }
+        }
+        wcount += (uint32_t)(__popcll(m0) + 2 * __popcll(m1) + 4 * __popcll(m2));
+      }
+    }
+    if (lane == 0) sh.wcount[wv] = wcount;
+    __syncthreads();
+    uint32_t total = 0;
+    bool fits = true;
+    for (int v = 0; v < kKWaves; ++v) {
+      total += sh.wcount[v];
+      fits = fits && sh.wcount[v] <= (uint32_t)kFCap;
+    }
+    if (fits && total >= (uint32_t)a.k) {
+      // every key >= lkey is a candidate, so counts among them are exact
+      auto cand_hist = [&](int shift, int bits, int pbits, uint32_t prefix) {
+        for (int b = tid; b < (1 << bits); b += kKThreads) sh.hist[b] = 0;
+        __syncthreads();
+        for (int t = tid; t < kKWaves * kFCap; t += kKThreads) {
+          const int r = t / kFCap, j = t - r * kFCap;
+          if ((uint32_t)j < sh.wcount[r]) {
+            const uint32_t key = sh.wkey[r][j];
+            if (pbits == 0 || (key >> (shift + bits)) == prefix)
+              atomicAdd(&sh.hist[(key >> shift) & ((1u << bits) - 1)], 1u);
+          }
+        }
+        __syncthreads();
+      };
+      cand_hist(20, 12, 0, 0);
+      crossing(4096, (uint32_t)a.k);
+      const uint32_t c1 = sh.bin, ab1 = sh.above;
+      cand_hist(10, 10, 12, c1);
+      crossing(1024, (uint32_t)a.k - ab1);
+      const uint32_t c2 = sh.bin, ab2 = sh.above;
+      cand_hist(0, 10, 22, (c1 << 10) | c2);
+      crossing(1024, (uint32_t)a.k - ab1 - ab2);
+      const uint32_t Tf = (c1 << 20) | (c2 << 10) | sh.bin;
+      const uint32_t need_eq_f = (uint32_t)a.k - (ab1 + ab2 + sh.above);
+      // per wave region: keys above and equal to the threshold
+      uint32_t g = 0, e = 0;
+      for (uint32_t j = lane; j < wcount; j += 64) {
+        const uint32_t key = sh.wkey[wv][j];
+        g += key > Tf ? 1u : 0u;
+        e += key == Tf ? 1u : 0u;
+      }
+      g = __reduce_add_sync(~0ull, g);
+      e = __reduce_add_sync(~0ull, e);
+      if (lane == 0) {
+        sh.wave_gt[wv] = g;
+        sh.wave_eq[wv] = e;
+      }
+      __syncthreads();
+      uint32_t fbase = 0, feq_before = 0;
+      for (int v = 0; v < wv; ++v) {
+        const uint32_t take =
+            feq_before >= need_eq_f ? 0u : min(sh.wave_eq[v], need_eq_f - feq_before);
+        fbase += sh.wave_gt[v] + take;
+        feq_before += sh.wave_eq[v];
+      }
+      uint32_t run_sel = 0, run_eq = 0;
+      for (uint32_t j0 = 0; j0 < wcount; j0 += 64) {
+        const uint32_t j = j0 + lane;
+        const bool ok = j < wcount;
+        const uint32_t key = ok ? sh.wkey[wv][j] : 0u;
+        const bool gt = ok && key > Tf, eq = ok && key == Tf;
+        const uint64_t eqm = __ballot(eq);
+        const uint32_t eq_rank = feq_before + run_eq + (uint32_t)__popcll(eqm & below);
+        const bool sel = gt || (eq && eq_rank < need_eq_f);
+        const uint64_t selm = __ballot(sel);
+        const uint32_t o = fbase + run_sel + (uint32_t)__popcll(selm & below);
+        if (sel && o < (uint32_t)a.k) {
+          const int32_t i = sh.widx[wv][j];
+          op[o] = pos_of(i);
+          if (os) os[o] = key_float(key);
+        }
+        run_sel += (uint32_t)__popcll(selm);
+        run_eq += (uint32_t)__popcll(eqm);
+      }
+      return;
+    }
+    __syncthreads();   // (the full-row passes reuse the LDS)
+  }
 
   // first digit: key bits 31..20
   histogram(20, 12, 0, 0);

@@ -106,6 +106,60 @@ def test_topk_many_ties_fallback():
         assert np.array_equal(host(pos), want), f"k={k}"
 
 
+def _check_topk(sc, k, what):
+    import torch
+    announce(f"topk {what} k={k} shape={tuple(sc.shape)}")
+    pos, val = B.topk_select(sc, k)
+    torch.cuda.synchronize()
+    s_host = host(sc)
+    want = O.topk_select(s_host.astype(np.float64), k)
+    assert np.array_equal(host(pos), want), what
+    assert np.array_equal(host(val).view(np.uint32),
+                          np.take_along_axis(s_host, want, axis=1).view(np.uint32)), what
+
+
+@pytest.mark.parametrize("k", [1, 64, 2048, 4096])
+def test_topk_sampled_bound_path(k):
+    """Rows of at least 65,536 keys take the sampled-bound path (one pass over
+    the row); the selection follows the rule exactly."""
+    import torch
+    g = torch.Generator(device="cuda").manual_seed(100 + k)
+    _check_topk(torch.randn((5, 200000), device="cuda", generator=g), k, "sampled bound")
+
+
+def test_topk_sampled_bound_ties():
+    """Scores quantized to quarter steps: thousands of keys equal the
+    threshold, which the sampled-bound path resolves by lower position."""
+    import torch
+    g = torch.Generator(device="cuda").manual_seed(11)
+    sc = torch.round(torch.randn((4, 131072), device="cuda", generator=g) * 4) / 4
+    for k in (2048, 4096):
+        _check_topk(sc, k, "sampled ties")
+
+
+def test_topk_sampled_bound_fallbacks():
+    """The exact full-row passes take over (same result) when (a) the sampled
+    bound lies too high: the sample blocks hold log-uniform large values that
+    the rest of the row never reaches, so fewer than k keys clear the bound;
+    (b) one wave's segment holds more candidates than its LDS region (every
+    large key in the first eighth of the row); (c) rows are not 16-byte
+    aligned (odd leading dimension)."""
+    import torch
+    g = torch.Generator(device="cuda").manual_seed(12)
+    n = 131072
+    sc = torch.randn((3, n), device="cuda", generator=g)
+    # sample blocks of a 131,072-key row: 64 blocks of 256 keys at 2,048 j
+    blocks = (torch.arange(64, device="cuda")[:, None] * 2048 +
+              torch.arange(256, device="cuda")[None, :]).reshape(-1)
+    sc[:, blocks] = torch.exp2(torch.rand((3, blocks.numel()), device="cuda", generator=g) * 20)
+    _check_topk(sc, 2048, "bound too high")
+    sc = torch.randn((3, n), device="cuda", generator=g)
+    sc[:, : n // 8] += 10.0
+    _check_topk(sc, 2048, "region overflow")
+    sc = torch.randn((3, n + 1), device="cuda", generator=g)[:, :n]   # leading dimension n + 1
+    _check_topk(sc, 2048, "unaligned rows")
+
+
 def test_topk_fewer_than_k_and_offsets():
     import torch
     sc = torch.tensor([[1.0, 3.0, 2.0, 3.0, -1.0], [0.0, 0.0, 0.0, 0.0, 0.0]], device="cuda")
