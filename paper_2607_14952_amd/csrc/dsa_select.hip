@@ -234,8 +234,8 @@ __device__ __forceinline__ uint32_t okey(float x) {
 // there.  A region overflow, or fewer than k keys at or above the bound,
 // falls back to the full-row passes.
 constexpr int64_t kFMinN = 65536;
-constexpr int kFMaxK = 4096;
-constexpr int kFCap = 1536;     // candidates per wave region
+constexpr int kFMaxK = 2048;
+constexpr int kFCap = 1000;     // candidates per wave region (LDS <= 80 KiB: two rows per CU)
 constexpr int kFUnroll = 8;     // 16-byte loads in flight per lane
 
 struct TopkShared {
@@ -253,6 +253,8 @@ struct TopkShared {
   uint32_t wave_gt[kKWaves], wave_eq[kKWaves], wcount[kKWaves];
   uint32_t bin, above, count;
 };
+
+static_assert(sizeof(TopkShared) <= 80 * 1024, "two top-k workgroups per CU");
 
 __device__ __forceinline__ float key_float(uint32_t key) {
   return __uint_as_float((key & 0x80000000u) ? (key & 0x7FFFFFFFu) : ~key);
@@ -339,22 +341,29 @@ __global__ __launch_bounds__(kKThreads) void topk_kernel(TopkArgs a) {
   };
 
   if (a.n >= kFMinN && a.k <= kFMaxK && (reinterpret_cast<uintptr_t>(x) & 15) == 0) {
-    // --- sample: 64 blocks spread over the row, 12-bit histogram
+    // --- sample: 64 blocks spread over the row; digit histograms of their keys
     const int blk = (int)min<int64_t>(1024, max<int64_t>(256, (a.n / 512) / 256 * 256));
-    for (int b = tid; b < 4096; b += kKThreads) sh.hist[b] = 0;
-    __syncthreads();
-    for (int j = wv; j < 64; j += kKWaves) {
-      const int64_t start = ((int64_t)j * a.n / 64) & ~int64_t(3);
-      for (int c0 = 0; c0 < blk; c0 += 256) {
-        const int64_t i = start + c0 + 4 * lane;
-        if (i + 3 < a.n) {
-          const f32x4 v = *reinterpret_cast<const f32x4*>(x + i);
+    auto sample_hist = [&](int shift, int bits, int pbits, uint32_t prefix) {
+      for (int b = tid; b < (1 << bits); b += kKThreads) sh.hist[b] = 0;
+      __syncthreads();
+      for (int j = wv; j < 64; j += kKWaves) {
+        const int64_t start = ((int64_t)j * a.n / 64) & ~int64_t(3);
+        for (int c0 = 0; c0 < blk; c0 += 256) {
+          const int64_t i = start + c0 + 4 * lane;
+          if (i + 3 < a.n) {
+            const f32x4 v = *reinterpret_cast<const f32x4*>(x + i);
 #pragma unroll
-          for (int c = 0; c < 4; ++c) atomicAdd(&sh.hist[okey(v[c]) >> 20], 1u);
+            for (int c = 0; c < 4; ++c) {
+              const uint32_t key = okey(v[c]);
+              if (pbits == 0 || (key >> (shift + bits)) == prefix)
+                atomicAdd(&sh.hist[(key >> shift) & ((1u << bits) - 1)], 1u);
+            }
+          }
         }
       }
-    }
-    __syncthreads();
+      __syncthreads();
+    };
+    sample_hist(20, 12, 0, 0);
     // samples actually read: blocks whose 4-key groups lie inside the row
     uint32_t n_s = 0;
     for (int b = tid; b < 4096; b += kKThreads) n_s += sh.hist[b];
@@ -363,14 +372,17 @@ __global__ __launch_bounds__(kKThreads) void topk_kernel(TopkArgs a) {
     __syncthreads();
     n_s = 0;
     for (int v = 0; v < kKWaves; ++v) n_s += sh.wave_gt[v];
-    // bound: the bin where the sample count from the top reaches twice the
-    // count expected above the k-th key (at least 16)
+    // bound: the sample key, to 22 bits, at which the sample count from the
+    // top reaches twice the count expected above the k-th key (at least 16)
     const double want = 2.0 * (double)a.k * (double)n_s / (double)a.n;
     const uint32_t need_s = (uint32_t)min<double>((double)n_s, max<double>(16.0, ceil(want)));
     uint32_t lkey = 0;
     if (need_s >= 1) {
       crossing(4096, need_s);
-      lkey = sh.bin << 20;
+      const uint32_t s1 = sh.bin, sa1 = sh.above;
+      sample_hist(10, 10, 12, s1);
+      crossing(1024, need_s - sa1);
+      lkey = (s1 << 20) | (sh.bin << 10);
     }
     // --- one pass: wave v gathers its segment's keys >= lkey, in position order
     const int64_t fseg = ((a.n + kKWaves - 1) / kKWaves + 255) / 256 * 256;

@@ -118,10 +118,11 @@ def _check_topk(sc, k, what):
                           np.take_along_axis(s_host, want, axis=1).view(np.uint32)), what
 
 
-@pytest.mark.parametrize("k", [1, 64, 2048, 4096])
+@pytest.mark.parametrize("k", [1, 64, 1000, 2048, 4096])
 def test_topk_sampled_bound_path(k):
-    """Rows of at least 65,536 keys take the sampled-bound path (one pass over
-    the row); the selection follows the rule exactly."""
+    """Rows of at least 65,536 keys with k <= 2,048 take the sampled-bound path
+    (one pass over the row); k = 4,096 takes the full-row passes.  The
+    selection follows the rule exactly either way."""
     import torch
     g = torch.Generator(device="cuda").manual_seed(100 + k)
     _check_topk(torch.randn((5, 200000), device="cuda", generator=g), k, "sampled bound")
@@ -133,7 +134,7 @@ def test_topk_sampled_bound_ties():
     import torch
     g = torch.Generator(device="cuda").manual_seed(11)
     sc = torch.round(torch.randn((4, 131072), device="cuda", generator=g) * 4) / 4
-    for k in (2048, 4096):
+    for k in (1024, 2048):
         _check_topk(sc, k, "sampled ties")
 
 
