@@ -100,8 +100,13 @@ def measured_ceilings():
 
 
 def gpu_clocks():
-    """Current shader / memory clocks as rocm-smi reports them (None when unavailable)."""
+    """Current shader / memory clocks as rocm-smi reports them (None when unavailable).
+    Skipped under rocprofv3 (its ROCPROF_* variables are set): with counter
+    collection the profiler initialises the GPU in every child process too, and
+    rocm-smi starts through an interpreter that its launcher execs."""
     import subprocess
+    if any(k.startswith("ROCPROF_") for k in os.environ):
+        return None
     try:
         r = subprocess.run(["rocm-smi", "--showclocks", "--json"], stdout=subprocess.PIPE,
                            stderr=subprocess.DEVNULL, text=True, timeout=20)

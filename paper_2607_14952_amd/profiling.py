@@ -186,15 +186,21 @@ def write_traffic(fetch_dir: str, write_dir: str, out_path: str, calib_bytes: in
     fetch = counter_per_dispatch(fetch_dir, "FETCH_SIZE")
     write = counter_per_dispatch(write_dir, "WRITE_SIZE")
 
-    def calib(per):
-        cands = [(k, v) for k, v in per.items() if COPY_KERNEL_HINT in k.lower()]
-        if not cands:
+    # The calibration copy is the copy dispatch whose WRITE_SIZE is closest to
+    # calib_bytes (the write counter reads copies exactly); the FETCH run
+    # dispatches the same kernels in the same order, so the same index is used.
+    def copies(per):
+        c = [(k, v) for k, v in per.items() if COPY_KERNEL_HINT in k.lower()]
+        if not c:
             raise RuntimeError("calibration copy kernel not found in the counter output")
-        k, v = max(cands, key=lambda kv: max(kv[1]))
-        return k, max(v)
+        return c[0]
 
-    ck_f, cf = calib(fetch)
-    ck_w, cw = calib(write)
+    ck_w, wv = copies(write)
+    ck_f, fv = copies(fetch)
+    j = min(range(len(wv)), key=lambda i: abs(wv[i] * 1024.0 - calib_bytes))
+    if j >= len(fv):
+        raise RuntimeError("the FETCH run has fewer copy dispatches than the WRITE run")
+    cf, cw = fv[j], wv[j]
     scale_f = calib_bytes / (cf * 1024.0)
     scale_w = calib_bytes / (cw * 1024.0)
     kernels = {}
