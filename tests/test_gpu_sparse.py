@@ -70,6 +70,14 @@ def test_sparse_window_only_and_offset_rows():
     run(cfg2, h2, q_pos0=cfg2.prefix_len + 50)
 
 
+def test_sparse_two_head_groups():
+    """256 query heads: two workgroups per token (grid y = head group), each
+    over its own 128 heads of the shared latent rows; a response length that
+    is not a multiple of anything the kernels tile by."""
+    cfg = SMALL.scaled(name="c5_256h", n_q_heads=256, resp_len=23, topk=97)
+    run(cfg, inputs.sparse_inputs(cfg))
+
+
 @pytest.mark.timeout(900)
 def test_c5_full_size_sampled():
     cfg = configs.C5
