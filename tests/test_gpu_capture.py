@@ -72,3 +72,45 @@ def test_capture_small():
     unused = sorted(set(range(cfg.n_phys_pages)) - set(h["page_table"].tolist()))
     assert unused, "the pool has spare pages"
     assert not bool(cap.k_pool[unused].any()) and not bool(cap.v_pool[unused].any())
+
+
+@pytest.mark.timeout(900)
+def test_capture_2m_sampled():
+    """The full 2,097,152-position capture (512 chunks of 4,096, the
+    benchmark's configuration): sampled rows of chunks at three depths (about
+    4K, 262K and 2M visible keys) against the oracle's attention at their own
+    positions, and the stored K/V bit for bit at sampled positions."""
+    import torch
+    cfg = configs.CAPTURE_2M
+    announce("capture 2m: inputs")
+    h = inputs.capture_inputs(cfg)
+    dev = {k: to_device(v) for k, v in h.items()}
+    cap = PrefixCapture(cfg, dev)
+    keep = {0: [0, 4095], 64: [0, 2047], cfg.n_chunks - 1: [1, 4095]}
+    saved = {}
+    o = torch.empty((cfg.chunk, cfg.n_q_heads, cfg.head_dim), dtype=torch.bfloat16, device="cuda")
+    for c in range(cfg.n_chunks):
+        if c % 128 == 0:
+            announce(f"capture 2m: chunk {c}")
+        b, e = cfg.chunk_range(c)
+        cap.chunk(c, out=o[:e - b])
+        if c in keep:
+            r = keep[c]
+            saved[c] = (host(o[r]), host(cap.lse[:, r]))
+    torch.cuda.synchronize()
+    kp, tbl = _dense_pool(h["k"], cfg.page_size)
+    vp, _ = _dense_pool(h["v"], cfg.page_size)
+    for c, rows in keep.items():
+        b, _ = cfg.chunk_range(c)
+        for j, r in enumerate(rows):
+            announce(f"capture 2m: oracle row {b + r}")
+            q = h["q_blocks"][c % cfg.n_q_blocks][r][None]
+            o_ref, l_ref = O.attn_fwd(q, kp, vp, tbl, page_size=cfg.page_size, q_pos0=b + r,
+                                      scale=cfg.scale)
+            got_o, got_l = saved[c]
+            assert rel_l2(got_o[j][None], o_ref) <= TOL_BF16["out"], f"row {b + r} out"
+            assert lse_err(got_l[:, j:j + 1], l_ref) <= TOL_BF16["lse"], f"row {b + r} lse"
+    pos = np.array([0, 4095, 4096, 1_048_575, cfg.length - 1])
+    k, v = B.gather_kv(cap.kv, 0, cfg.length)
+    as_bits = lambda t: t.view(torch.int16).cpu().numpy().view(np.uint16)  # noqa: E731
+    assert np.array_equal(as_bits(k[pos]), h["k"][pos]) and np.array_equal(as_bits(v[pos]), h["v"][pos])
