@@ -241,3 +241,47 @@ def test_sparse_replay_with_selection():
     h_sel = dict(h, idx=idx.cpu().numpy())
     from tests.test_gpu_sparse import run as sparse_run
     sparse_run(cfg, h_sel)
+
+
+@pytest.mark.timeout(900)
+def test_dsa_c5_full_size_sampled():
+    """c5's selection at full size (2,048 tokens x 2,097,152 positions, 32
+    index heads, top-2,048; the sampled-bound top-k path on real index
+    scores): sampled rows' scores against the fp64 oracle, their selection
+    equal to the oracle's rule on the GPU scores and valid against the fp64
+    scores, and the per-shard candidate mode equal to the global one."""
+    import torch
+    from paper_2607_14952_amd import configs
+    from paper_2607_14952_amd.dsa import DsaSelect
+    cfg = configs.C5.scaled(index_heads=32)
+    announce("dsa c5: inputs")
+    h = inputs.sparse_inputs(cfg)
+    dev = {k: to_device(h[k]) for k in ("q_index", "w_index", "k_index_pool", "page_table")}
+    announce("dsa c5: global selection")
+    g = DsaSelect(cfg, dev, mode="global")
+    idx = g.run().clone()
+    announce("dsa c5: candidate selection")
+    idx_c = DsaSelect(cfg, dev, mode="candidates", n_shards=8).run()
+    torch.cuda.synchronize()
+    assert np.array_equal(host(idx), host(idx_c)), "candidates == global"
+    rows = [0, 1, 1000, cfg.resp_len - 1]
+    P = cfg.prefix_len
+    sc = host(g.scores[rows, :P])
+    want = O.topk_select(sc.astype(np.float64), cfg.topk)
+    assert np.array_equal(host(idx)[rows], want), "selection == the rule on the GPU scores"
+    announce("dsa c5: oracle scores for the sampled rows")
+    hr = dict(h, q_index=h["q_index"][rows], w_index=h["w_index"][rows])
+    ref = O.dsa_index_scores(hr["q_index"], hr["w_index"], h["k_index_pool"], h["page_table"],
+                             page_size=cfg.page_size, pos_begin=0, pos_end=P)
+    # sum_j |w_j| |q_j . k_s| per row, with matrix products (2M positions)
+    K = O.decode(O.gather(h["k_index_pool"], h["page_table"], cfg.page_size, np.arange(P)))
+    scale = np.stack([np.abs(hr["w_index"][j].astype(np.float64)) @
+                      np.abs(O.decode(hr["q_index"][j]) @ K.T) for j in range(len(rows))])
+    del K
+    err = np.abs(sc - ref) / np.maximum(scale, 1e-30)
+    assert err.max() <= 2e-6, f"max scaled error {err.max():.2e}"
+    tol = 2e-6 * scale.max(axis=1)
+    for j in range(len(rows)):
+        mask = np.zeros(P, bool)
+        mask[want[j]] = True
+        assert ref[j][mask].min() >= ref[j][~mask].max() - 2 * tol[j], f"row {rows[j]}"
