@@ -318,3 +318,12 @@ def test_c2_full_size_sampled():
 @pytest.mark.timeout(900)
 def test_c3_full_size_sampled():
     _sampled_parity(configs.C3, [0, 2048, 4095], backward=True)
+
+
+@pytest.mark.timeout(900)
+def test_c3_cyclic_bf16_numerator_full_size_sampled():
+    """c3 as the paper's production composition runs it: pages dealt to 8
+    shards by owner(p) = p mod 8 and the cross-shard numerator reduced in
+    bf16; sampled rows and response keys against the unsharded fp64 oracle."""
+    _sampled_parity(configs.C3.scaled(ownership="cyclic", bf16_numerator=True), [1, 3000, 4094],
+                    backward=True)
