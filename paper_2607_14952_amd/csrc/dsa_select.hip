@@ -166,6 +166,9 @@ __global__ __launch_bounds__(64 * kWaves, 1) void dsa_score_kernel(DsaArgs a) {
 #pragma unroll
     for (int j = 0; j < kHPW; j += 2) {
       f32x16 s0 = zero16(), s1 = zero16();
+      // the MFMA chain at raised wave priority: while the other wave of the
+      // SIMD folds its scores (VALU), this one keeps issuing MFMAs (-2.5%)
+      __builtin_amdgcn_s_setprio(1);
 #pragma unroll
       for (int ks = 0; ks < 8; ++ks) {
         if (j == 0 && ks + kIKAhead < 8)
@@ -176,6 +179,7 @@ __global__ __launch_bounds__(64 * kWaves, 1) void dsa_score_kernel(DsaArgs a) {
         if (j == 0 && ks < kFI) f.issue(next, rn, ks, nvn);
         mfma_fence();
       }
+      __builtin_amdgcn_s_setprio(0);
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         part[r] = fmaf(wv[j], fmaxf(s0[r], 0.f), part[r]);
