@@ -144,7 +144,8 @@ def test_topk_sampled_bound_fallbacks():
     the rest of the row never reaches, so fewer than k keys clear the bound;
     (b) one wave's segment holds more candidates than its LDS region (every
     large key in the first eighth of the row); (c) rows are not 16-byte
-    aligned (odd leading dimension)."""
+    aligned (odd leading dimension); (d) every key is equal, so the regions
+    overflow and the full-row passes meet more than 4,096 ties in one bin."""
     import torch
     g = torch.Generator(device="cuda").manual_seed(12)
     n = 131072
@@ -159,6 +160,11 @@ def test_topk_sampled_bound_fallbacks():
     _check_topk(sc, 2048, "region overflow")
     sc = torch.randn((3, n + 1), device="cuda", generator=g)[:, :n]   # leading dimension n + 1
     _check_topk(sc, 2048, "unaligned rows")
+    # every key equal (then one larger key): the regions overflow and the
+    # fallback takes its heavy-tie passes; the lowest positions win the ties
+    sc = torch.zeros((2, n), device="cuda")
+    sc[1, 70000] = 1.0
+    _check_topk(sc, 2048, "all equal")
 
 
 def test_topk_fewer_than_k_and_offsets():
