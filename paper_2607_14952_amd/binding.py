@@ -117,8 +117,23 @@ def _torch():
     return torch
 
 
-def _ptr(t):
-    return None if t is None else t.data_ptr()
+def _ptr(t, dtype=None, name="tensor", dense=True):
+    """Device address of a tensor argument (None stays NULL), after checking
+    that it lives on the GPU, has the expected dtype, and is contiguous
+    (dense) or has unit stride in its last dimension (row-strided views whose
+    leading stride is passed on).  The library itself cannot tell a host
+    pointer from a device one."""
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a GPU tensor (got device {t.device})")
+    if dtype is not None and t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype} (got {t.dtype})")
+    if dense and not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if not dense and t.dim() and t.stride(-1) != 1:
+        raise ValueError(f"{name} must have unit stride in its last dimension")
+    return t.data_ptr()
 
 
 def _stream(stream):
@@ -166,10 +181,11 @@ def make_params(q, kv: PagedKV, *, n_q=None, n_q_heads=None, prefix_len: int, q_
     p.q_pos0 = q_pos0
     p.softmax_scale = scale
     p.flags = flags
-    p.q = _ptr(q)
-    p.k_pool = _ptr(kv.k_pool)
-    p.v_pool = _ptr(kv.v_pool)
-    p.page_table = _ptr(kv.page_table)
+    torch = _torch()
+    p.q = _ptr(q, kv.k_pool.dtype, "q")
+    p.k_pool = _ptr(kv.k_pool, None, "k_pool")
+    p.v_pool = _ptr(kv.v_pool, kv.k_pool.dtype, "v_pool")
+    p.page_table = _ptr(kv.page_table, torch.int32, "page_table")
     p.pool_epoch = kv.epoch
     p.expected_epoch = kv.epoch if expected_epoch is None else expected_epoch
     return p
@@ -200,8 +216,9 @@ def scatter_kv(kv: PagedKV, pos_begin: int, k_src, v_src, *, flags: int = 0, str
     p = make_params(dummy_q, kv, n_q=0, n_q_heads=kv.k_pool.shape[2], prefix_len=0, q_pos0=0,
                     scale=1.0, flags=flags)
     p.q = None
-    check(load_library().ls_scatter_kv(ctypes.byref(p), pos_begin, pos_begin + n, _ptr(k_src),
-                                       _ptr(v_src), _stream(stream)))
+    check(load_library().ls_scatter_kv(ctypes.byref(p), pos_begin, pos_begin + n,
+                                       _ptr(k_src, kv.k_pool.dtype, "k_src"),
+                                       _ptr(v_src, kv.v_pool.dtype, "v_src"), _stream(stream)))
 
 
 def prefix_attn_fwd(q, kv: PagedKV, splits, *, prefix_len: int, q_pos0: int, scale: float,
@@ -220,8 +237,10 @@ def prefix_attn_fwd(q, kv: PagedKV, splits, *, prefix_len: int, q_pos0: int, sca
     arr = (Split * n)(*[Split(int(b), int(e)) for b, e in splits])
     p = make_params(q, kv, prefix_len=prefix_len, q_pos0=q_pos0, scale=scale, flags=flags,
                     expected_epoch=expected_epoch)
-    check(load_library().ls_prefix_attn_fwd(ctypes.byref(p), arr, n, _ptr(out_part),
-                                            _ptr(lse_part), _stream(stream)))
+    check(load_library().ls_prefix_attn_fwd(ctypes.byref(p), arr, n,
+                                            _ptr(out_part, torch.float32, "out_part"),
+                                            _ptr(lse_part, torch.float32, "lse_part"),
+                                            _stream(stream)))
     return out_part, lse_part
 
 
@@ -235,9 +254,10 @@ def lse_merge(out_part, lse_part, *, out_dtype=None, out=None, lse=None, flags: 
         out = torch.empty((R, H, Dv), dtype=out_dtype, device=out_part.device)
     if lse is None:
         lse = torch.empty((H, R), dtype=torch.float32, device=out_part.device)
-    check(load_library().ls_lse_merge(_ptr(out_part), _ptr(lse_part), n, R, H, Dv,
-                                      _dtype_code(out), _ptr(out), _ptr(lse), flags,
-                                      _stream(stream)))
+    check(load_library().ls_lse_merge(_ptr(out_part, torch.float32, "out_part"),
+                                      _ptr(lse_part, torch.float32, "lse_part"), n, R, H, Dv,
+                                      _dtype_code(out), _ptr(out, None, "out"),
+                                      _ptr(lse, torch.float32, "lse"), flags, _stream(stream)))
     return out, lse
 
 
@@ -273,9 +293,12 @@ def prefix_attn_bwd(q, kv: PagedKV, d_out, out, lse, *, prefix_len: int, q_pos0:
         workspace = bwd_workspace(q, kv, prefix_len=prefix_len, q_pos0=q_pos0)
     p = make_params(q, kv, prefix_len=prefix_len, q_pos0=q_pos0, scale=scale, flags=flags,
                     expected_epoch=expected_epoch)
+    f32 = torch.float32
     check(load_library().ls_prefix_attn_bwd(
-        ctypes.byref(p), kv_begin, kv_end, _ptr(d_out), _ptr(out), _dtype_code(out), _ptr(lse),
-        _ptr(dq), _ptr(dk_resp), _ptr(dv_resp), _ptr(workspace), workspace.numel(),
+        ctypes.byref(p), kv_begin, kv_end, _ptr(d_out, q.dtype, "d_out"), _ptr(out, None, "out"),
+        _dtype_code(out), _ptr(lse, f32, "lse"), _ptr(dq, f32, "dq"),
+        _ptr(dk_resp, f32, "dk_resp"), _ptr(dv_resp, f32, "dv_resp"),
+        _ptr(workspace, None, "workspace"), workspace.numel() * workspace.element_size(),
         _stream(stream)))
     return dq, dk_resp, dv_resp
 
@@ -310,8 +333,11 @@ def sparse_attn_fwd(q, latent: PagedKV, idx, *, prefix_len: int, q_pos0: int, sc
         workspace = sparse_workspace(q, latent, topk, prefix_len=prefix_len, q_pos0=q_pos0,
                                      backward=False)
     p = _sparse_params(q, latent, prefix_len=prefix_len, q_pos0=q_pos0, scale=scale, flags=flags)
-    check(load_library().ls_sparse_attn_fwd(ctypes.byref(p), _ptr(idx), topk, _ptr(out),
-                                            _ptr(lse), _ptr(workspace), workspace.numel(),
+    check(load_library().ls_sparse_attn_fwd(ctypes.byref(p), _ptr(idx, torch.int32, "idx"), topk,
+                                            _ptr(out, torch.float32, "out"),
+                                            _ptr(lse, torch.float32, "lse"),
+                                            _ptr(workspace, None, "workspace"),
+                                            workspace.numel() * workspace.element_size(),
                                             _stream(stream)))
     return out, lse
 
@@ -328,9 +354,14 @@ def sparse_attn_bwd(q, latent: PagedKV, idx, d_out, out, lse, *, prefix_len: int
         workspace = sparse_workspace(q, latent, topk, prefix_len=prefix_len, q_pos0=q_pos0,
                                      backward=True)
     p = _sparse_params(q, latent, prefix_len=prefix_len, q_pos0=q_pos0, scale=scale, flags=flags)
-    check(load_library().ls_sparse_attn_bwd(ctypes.byref(p), _ptr(idx), topk, _ptr(d_out),
-                                            _ptr(out), _dtype_code(out), _ptr(lse), _ptr(dq),
-                                            _ptr(workspace), workspace.numel(), _stream(stream)))
+    check(load_library().ls_sparse_attn_bwd(ctypes.byref(p), _ptr(idx, torch.int32, "idx"), topk,
+                                            _ptr(d_out, torch.bfloat16, "d_out"),
+                                            _ptr(out, None, "out"), _dtype_code(out),
+                                            _ptr(lse, torch.float32, "lse"),
+                                            _ptr(dq, torch.float32, "dq"),
+                                            _ptr(workspace, None, "workspace"),
+                                            workspace.numel() * workspace.element_size(),
+                                            _stream(stream)))
     return dq
 
 
@@ -344,10 +375,12 @@ def dsa_index_scores(q_index, w_index, k_index_pool, page_table, *, pos_begin: i
     if scores is None:
         scores = torch.empty((n_q, max(4, n + (-n) % 4)), dtype=torch.float32,
                              device=q_index.device)
-    p = DsaParams(q_index.data_ptr(), w_index.data_ptr(), k_index_pool.data_ptr(),
-                  page_table.data_ptr(), k_index_pool.shape[0], page_table.shape[0], n_q, H, d,
-                  k_index_pool.shape[1])
-    check(load_library().ls_dsa_index_scores(ctypes.byref(p), pos_begin, pos_end, _ptr(scores),
+    p = DsaParams(_ptr(q_index, torch.bfloat16, "q_index"), _ptr(w_index, torch.float32, "w_index"),
+                  _ptr(k_index_pool, torch.bfloat16, "k_index_pool"),
+                  _ptr(page_table, torch.int32, "page_table"), k_index_pool.shape[0],
+                  page_table.shape[0], n_q, H, d, k_index_pool.shape[1])
+    check(load_library().ls_dsa_index_scores(ctypes.byref(p), pos_begin, pos_end,
+                                             _ptr(scores, torch.float32, "scores", dense=False),
                                              scores.stride(0), _stream(stream)))
     return scores[:, :n]
 
@@ -367,7 +400,10 @@ def topk_select(scores, k: int, *, n: int | None = None, positions=None, pos_off
     assert out_pos.stride(0) == out_scores.stride(0) and out_pos.stride(1) == 1
     if positions is not None:
         assert positions.stride(0) == scores.stride(0)
-    check(load_library().ls_topk_select(_ptr(scores), scores.stride(0), _ptr(positions), rows, n,
-                                        pos_offset, k, _ptr(out_pos), _ptr(out_scores),
-                                        out_pos.stride(0), _stream(stream)))
+    check(load_library().ls_topk_select(
+        _ptr(scores, torch.float32, "scores", dense=False), scores.stride(0),
+        _ptr(positions, torch.int32, "positions", dense=False), rows, n, pos_offset, k,
+        _ptr(out_pos, torch.int32, "out_pos", dense=False),
+        _ptr(out_scores, torch.float32, "out_scores", dense=False), out_pos.stride(0),
+        _stream(stream)))
     return out_pos, out_scores

@@ -210,3 +210,53 @@ def test_topk_rejects():
                               16, None) == -1                                   # positions >= 2^31
     assert lib.ls_topk_select(FAKE, 1000, None, 4, 1000, 0, 16, FAKE + 64, None, 16, None) == -4
     assert lib.ls_topk_select(FAKE, 1000, None, 0, 1000, 0, 16, FAKE * 64, None, 16, None) == 0
+
+
+# ------------------------------------------------------------ binding argument checks
+class _FakeTensor:
+    """Just enough of a tensor for the binding's pointer checks."""
+
+    def __init__(self, dtype, cuda=True, contiguous=True, last_stride=1):
+        self.dtype, self.is_cuda = dtype, cuda
+        self._contig, self._last = contiguous, last_stride
+        self.device = "cuda:0" if cuda else "cpu"
+
+    def is_contiguous(self):
+        return self._contig
+
+    def dim(self):
+        return 2
+
+    def stride(self, i):
+        return self._last if i == -1 else 64
+
+    def data_ptr(self):
+        return 0x1000
+
+
+def test_binding_checks_device_dtype_and_layout():
+    """A host tensor would reach a kernel as a host address, a wrong dtype would be
+    reinterpreted and a strided tensor misread: the binding refuses all three before
+    calling the library."""
+    import torch
+    f32 = torch.float32
+    assert B._ptr(None) is None
+    assert B._ptr(_FakeTensor(f32), f32, "x") == 0x1000
+    with pytest.raises(ValueError, match="GPU tensor"):
+        B._ptr(_FakeTensor(f32, cuda=False), f32, "x")
+    with pytest.raises(TypeError, match="must be torch.float32"):
+        B._ptr(_FakeTensor(torch.bfloat16), f32, "x")
+    with pytest.raises(ValueError, match="contiguous"):
+        B._ptr(_FakeTensor(f32, contiguous=False), f32, "x")
+    # row-strided views: only the last dimension has to be unit-stride
+    assert B._ptr(_FakeTensor(f32, contiguous=False), f32, "x", dense=False) == 0x1000
+    with pytest.raises(ValueError, match="unit stride"):
+        B._ptr(_FakeTensor(f32, contiguous=False, last_stride=2), f32, "x", dense=False)
+    # through an entry point: host tensors are refused before anything is launched
+    q = torch.zeros((4, 2, 64), dtype=f32)
+    pool = torch.zeros((2, 64, 1, 64), dtype=f32)
+    kv = B.PagedKV(pool, pool, torch.zeros(2, dtype=torch.int32))
+    with pytest.raises(ValueError, match="GPU tensor"):
+        B.prefix_attn_fwd(q, kv, [(0, 4)], prefix_len=0, q_pos0=0, scale=0.125)
+    with pytest.raises(ValueError, match="GPU tensor"):
+        B.topk_select(torch.zeros((2, 8)), 3)
