@@ -317,7 +317,10 @@ def test_c2_full_size_sampled():
 
 @pytest.mark.timeout(900)
 def test_c3_full_size_sampled():
-    _sampled_parity(configs.C3, [0, 2048, 4095], backward=True)
+    """c3 as bench.py times it; rows on both sides of the dq (16-token) and
+    forward (32-token) workgroup boundaries, the middle, the last, and planted
+    targets."""
+    _sampled_parity(configs.C3, [0, 15, 16, 31, 32, 2048, 4095], backward=True)
 
 
 @pytest.mark.timeout(900)
