@@ -35,6 +35,7 @@ class ReplayConfig:
     pool_slack: float = 1.0    # physical pages / logical pages (>= 1)
     plant_frac: float = 0.0    # fraction of prefix keys aligned to a random query
     plant_gain: float = 4.0
+    plant_unit: bool = False   # add gain * q / |q| instead of gain * q (the literal "+4 sigma" reading)
     backward: bool = True
     sparse: bool = False       # MLA/DSA latent replay (one shared latent row)
     topk: int = 0

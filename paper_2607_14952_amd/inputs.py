@@ -140,8 +140,10 @@ def plant_targets(cfg, q_f32: np.ndarray, table: np.ndarray):
     plants: dict[int, list] = {}
     for j, t, h in zip(pos.tolist(), rows.tolist(), heads.tolist()):
         p = int(table[j // cfg.page_size])
-        plants.setdefault(p, []).append(
-            (j % cfg.page_size, h // cfg.group, cfg.plant_gain * q_f32[t, h]))
+        d = q_f32[t, h]
+        if cfg.plant_unit:   # the score-sigma variant: a unit direction
+            d = d / np.float32(np.linalg.norm(d))
+        plants.setdefault(p, []).append((j % cfg.page_size, h // cfg.group, cfg.plant_gain * d))
     return (pos, rows, heads), plants
 
 

@@ -119,6 +119,12 @@ def test_bf16_small_planted():
     full_case(BF16_SMALL)
 
 
+def test_bf16_small_planted_unit():
+    """The secondary planting reading (each planted key moves 4 along the unit
+    direction of its target query, the literal "+4 score-sigma")."""
+    full_case(BF16_SMALL.scaled(name="bf16_small_unit", plant_unit=True))
+
+
 def test_bf16_dkdv_row_chunks_and_key_blocks():
     """Response gradients summed over several row chunks of the dk/dv kernel
     and several key blocks, every key and row compared.  640 tokens x G = 8 =
