@@ -49,6 +49,15 @@ def flops(cfg):
     return fwd, bwd
 
 
+def sparse_flops(cfg):
+    """Sparse latent replay: each row visits its top-k prefix entries plus the
+    causal response window.  Forward: Q.K^T over Dk and P.V over Dv; backward
+    (dq only): the QK^T recompute (Dk), dO.V^T (Dv) and dS.K (Dk)."""
+    R, H, Dk, Dv = cfg.resp_len, cfg.n_q_heads, cfg.head_dim, cfg.head_dim_v
+    vis = R * cfg.topk + R * (R + 1) // 2
+    return 2 * H * (Dk + Dv) * vis, 2 * H * (2 * Dk + Dv) * vis
+
+
 def log(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
@@ -266,10 +275,10 @@ def run_sparse(cfg, args):
     kw = dict(prefix_len=cfg.prefix_len, q_pos0=cfg.q_pos0, scale=cfg.scale)
     ws = B.sparse_workspace(q, kv, cfg.topk, backward=True, prefix_len=cfg.prefix_len,
                             q_pos0=cfg.q_pos0)
-    out = torch.empty((cfg.resp_len, cfg.n_q_heads, 512), dtype=torch.float32, device="cuda")
+    out = torch.empty((cfg.resp_len, cfg.n_q_heads, cfg.head_dim_v), dtype=torch.float32, device="cuda")
     lse = torch.empty((cfg.n_q_heads, cfg.resp_len), dtype=torch.float32, device="cuda")
-    out_b = torch.empty((cfg.resp_len, cfg.n_q_heads, 512), dtype=torch.bfloat16, device="cuda")
-    dq = torch.empty((cfg.resp_len, cfg.n_q_heads, 576), dtype=torch.float32, device="cuda")
+    out_b = torch.empty((cfg.resp_len, cfg.n_q_heads, cfg.head_dim_v), dtype=torch.bfloat16, device="cuda")
+    dq = torch.empty((cfg.resp_len, cfg.n_q_heads, cfg.head_dim), dtype=torch.float32, device="cuda")
 
     def step(ev=None):
         nonlocal idx
@@ -302,8 +311,7 @@ def run_sparse(cfg, args):
     wall = time.perf_counter() - t0
     R, H = cfg.resp_len, cfg.n_q_heads
     vis = R * cfg.topk + R * (R + 1) // 2
-    fwd_fl = 2 * H * (576 + 512) * vis
-    bwd_fl = 2 * H * (576 + 512 + 576) * vis
+    fwd_fl, bwd_fl = sparse_flops(cfg)
     gathered = vis * 1152
     fwd_ms = sum(e[0].elapsed_time(e[1]) for e in evs) / args.steps
     bwd_ms = sum(e[1].elapsed_time(e[2]) for e in evs) / args.steps
