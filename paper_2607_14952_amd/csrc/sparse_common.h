@@ -7,8 +7,8 @@
 //
 // Key lists are resolved to physical latent rows once per call.  A workgroup
 // owns one token, lanes own heads (scores computed transposed, S^T = K Q^T).
-// Gathered rows (1152 bytes) stream by direct global->LDS loads into a
-// three-slot ring; 16-byte chunks are permuted inside aligned 8-chunk groups
+// Gathered rows (1152 bytes) stream by direct global->LDS loads into a ring
+// of tiles (four slots in the forward, three in the backward); 16-byte chunks are permuted inside aligned 8-chunk groups
 // so row reads and transposing column reads are bank-conflict free.
 // The forward kernel is in sparse_fwd.hip, the dq backward in sparse_bwd.hip.
 #pragma once
@@ -130,6 +130,14 @@ struct SFetch {
   // the token's resolved key list: lane k and lane k + 32 hold key row k's
   __device__ __forceinline__ int32_t rows_of(__amdgpu_buffer_rsrc_t phys_t, int T, int lane) const {
     return __builtin_amdgcn_raw_buffer_load_b32(phys_t, (T * kKeys + (lane & 31)) * 4, 0, 0);
+  }
+  // The same list as rows_of, brought into LDS by one direct load (4 bytes per
+  // lane; dst is the wave's own 64-entry region): it travels with a stage of
+  // direct loads and is complete when that stage is.
+  __device__ __forceinline__ void rows_to_lds(int32_t* dst, __amdgpu_buffer_rsrc_t phys_t, int T,
+                                              int lane) const {
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(phys_t, LS_LDS(dst), 4, (T * kKeys + (lane & 31)) * 4,
+                                             0, 0, 0);
   }
   // w: the wave (uniform)
   __device__ __forceinline__ void issue_one(char* tile, __amdgpu_buffer_rsrc_t r, int32_t rows,

@@ -5,26 +5,38 @@
 // the response window).  Each gathered row is fetched once per token, and the
 // waves need no exchange: one barrier per tile serves the ring.  Q (144
 // registers) and the output accumulator (256) stay in registers, one wave per
-// SIMD.  Gathered rows stream into a three-slot LDS ring, two tiles ahead;
-// tile t is fully consumed in iteration t.  Tokens with more keys (later
-// ones: the response window grows with t) are dispatched first.
+// SIMD.  Gathered rows stream into a four-slot LDS ring, three tiles ahead;
+// tile t is fully consumed in iteration t.  A slot holds a 36 KiB tile and,
+// after it, each wave's copy of the physical rows of tile t + 3, which travel
+// with the stage of tile t: no register holds a row list that is still in
+// flight, and the two kinds of direct load into a slot share its pointer.
+// Tokens with more keys (later ones: the response window grows with t) are
+// dispatched first.
 #include "sparse_common.h"
 
 namespace ls {
 namespace {
 using namespace sparse;
 
-constexpr int kFSlots = 3;
+constexpr int kFSlots = 4;
+constexpr int kSlotBytes = kTile + 4 * 256;   // tile + 4 waves x 64 row entries
 
 // One tile.  `next` and `tile` are distinct ring slots; the restrict
 // qualifiers tell the compiler so, which keeps it from waiting for the direct
-// loads before reading `tile`.
+// loads before reading `tile`.  The rows of the stage issued here come from
+// `tile`'s row area; the stage carries the rows of tile T_rows into `next`'s.
 __device__ __forceinline__ void fwd_tile(const SparseArgs& a, char* __restrict__ next,
                                          const char* __restrict__ tile, const SFetch& f,
-                                         __amdgpu_buffer_rsrc_t pool, int32_t pr, int w,
+                                         __amdgpu_buffer_rsrc_t pool, int w,
                                          const bf16x8* qreg, const SOffsets& so, int T, int n_t,
-                                         int hh, f32x16* oacc, float& m_run, float& l_run) {
-  f32x16 s = s_scores(tile, qreg, so, [&](int i) { f.issue_one(next, pool, pr, w, i); });
+                                         int hh, f32x16* oacc, float& m_run, float& l_run,
+                                         __amdgpu_buffer_rsrc_t phys_t, int T_rows, int lane) {
+  const int32_t pr = reinterpret_cast<const int32_t*>(tile + kTile + 256 * w)[lane];
+  f32x16 s = s_scores(tile, qreg, so, [&](int i) {
+    f.issue_one(next, pool, pr, w, i);
+    if (i == 8)
+      f.rows_to_lds(reinterpret_cast<int32_t*>(next + kTile + 256 * w), phys_t, T_rows, lane);
+  });
   if ((T + 1) * kKeys > n_t) {
 #pragma unroll
     for (int r = 0; r < 16; ++r)
@@ -40,7 +52,7 @@ __device__ __forceinline__ void fwd_tile(const SparseArgs& a, char* __restrict__
 }
 
 __global__ __launch_bounds__(256, 1) void sparse_fwd_kernel(SparseArgs a) {
-  __shared__ __attribute__((aligned(1024))) char smem[kFSlots * kTile];
+  __shared__ __attribute__((aligned(1024))) char smem[kFSlots * kSlotBytes];
   const int tid = threadIdx.x, lane = tid & 63;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int l32 = lane & 31, hh = lane >> 5;
@@ -51,18 +63,25 @@ __global__ __launch_bounds__(256, 1) void sparse_fwd_kernel(SparseArgs a) {
   const __amdgpu_buffer_rsrc_t phys_t = phys_rsrc(a, t);
   const __amdgpu_buffer_rsrc_t pool = pool_rsrc(a.latent);
   // tiles past the last one are clamped to it: every iteration issues one
-  // stage of 9 direct loads per wave, and rows stay inside the key list
+  // stage of 10 direct loads per wave (9 row chunks and a row list), and rows
+  // stay inside the key list
   auto clamp = [&](int T) { return T < n_tiles ? T : n_tiles - 1; };
 
   SFetch f;
   f.init(lane, w);
   const SOffsets so = s_offsets(lane);
-  // the row lists of the first three tiles load before any tile does, so
-  // the waits for them do not order the first two stages
-  const int32_t r0 = f.rows_of(phys_t, 0, lane), r1 = f.rows_of(phys_t, clamp(1), lane);
-  int32_t pr = f.rows_of(phys_t, clamp(2), lane), pn;
+  // the row lists of the first three tiles and Q load before any tile does
+  const int32_t r0 = f.rows_of(phys_t, 0, lane), r1 = f.rows_of(phys_t, clamp(1), lane),
+                r2 = f.rows_of(phys_t, clamp(2), lane);
+  auto rows_area = [&](int slot) {
+    return reinterpret_cast<int32_t*>(smem + slot * kSlotBytes + kTile + 256 * w);
+  };
   f.issue(smem, pool, r0, w);
-  f.issue(smem + kTile, pool, r1, w);
+  f.rows_to_lds(rows_area(0), phys_t, clamp(3), lane);
+  f.issue(smem + kSlotBytes, pool, r1, w);
+  f.rows_to_lds(rows_area(1), phys_t, clamp(4), lane);
+  f.issue(smem + 2 * kSlotBytes, pool, r2, w);
+  f.rows_to_lds(rows_area(2), phys_t, clamp(5), lane);
 
   bf16x8 qreg[36];   // Q^T operand: q[t][head][16*ks + 8*hh .. +7]
   {
@@ -79,12 +98,10 @@ __global__ __launch_bounds__(256, 1) void sparse_fwd_kernel(SparseArgs a) {
   tile_barrier();
 
   for (int T = 0; T < n_tiles; ++T) {
-    pn = f.rows_of(phys_t, clamp(T + 3), lane);
-    __builtin_amdgcn_sched_barrier(0);   // row indices load ahead of this stage's direct loads
-    fwd_tile(a, smem + ((T + 2) % kFSlots) * kTile, smem + (T % kFSlots) * kTile, f, pool, pr, w,
-             qreg, so, T, n_t, hh, oacc, m_run, l_run);
-    pr = pn;
-    __builtin_amdgcn_s_waitcnt(0x0F79);   // vmcnt(9): only this iteration's stage may be in flight
+    fwd_tile(a, smem + ((T + 3) % kFSlots) * kSlotBytes, smem + (T % kFSlots) * kSlotBytes, f,
+             pool, w, qreg, so, T, n_t, hh, oacc, m_run, l_run, phys_t, clamp(T + 6), lane);
+    // vmcnt(20): the stages of tiles T + 2 and T + 3 may be in flight
+    __builtin_amdgcn_s_waitcnt(0x4F74);
     tile_barrier();
   }
   wait_fetch();   // no direct load is left in flight when the waves end
