@@ -70,8 +70,8 @@ def kernel_stats(directory: str):
     return out
 
 
-def dispatch_medians(directory: str):
-    """kernel name -> median dispatch duration (ns) from the kernel trace."""
+def dispatch_durations(directory: str):
+    """kernel name -> list of dispatch durations (ns) from the kernel trace."""
     files = _find(directory, "kernel_trace.csv")
     if not files:
         return {}
@@ -81,7 +81,26 @@ def dispatch_medians(directory: str):
             name = _col(row, "Kernel_Name", "KernelName", "Name")
             t = float(_col(row, "End_Timestamp")) - float(_col(row, "Start_Timestamp"))
             per[name].append(t)
-    return {k: _median(v) for k, v in per.items()}
+    return per
+
+
+def dispatch_medians(directory: str):
+    """kernel name -> median dispatch duration (ns) from the kernel trace."""
+    return {k: _median(v) for k, v in dispatch_durations(directory).items()}
+
+
+def long_launches(durations, min_ms: float = 1.0):
+    """For a kernel launched at very different sizes (its shortest dispatch
+    under a fifth of its longest, the longest at least min_ms), the count and
+    mean duration (ns) of the dispatches at least half as long as the longest;
+    None otherwise."""
+    if not durations:
+        return None
+    hi = max(durations)
+    if hi < min_ms * 1e6 or min(durations) >= 0.2 * hi:
+        return None
+    big = [d for d in durations if d >= 0.5 * hi]
+    return len(big), sum(big) / len(big)
 
 
 def write_stats_md(directory: str, out_path: str, command: str, title: str) -> None:
@@ -98,6 +117,17 @@ def write_stats_md(directory: str, out_path: str, command: str, title: str) -> N
         lines.append(f"| `{r['name'][:110]}` | {r['calls']} | {r['avg_ns'] / 1e6:.3f} | {ms} | "
                      f"{r['min_ns'] / 1e6:.3f} | {r['max_ns'] / 1e6:.3f} | "
                      f"{r['total_ns'] / 1e6:.2f} | {r['pct']:.2f} |")
+    durs = dispatch_durations(directory)
+    mixed = []
+    for r in sorted(rows, key=lambda r: -r["total_ns"]):
+        ll = long_launches(durs.get(r["name"], []))
+        if ll is not None:
+            mixed.append(f"| `{r['name'][:110]}` | {ll[0]} | {ll[1] / 1e6:.3f} |")
+    if mixed:
+        lines += ["", "Kernels launched at very different sizes (for example one call per prefix "
+                  "shard and a short one over the response keys): count and mean duration of "
+                  "the launches at least half as long as the longest.", "",
+                  "| kernel | long launches | avg ms |", "|---|---:|---:|"] + mixed
     with open(out_path, "w") as f:
         f.write("\n".join(lines) + "\n")
 

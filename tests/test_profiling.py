@@ -99,3 +99,13 @@ def test_stats_table(tmp_path):
     assert rows[0].startswith("| `k_slow`"), "sorted by total time"
     fast = [c.strip() for c in rows[1].strip("|").split("|")]
     assert fast[1:4] == ["3", "1.000", "1.000"]                   # calls, average, median
+    assert "long launches" not in text                            # no kernel of mixed sizes
+
+
+def test_long_launches():
+    ms = 1e6
+    # three shard-sized launches and one short one over the response keys
+    assert P.long_launches([22 * ms, 21 * ms, 23 * ms, 0.3 * ms]) == (3, pytest.approx(22 * ms))
+    assert P.long_launches([22 * ms, 21 * ms]) is None            # one size
+    assert P.long_launches([0.5 * ms, 0.01 * ms]) is None         # all short
+    assert P.long_launches([]) is None
