@@ -441,6 +441,12 @@ def main():
         print("no GPU visible", file=sys.stderr)
         sys.exit(1)
     cfg = configs.get(args.config)
+    if args.calib_copy:
+        src = torch.ones(1 << 28, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     if isinstance(cfg, configs.CaptureConfig):
         run_capture(cfg, args)
         return
@@ -463,12 +469,6 @@ def main():
     step = ReplayStep(cfg, dev, backward=True, stream=stream)
     fwd_fl, bwd_fl = flops(cfg)
 
-    if args.calib_copy:
-        src = torch.ones(1 << 28, dtype=torch.float32, device="cuda")
-        dst = torch.empty_like(src)
-        dst.copy_(src)
-        torch.cuda.synchronize()
-        del src, dst
     for w in range(args.warmup):
         step.step()
         torch.cuda.synchronize()
