@@ -8,8 +8,9 @@
 //
 // Keys are processed in 32-key tiles aligned to multiples of 32 (one page-table
 // entry per tile when pages hold >= 32 positions).  K and V rows are fetched
-// with direct global->LDS loads into a four-slot ring, two tiles ahead (each
-// wave waits only for the older of the two stages in flight); no VGPRs stage
+// with direct global->LDS loads into a four-slot ring: three tiles ahead with
+// 8 waves, two ahead with 4 (whose pipelined loop also keeps the previous V);
+// each wave waits only for the oldest stage in flight, and no VGPRs stage
 // them.  The K^T operand is one 16-byte LDS read per lane; the V^T operand
 // comes from transposing LDS reads of the row-major V tile.
 //
