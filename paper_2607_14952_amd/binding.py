@@ -397,9 +397,13 @@ def topk_select(scores, k: int, *, n: int | None = None, positions=None, pos_off
         out_pos = torch.empty((rows, k), dtype=torch.int32, device=scores.device)
     if out_scores is None:
         out_scores = torch.empty((rows, k), dtype=torch.float32, device=scores.device)
-    assert out_pos.stride(0) == out_scores.stride(0) and out_pos.stride(1) == 1
-    if positions is not None:
-        assert positions.stride(0) == scores.stride(0)
+    # the library takes one row stride for the two outputs and one for scores and positions
+    if out_pos.stride(0) != out_scores.stride(0) or out_pos.stride(1) != 1 \
+            or out_scores.stride(1) != 1:
+        raise ValueError("topk_select: out_pos and out_scores must share one row stride and "
+                         "have unit column stride")
+    if positions is not None and positions.stride(0) != scores.stride(0):
+        raise ValueError("topk_select: positions must have the row stride of scores")
     check(load_library().ls_topk_select(
         _ptr(scores, torch.float32, "scores", dense=False), scores.stride(0),
         _ptr(positions, torch.int32, "positions", dense=False), rows, n, pos_offset, k,

@@ -47,7 +47,9 @@ class DsaSelect:
             return self.idx
         # per-shard candidates (positions ascending across shards), then the merge
         for s, (b, e) in enumerate(self.shards):
-            assert e - b >= k, "each shard must hold at least k positions"
+            if e - b < k:
+                raise ValueError(f"candidate selection: shard [{b}, {e}) holds fewer than "
+                                 f"k = {k} positions")
             B.topk_select(self.scores[:, b:], k, n=e - b, pos_offset=b,
                           out_pos=self.cand_pos[:, s * k:(s + 1) * k],
                           out_scores=self.cand_sc[:, s * k:(s + 1) * k], stream=self.stream)

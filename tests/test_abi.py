@@ -260,3 +260,10 @@ def test_binding_checks_device_dtype_and_layout():
         B.prefix_attn_fwd(q, kv, [(0, 4)], prefix_len=0, q_pos0=0, scale=0.125)
     with pytest.raises(ValueError, match="GPU tensor"):
         B.topk_select(torch.zeros((2, 8)), 3)
+    # one row stride for both outputs, one for scores and positions
+    wide = torch.zeros((2, 10), dtype=torch.int32)
+    with pytest.raises(ValueError, match="share one row stride"):
+        B.topk_select(torch.zeros((2, 8)), 3, out_pos=wide[:, :3],
+                      out_scores=torch.zeros((2, 3)))
+    with pytest.raises(ValueError, match="row stride of scores"):
+        B.topk_select(torch.zeros((2, 8)), 3, positions=torch.zeros((2, 9), dtype=torch.int32))
