@@ -78,6 +78,14 @@ def test_sparse_two_head_groups():
     run(cfg, inputs.sparse_inputs(cfg))
 
 
+def test_sparse_two_to_four_tiles():
+    """Key lists of 33 .. 128 entries (2, 3 and 4 tiles of 32): the forward
+    keeps three tiles in flight, so these tokens end inside its prologue or its
+    first iterations, where later tiles are clamped to the last one."""
+    cfg = SMALL.scaled(name="c5_few_tiles", resp_len=96, topk=32)
+    run(cfg, inputs.sparse_inputs(cfg))
+
+
 @pytest.mark.timeout(900)
 def test_c5_full_size_sampled():
     cfg = configs.C5
