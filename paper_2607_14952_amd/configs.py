@@ -184,7 +184,9 @@ class CaptureConfig:
     page_size: int
     length: int                    # prompt positions captured
     chunk: int                     # positions per capture chunk
-    keys_per_split: int = 262_144  # earlier-chunk keys per split of a chunk's forward
+    # earlier-chunk keys per split of a chunk's forward: short splits give every chunk
+    # many equal workgroups (the last chunk 64 pieces + its own), which keeps all CUs busy
+    keys_per_split: int = 32_768
     q_blocks: int = 0              # distinct query blocks; chunk c uses block c mod q_blocks (0: own)
     pool_slack: float = 1.0
     table: str = "perm"

@@ -27,7 +27,7 @@ def test_splits_cover_earlier_keys_then_own():
         assert flat == list(range(b)), "earlier keys covered once, in order"
         assert all(s1 - s0 <= cfg.keys_per_split for s0, s1 in sp[:-1])
     CAP = configs.CAPTURE_2M
-    assert len(CAP.chunk_splits(CAP.n_chunks - 1)) == 9      # 8 x 262,144 earlier keys + own
+    assert len(CAP.chunk_splits(CAP.n_chunks - 1)) == 65     # 64 x 32,704 earlier keys + own
     assert CAP.n_chunks == 512 and CAP.visible() == CAP.length * (CAP.length + 1) // 2
 
 
