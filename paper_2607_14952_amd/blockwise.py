@@ -73,7 +73,10 @@ class BlockwiseReplay:
         shard = cfg.prefix_len // cfg.n_shards
         self.prefix_ranges = [(s * shard, cfg.prefix_len if s == cfg.n_shards - 1 else (s + 1) * shard)
                               for s in range(cfg.n_shards)]
-        n_parts = cfg.n_shards + 1
+        # the forward's prefix splits: each shard range cut splits_per_shard ways, so
+        # a launch holds many equal workgroups; the backward runs once per shard range
+        self.fwd_ranges = cfg.splits()[:-1]
+        n_parts = len(self.fwd_ranges) + 1
         self.n_parts = n_parts
         self.out_part_flat = torch.empty(n_parts * blk * Hq * Dv, **kw)
         self.lse_part_flat = torch.empty(n_parts * Hq * blk, **kw)
@@ -96,7 +99,7 @@ class BlockwiseReplay:
         qb, dob = q[rows], d_out[rows]
         q0 = c.prefix_len + rows.start
         kv_end = q0 + qb.shape[0]
-        splits = self.prefix_ranges + [(c.prefix_len, kv_end)]
+        splits = self.fwd_ranges + [(c.prefix_len, kv_end)]
         n = qb.shape[0]
         Hq, Dv, P = c.n_q_heads, c.head_dim_v, self.n_parts
         op = self.out_part_flat[:P * n * Hq * Dv].view(P, n, Hq, Dv)

@@ -158,7 +158,7 @@ C3 = ReplayConfig(name="c3_replay_2m", seed=3, dtype="bf16", n_q_heads=16, n_kv_
 # 4.46M resident prefix, 8 members of 8,192 tokens replayed in 2,048-token blocks.
 C4 = ReplayConfig(name="c4_resident_4p46m_g8", seed=4, dtype="bf16", n_q_heads=16,
                   n_kv_heads=2, head_dim=256, head_dim_v=256, page_size=256,
-                  prefix_len=4_456_448, resp_len=8192, n_shards=8, splits_per_shard=1,
+                  prefix_len=4_456_448, resp_len=8192, n_shards=8, splits_per_shard=8,
                   table="sample", pool_slack=1.125, members=8, block=2048)
 
 # MLA/DSA-style sparse latent replay.
