@@ -1,6 +1,7 @@
-"""Chunked capture planning (CPU): chunk ranges and split plans cover every
-key each chunk's rows can see, exactly once, and the page table hands every
-chunk pages of its own."""
+"""Split planning (CPU): capture chunk ranges and split plans cover every key
+each chunk's rows can see, exactly once, and the page table hands every chunk
+pages of its own; the blockwise forward's pieces tile the prefix and nest in
+the backward's shard ranges."""
 import numpy as np
 
 from paper_2607_14952_amd import configs, inputs
@@ -46,3 +47,22 @@ def test_capture_inputs_are_chunk_draws():
     # a longer prompt with the same chunking keeps the earlier chunks' rows
     longer = inputs.capture_inputs(configs.CaptureConfig(**{**SMALL.__dict__, "length": 6 * 512}))
     assert np.array_equal(longer["k"][:5 * 512], h["k"][:5 * 512])
+
+
+def test_blockwise_forward_plan():
+    """c4's block forward: each of the 8 shard ranges cut 8 ways, contiguous,
+    covering the prefix once, within one launch's split limit; the response
+    split follows (its end moves with the block)."""
+    cfg = configs.C4
+    sp = cfg.splits()
+    prefix = sp[:-1]
+    assert len(prefix) == cfg.n_shards * cfg.splits_per_shard == 64
+    assert prefix[0][0] == 0 and prefix[-1][1] == cfg.prefix_len
+    assert all(a[1] == b[0] for a, b in zip(prefix, prefix[1:])), "contiguous"
+    assert {e - b for b, e in prefix} == {cfg.prefix_len // 64}
+    assert len(sp) <= 128
+    # the backward's shard ranges are unions of consecutive forward pieces
+    shard = cfg.prefix_len // cfg.n_shards
+    for s in range(cfg.n_shards):
+        pieces = prefix[8 * s:8 * s + 8]
+        assert pieces[0][0] == s * shard and pieces[-1][1] == (s + 1) * shard
