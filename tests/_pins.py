@@ -338,6 +338,42 @@ def pin_sparse_subset(O):
     assert rel_l2(dq, num) < 1e-6, f"sparse dq vs finite differences {rel_l2(dq, num):.2e}"
 
 
+# ---------------------------------------------------------------- input decoding
+def pin_decode(O):
+    """bf16 bit patterns decode to the values the bfloat16 format defines
+    (sign, 8-bit exponent with bias 127, 7-bit fraction; the upper half of the
+    fp32 encoding): hand-made patterns against their exact values, every one of
+    the 65,536 patterns against torch's bfloat16 -> float64 cast, and fp32
+    input passed through unchanged."""
+    import torch
+    hand = {
+        0x3F80: 1.0, 0xBF80: -1.0, 0xC020: -2.5, 0x4049: 3.140625, 0x4000: 2.0,
+        0x3F00: 0.5, 0x3FC0: 1.5, 0x3F81: 1.0 + 2.0 ** -7, 0x0080: 2.0 ** -126,
+        0x0001: 2.0 ** -133, 0x007F: 127 * 2.0 ** -133, 0x7F7F: (2.0 - 2.0 ** -7) * 2.0 ** 127,
+        0x4780: 65536.0, 0xC7C3: -99840.0,
+    }
+    bits = np.array(list(hand), dtype=np.uint16)
+    got = O.decode(bits)
+    assert got.dtype == np.float64, "decode must return float64"
+    assert np.array_equal(got, np.array(list(hand.values()))), f"decode of hand patterns: {got}"
+    z = O.decode(np.array([0x0000, 0x8000], dtype=np.uint16))
+    assert np.array_equal(z, [0.0, 0.0]) and not np.signbit(z[0]) and np.signbit(z[1]), "signed zeros"
+    inf = O.decode(np.array([0x7F80, 0xFF80], dtype=np.uint16))
+    assert np.array_equal(inf, [np.inf, -np.inf]), "infinities"
+    assert np.all(np.isnan(O.decode(np.array([0x7FC0, 0xFFC1, 0x7F81], dtype=np.uint16)))), "NaNs"
+    every = np.arange(65536, dtype=np.uint32).astype(np.uint16)
+    want = torch.from_numpy(every.view(np.int16).copy()).view(torch.bfloat16).to(torch.float64).numpy()
+    got = O.decode(every)
+    nan = np.isnan(want)
+    assert np.array_equal(np.isnan(got), nan), "decode: NaN patterns differ from torch"
+    assert np.array_equal(got[~nan], want[~nan]), "decode differs from torch's bfloat16 cast"
+    rng = np.random.default_rng(22)
+    x = rng.standard_normal((3, 5)).astype(np.float32)
+    assert np.array_equal(O.decode(x), x.astype(np.float64)), "fp32 input must pass through"
+    shaped = O.decode(every[:24].reshape(2, 3, 4))
+    assert shaped.shape == (2, 3, 4) and np.array_equal(shaped.ravel(), O.decode(every[:24])), "shape"
+
+
 # ---------------------------------------------------------------- production composition
 def pin_bf16_round(O):
     """bf16 rounding equals torch's float32 -> bfloat16 cast (round to nearest
@@ -484,6 +520,6 @@ def pin_topk_local_candidates_merge(O):
 ALL_PINS = [pin_single_key, pin_identical_keys, pin_zero_query, pin_scale_and_gqa,
             pin_merge_closed_form, pin_split_merge_invariance, pin_causal, pin_gather_bruteforce,
             pin_finite_differences, pin_bwd_partition, pin_torch_autograd, pin_sampled_rows,
-            pin_sparse_full_index_is_dense, pin_sparse_subset, pin_bf16_round,
+            pin_sparse_full_index_is_dense, pin_sparse_subset, pin_decode, pin_bf16_round,
             pin_bf16_numerator_merge, pin_cyclic_ownership, pin_dsa_index_closed_form,
             pin_topk_ties_and_order, pin_topk_local_candidates_merge]

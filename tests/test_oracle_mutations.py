@@ -39,6 +39,11 @@ MUTATIONS = [
     ("sparse_values_tail", "o[k_] = (w / z[:, None]) @ C[:, :head_dim_v]",
      "o[k_] = (w / z[:, None]) @ C[:, -head_dim_v:]"),
     ("sparse_dq_no_delta", "dS = P * (dP - delta[:, None])\n        dq[k_]", "dS = P * dP\n        dq[k_]"),
+    ("decode_shift_15", "return (x.astype(np.uint32) << np.uint32(16))",
+     "return (x.astype(np.uint32) << np.uint32(15))"),
+    ("decode_as_fp16", "return (x.astype(np.uint32) << np.uint32(16)).view(np.float32).astype(np.float64)",
+     "return x.view(np.float16).astype(np.float64)"),
+    ("decode_via_fp16_bits", "if x.dtype == np.uint16:", "if x.dtype == np.float16:"),
     ("bf16_truncate", "return np.ldexp(np.rint(np.ldexp(m, 8)), e - 8)",
      "return np.ldexp(np.trunc(np.ldexp(m, 8)), e - 8)"),
     ("bf16_fp16_width", "return np.ldexp(np.rint(np.ldexp(m, 8)), e - 8)",
