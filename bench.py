@@ -102,28 +102,64 @@ def measured_ceilings():
     dst = torch.empty_like(src)
     ms = time_ms(lambda: dst.copy_(src), 5)
     copy = 2 * src.numel() * 4 / (ms * 1e-3) / 1e9
-    del src, dst
+    del dst
     torch.cuda.empty_cache()
     return {"bf16_gemm_tflops": round(gemm, 1), "gemm_shape": [n, n, n],
-            "d2d_copy_gbs": round(copy, 1), "copy_bytes": 1 << 32}
+            "d2d_copy_gbs": round(copy, 1), "copy_bytes": 1 << 32,
+            **hbm_read_ceiling(src)}
+
+
+def hbm_read_ceiling(buf=None):
+    """Read-only ceiling: ls_hbm_read_probe over a 4 GiB buffer (each byte read
+    once, 8 loads of 16 bytes in flight per lane, XOR of the words)."""
+    import torch
+    from paper_2607_14952_amd import binding as B
+    if buf is None:
+        buf = torch.empty(1 << 30, dtype=torch.float32, device="cuda")
+        buf.fill_(1.0)
+    out = torch.zeros(1, dtype=torch.int32, device=buf.device)
+    ms = time_ms(lambda: B.hbm_read_probe(buf, out), 10)
+    nbytes = buf.numel() * buf.element_size()
+    return {"hbm_read_gbs": round(nbytes / (ms * 1e-3) / 1e9, 1), "read_bytes": nbytes}
 
 
 def gpu_clocks():
-    """Current shader / memory clocks as rocm-smi reports them (None when unavailable).
-    Skipped under rocprofv3 (its ROCPROF_* variables are set): with counter
-    collection the profiler initialises the GPU in every child process too, and
-    rocm-smi starts through an interpreter that its launcher execs."""
-    import subprocess
-    if any(k.startswith("ROCPROF_") for k in os.environ):
-        return None
+    """The DPM levels of the shader and memory clocks, read in-process from the
+    amdgpu sysfs files (the level marked '*' is the current one; no tool is
+    started).  None when the files are not readable.  This is a snapshot after
+    the timed steps: the clock the chip holds under MFMA load comes from
+    counters (GRBM_GUI_ACTIVE over the kernel time, in the utilization
+    summaries)."""
+    import glob
+    out = {}
+    for path in sorted(glob.glob("/sys/class/drm/card*/device/pp_dpm_sclk")):
+        dev = os.path.dirname(path)
+        for name in ("pp_dpm_sclk", "pp_dpm_mclk"):
+            try:
+                with open(os.path.join(dev, name)) as f:
+                    lines = [ln.strip() for ln in f if ln.strip()]
+            except OSError:
+                continue
+            cur = [ln for ln in lines if ln.endswith("*")]
+            out[name] = {"levels": lines, "current": cur[0] if cur else None}
+        if out:
+            out["device"] = dev
+            break
+    return out or None
+
+
+def host_cpu():
+    """Logical CPUs this process may run on, and the CPU model."""
+    model = platform.processor() or platform.machine()
     try:
-        r = subprocess.run(["rocm-smi", "--showclocks", "--json"], stdout=subprocess.PIPE,
-                           stderr=subprocess.DEVNULL, text=True, timeout=20)
-        d = json.loads(r.stdout)
-        card = next(iter(d.values()))
-        return {k: v for k, v in card.items() if "sclk" in k.lower() or "mclk" in k.lower()}
-    except Exception:  # pragma: no cover - tool missing or output changed
-        return None
+        with open("/proc/cpuinfo") as f:
+            for ln in f:
+                if ln.lower().startswith("model name"):
+                    model = ln.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return len(os.sched_getaffinity(0)), model
 
 
 def bf16_numerator_cost(step, stream, reps=20):
@@ -193,7 +229,11 @@ def cpu_baseline(cfg, host, n_rows=16, n_shards=2):
                prefix_len=cfg.prefix_len, kv_begin=b, kv_end=e, **kw)
     dt = time.perf_counter() - t0
     fl = (4 + 6) * Hq * cfg.head_dim * n_rows * (e - b)
+    affinity, model = host_cpu()
     return {"value": fl / dt / 1e12, "unit": "TFLOP/s", "cores": int(blas_threads),
+            "cores_note": "BLAS threads the oracle ran on (its matmuls are the only "
+                          "multithreaded part)",
+            "affinity_cpus": affinity, "cpu_model": model, "blas_threads": int(blas_threads),
             "kind": "oracle",
             "sample": f"fp64 numpy oracle: split forward + dq of query rows 0..{n_rows - 1} "
                       f"(all {Hq} heads) over prefix keys [{b}, {e}) of the paged store; "
@@ -423,6 +463,9 @@ def main():
                     help="c5: select each row's top-k with the DSA index scores inside the step")
     ap.add_argument("--dsa-mode", choices=("global", "candidates"), default="global",
                     help="selection: one top-k per row, or per-shard candidates and a merge")
+    ap.add_argument("--streaming-only", action="store_true",
+                    help="c3 inputs: time only the page streaming pass (R = 16) and the read "
+                         "ceiling (for counter runs on that pass alone)")
     ap.add_argument("--skip-extras", action="store_true",
                     help="skip page streaming, measured ceilings and clocks (profiling runs: the "
                          "streaming pass reuses the forward kernel)")
@@ -466,6 +509,15 @@ def main():
     log(f"inputs ready in {time.perf_counter() - t:.1f} s; copying to HBM")
     dev = device_inputs(host)
     stream = torch.cuda.current_stream()
+    if args.streaming_only:
+        ps = page_streaming(cfg, dev)
+        del dev
+        torch.cuda.empty_cache()
+        ceil = hbm_read_ceiling()
+        ps["frac_of_read_ceiling"] = round(ps["gbs"] / ceil["hbm_read_gbs"], 4)
+        print(json.dumps({"page_streaming": ps, "read_ceiling": ceil,
+                          "gpu": torch.cuda.get_device_name(0)}), flush=True)
+        return
     step = ReplayStep(cfg, dev, backward=True, stream=stream)
     fwd_fl, bwd_fl = flops(cfg)
 
@@ -580,7 +632,6 @@ def main():
         torch.cuda.empty_cache()
         log("timing the CPU oracle sample")
         cb = cpu_baseline(cfg, host, args.cpu_rows)
-        cb["cpu"] = platform.processor() or platform.machine()
         result["cpu_baseline"] = {k: (round(v, 6) if isinstance(v, float) else v)
                                   for k, v in cb.items()}
     else:
@@ -592,6 +643,11 @@ def main():
         ceil["frac_of_gemm"] = round(value / ceil["bf16_gemm_tflops"], 4)
         ceil["roofline_frac_of_gemm"] = round(roofline["achieved"] / ceil["bf16_gemm_tflops"], 4)
         result["measured_ceilings"] = ceil
+        ps = result["page_streaming"]
+        ps["frac_of_read_ceiling"] = round(ps["gbs"] / ceil["hbm_read_gbs"], 4)
+        ps["frac_of_copy_ceiling"] = round(ps["gbs"] / ceil["d2d_copy_gbs"], 4)
+        result["merge_frac_of_hbm_peak"] = round(result["merge_gbs"] / PEAK_HBM_GBS, 4)
+        result["merge_frac_of_read_ceiling"] = round(result["merge_gbs"] / ceil["hbm_read_gbs"], 4)
     print(json.dumps(result), flush=True)
 
 

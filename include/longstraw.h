@@ -78,7 +78,9 @@ enum {
   LS_FLAG_CHECKED = 1u,        /* validate the page table (synchronous D2H copy) */
   LS_FLAG_ACCUMULATE_DQ = 4u,  /* backward: dq += contribution instead of dq = */
   LS_FLAG_ACCUMULATE_DKV = 8u, /* backward: dk/dv_resp += instead of = */
-  LS_FLAG_BF16_NUMERATOR = 16u /* merge: reduce the numerator in bf16 (see ls_lse_merge) */
+  LS_FLAG_BF16_NUMERATOR = 16u, /* merge: reduce the numerator in bf16 (see ls_lse_merge) */
+  LS_FLAG_PREP_READY = 32u      /* backward: the workspace already holds Delta and lse * log2(e)
+                                   (see ls_prefix_attn_bwd) */
 };
 
 /* One replay call: a block of n_q response rows against one paged KV store. */
@@ -192,7 +194,14 @@ size_t ls_prefix_attn_bwd_workspace_size(const ls_attn_params* p);
  * LS_FLAG_ACCUMULATE_DQ / LS_FLAG_ACCUMULATE_DKV select += over =.
  * workspace: device memory of ls_prefix_attn_bwd_workspace_size(p) bytes for
  *   the same p (it grows with the response length q_pos0 + n_q - prefix_len:
- *   the bf16 path keeps per-row-chunk dK/dV partial sums there).
+ *   the bf16 path keeps per-row-chunk dK/dV partial sums there).  Every call
+ *   first writes Delta_i = d_out_i . out_i and lse_i * log2(e) ([n_q_heads,
+ *   n_q] fp32 each) at the start of the workspace.  LS_FLAG_PREP_READY skips
+ *   that step: the caller asserts that an earlier call on the same stream, with
+ *   the same workspace, n_q, n_q_heads, d_out, out and lse, already wrote them
+ *   and nothing has overwritten them since (the key ranges of one backward
+ *   differ only in kv_begin/kv_end and the accumulate flags).  A workspace
+ *   without them gives wrong gradients, not an error.
  */
 ls_status ls_prefix_attn_bwd(const ls_attn_params* p, int64_t kv_begin, int64_t kv_end,
                              const void* d_out, const void* out, int32_t out_dtype,
@@ -205,11 +214,21 @@ ls_status ls_prefix_attn_bwd(const ls_attn_params* p, int64_t kv_begin, int64_t 
  * head_dim = 576 bf16 per position (n_kv_heads = 1, v_pool == k_pool); keys are
  * the whole row and values its first head_dim_v = 512 channels.  Query row t
  * (position q_pos0 + t) of every head attends to the prefix positions
- * idx[t][0 .. topk) (distinct, inside [0, prefix_len); int32 device array
- * [n_q, topk]) and to the response positions prefix_len .. q_pos0 + t.
- * n_q_heads must be a multiple of 128.  Positions outside the store are
- * clamped; duplicated or out-of-range indices are the caller's error
- * (LS_FLAG_CHECKED range-checks them on the host).
+ * idx[t][0 .. topk) (int32 device array [n_q, topk]) and to the response
+ * positions prefix_len .. q_pos0 + t.  An entry outside [0, prefix_len)
+ * selects no key: ls_topk_select pads a row with fewer than k candidates
+ * with -1, and a position at or past the prefix is already in the response
+ * window.  The selected positions of a row must be distinct (a duplicate
+ * would count twice); LS_FLAG_CHECKED copies idx to the host and rejects
+ * duplicates and entries that are neither -1 nor inside the prefix.
+ * n_q_heads must be a multiple of 128.
+ *
+ * The selection and the response window are one key set, so ls_sparse_attn_fwd
+ * returns the composed result directly (out and lse over the union) rather
+ * than one partial per part: the parts would only be merged again.  The
+ * workspace (size from ls_sparse_attn_workspace_size with backward = 0 or 1)
+ * holds each token's resolved key list and, for the backward, Delta, lse *
+ * log2(e) and dS; its contents need not survive between calls.
  */
 size_t ls_sparse_attn_workspace_size(const ls_attn_params* p, int32_t topk, int32_t backward);
 
@@ -270,6 +289,17 @@ ls_status ls_dsa_index_scores(const ls_dsa_params* p, int64_t pos_begin, int64_t
 ls_status ls_topk_select(const float* scores, int64_t ld, const int32_t* positions,
                          int32_t n_rows, int64_t n, int64_t pos_offset, int32_t k,
                          int32_t* out_pos, float* out_scores, int64_t out_ld, void* stream);
+
+/*
+ * ls_hbm_read_probe (measurement, not part of the replay path): reads `bytes`
+ * of device memory at buf once and XORs all its 32-bit words into *out
+ * (*out ^= XOR of the words; zero it first to get the XOR itself).  A
+ * read-only streaming pass with almost no arithmetic: its bytes per second are
+ * the read ceiling that the page streaming and the LSE merge are reported
+ * against.  buf 16-byte aligned, bytes a multiple of 16, out a 4-byte aligned
+ * device word outside buf.
+ */
+ls_status ls_hbm_read_probe(const void* buf, size_t bytes, uint32_t* out, void* stream);
 
 #ifdef __cplusplus
 }

@@ -256,8 +256,15 @@ def attn_bwd(q, k_pool, v_pool, page_table, d_out, *, page_size, prefix_len, q_p
 # sparse latent replay: Eq. dsa-attention over the selected prefix positions
 # --------------------------------------------------------------------------
 def _sparse_visible(idx_row, prefix_len, pos):
-    """Selected prefix positions, then the response positions up to ``pos``."""
-    return np.concatenate([np.asarray(idx_row, np.int64), np.arange(prefix_len, pos + 1)])
+    """Selected prefix positions, then the response positions up to ``pos``.
+
+    Eq. dsa-attention draws the selection from the prefix only.  An entry
+    outside ``[0, prefix_len)`` selects no key: the top-k pads a row that has
+    fewer than k candidates with -1, and a position at or past the prefix is
+    already in the response window."""
+    sel = np.asarray(idx_row, np.int64)
+    sel = sel[(sel >= 0) & (sel < prefix_len)]
+    return np.concatenate([sel, np.arange(prefix_len, pos + 1)])
 
 
 def sparse_fwd(q, latent_pool, page_table, idx, *, page_size, prefix_len, q_pos0, scale,

@@ -19,12 +19,13 @@ FLAG_CHECKED = 1
 FLAG_ACCUMULATE_DQ = 4
 FLAG_ACCUMULATE_DKV = 8
 FLAG_BF16_NUMERATOR = 16
+FLAG_PREP_READY = 32
 STATUS = {0: "LS_OK", -1: "LS_ERR_INVALID_ARG", -2: "LS_ERR_UNSUPPORTED", -3: "LS_ERR_WORKSPACE",
           -4: "LS_ERR_ALIAS", -5: "LS_ERR_STALE", -6: "LS_ERR_PAGE_OOB", -7: "LS_ERR_HIP"}
 EXPORTS = ["ls_abi_version", "ls_status_string", "ls_last_error", "ls_gather_kv", "ls_scatter_kv",
            "ls_prefix_attn_fwd", "ls_lse_merge", "ls_prefix_attn_bwd_workspace_size",
            "ls_prefix_attn_bwd", "ls_sparse_attn_workspace_size", "ls_sparse_attn_fwd",
-           "ls_sparse_attn_bwd", "ls_dsa_index_scores", "ls_topk_select"]
+           "ls_sparse_attn_bwd", "ls_dsa_index_scores", "ls_topk_select", "ls_hbm_read_probe"]
 
 
 class AttnParams(ctypes.Structure):
@@ -100,6 +101,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.ls_topk_select.restype = c_int32
     lib.ls_topk_select.argtypes = [c_void_p, c_int64, c_void_p, c_int32, c_int64, c_int64, c_int32,
                                    c_void_p, c_void_p, c_int64, c_void_p]
+    lib.ls_hbm_read_probe.restype = c_int32
+    lib.ls_hbm_read_probe.argtypes = [c_void_p, c_size_t, c_void_p, c_void_p]
     if lib.ls_abi_version() != ABI_VERSION:
         raise RuntimeError("liblongstraw ABI version mismatch")
     _lib = lib
@@ -411,3 +414,16 @@ def topk_select(scores, k: int, *, n: int | None = None, positions=None, pos_off
         _ptr(out_scores, torch.float32, "out_scores", dense=False), out_pos.stride(0),
         _stream(stream)))
     return out_pos, out_scores
+
+
+def hbm_read_probe(buf, out=None, *, stream=None):
+    """Read every byte of ``buf`` once (ls_hbm_read_probe); returns the int32
+    device word holding the XOR of its 32-bit words."""
+    torch = _torch()
+    if out is None:
+        out = torch.zeros(1, dtype=torch.int32, device=buf.device)
+    else:
+        out.zero_()
+    check(load_library().ls_hbm_read_probe(_ptr(buf, name="buf"), buf.numel() * buf.element_size(),
+                                           _ptr(out, torch.int32, "out"), _stream(stream)))
+    return out

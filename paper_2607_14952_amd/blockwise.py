@@ -118,7 +118,7 @@ class BlockwiseReplay:
         for r, (kb, ke) in enumerate(self.prefix_ranges + [(c.prefix_len, kv_end)]):
             B.prefix_attn_bwd(qb, self.prefix.kv, dob, out, lse, prefix_len=c.prefix_len,
                               q_pos0=q0, scale=c.scale, kv_begin=kb, kv_end=ke,
-                              flags=(B.FLAG_ACCUMULATE_DQ if r else 0)
+                              flags=((B.FLAG_ACCUMULATE_DQ | B.FLAG_PREP_READY) if r else 0)
                               | (0 if first else B.FLAG_ACCUMULATE_DKV),
                               dq=dq, dk_resp=self.dk[:kv_end - c.prefix_len],
                               dv_resp=self.dv[:kv_end - c.prefix_len], workspace=self.ws,

@@ -4,6 +4,7 @@
 #include <stdarg.h>
 #include <stdio.h>
 
+#include <algorithm>
 #include <string>
 #include <vector>
 
@@ -411,9 +412,12 @@ LS_API ls_status ls_prefix_attn_bwd(const ls_attn_params* p, int64_t kv_begin, i
   const BwdWorkspace wl = bwd_workspace_layout(p);
   float* delta = (float*)workspace;
   float* lse2 = (float*)((char*)workspace + wl.stat_bytes);
-  hipError_t e = ls::launch_bwd_prep(d_out, out, p->dtype == LS_BF16, out_dtype == LS_BF16, lse,
-                                     p->n_q, p->n_q_heads, p->head_dim_v, delta, lse2, s);
-  if (e != hipSuccess) return hip_fail(e, "backward prep launch");
+  hipError_t e = hipSuccess;
+  if (!(p->flags & LS_FLAG_PREP_READY)) {
+    e = ls::launch_bwd_prep(d_out, out, p->dtype == LS_BF16, out_dtype == LS_BF16, lse, p->n_q,
+                            p->n_q_heads, p->head_dim_v, delta, lse2, s);
+    if (e != hipSuccess) return hip_fail(e, "backward prep launch");
+  }
 
   ls::BwdArgs a;
   a.q = p->q;
@@ -453,11 +457,14 @@ LS_API ls_status ls_prefix_attn_bwd(const ls_attn_params* p, int64_t kv_begin, i
 // ---------------------------------------------------------------- sparse latent replay
 namespace {
 
+// Sparse workspace: the resolved key lists [n_q, n_max] int32 and their
+// lengths [n_q] int32 (both passes), then for the backward Delta and
+// lse * log2(e) [H, n_q] fp32 and dS [n_q, H, n_max] bf16; each padded to 256 B.
 struct SparseLayout {
   int64_t n_max;      // key-list length padded to a whole 32-key tile
-  size_t phys_bytes, stat_bytes, ds_bytes;
-  size_t fwd_bytes() const { return phys_bytes; }
-  size_t bwd_bytes() const { return phys_bytes + 2 * stat_bytes + ds_bytes; }
+  size_t phys_bytes, ntok_bytes, stat_bytes, ds_bytes;
+  size_t fwd_bytes() const { return phys_bytes + ntok_bytes; }
+  size_t bwd_bytes() const { return fwd_bytes() + 2 * stat_bytes + ds_bytes; }
 };
 
 size_t pad256(size_t x) { return (x + 255) / 256 * 256; }
@@ -467,6 +474,7 @@ SparseLayout sparse_layout(const ls_attn_params* p, int32_t topk) {
   const int64_t n = (int64_t)topk + (p->q_pos0 - p->prefix_len) + p->n_q;
   L.n_max = (n + 31) / 32 * 32;
   L.phys_bytes = pad256((size_t)p->n_q * L.n_max * 4);
+  L.ntok_bytes = pad256((size_t)p->n_q * 4);
   L.stat_bytes = pad256((size_t)p->n_q * p->n_q_heads * 4);
   L.ds_bytes = pad256((size_t)p->n_q * p->n_q_heads * L.n_max * 2);
   return L;
@@ -503,6 +511,7 @@ void fill_sparse(const ls_attn_params* p, const int32_t* idx, int32_t topk, cons
   a.page_table = p->page_table;
   a.idx = idx;
   a.phys = (int32_t*)ws;
+  a.ntok = (int32_t*)((char*)ws + L.phys_bytes);
   a.prefix_len = p->prefix_len;
   a.kv_len = kv_len_of(p);
   a.window0 = p->q_pos0 - p->prefix_len;
@@ -516,7 +525,8 @@ void fill_sparse(const ls_attn_params* p, const int32_t* idx, int32_t topk, cons
   a.accumulate_dq = (p->flags & LS_FLAG_ACCUMULATE_DQ) ? 1 : 0;
 }
 
-// Checked mode for the index lists: every selected position inside the prefix.
+// Checked mode for the index lists: every entry is a prefix position or the
+// -1 pad, and no row selects a position twice.
 ls_status check_idx(const ls_attn_params* p, const int32_t* idx, int32_t topk, hipStream_t s) {
   if (!(p->flags & LS_FLAG_CHECKED) || topk == 0) return LS_OK;
   std::vector<int32_t> host((size_t)p->n_q * topk);
@@ -524,8 +534,17 @@ ls_status check_idx(const ls_attn_params* p, const int32_t* idx, int32_t topk, h
   if (e == hipSuccess) e = hipStreamSynchronize(s);
   if (e != hipSuccess) return hip_fail(e, "checked mode: idx copy");
   for (size_t i = 0; i < host.size(); ++i)
-    if (host[i] < 0 || host[i] >= p->prefix_len)
-      return fail(LS_ERR_INVALID_ARG, "idx[%zu] = %d outside [0, prefix_len)", i, host[i]);
+    if (host[i] < -1 || host[i] >= p->prefix_len)
+      return fail(LS_ERR_INVALID_ARG, "idx[%zu] = %d neither -1 nor inside [0, prefix_len)", i,
+                  host[i]);
+  std::vector<int32_t> row((size_t)topk);
+  for (int32_t t = 0; t < p->n_q; ++t) {
+    row.assign(host.begin() + (size_t)t * topk, host.begin() + (size_t)(t + 1) * topk);
+    std::sort(row.begin(), row.end());
+    for (int32_t k = 1; k < topk; ++k)
+      if (row[k] >= 0 && row[k] == row[k - 1])
+        return fail(LS_ERR_INVALID_ARG, "idx row %d selects position %d twice", t, row[k]);
+  }
   return LS_OK;
 }
 
@@ -598,7 +617,7 @@ LS_API ls_status ls_sparse_attn_bwd(const ls_attn_params* p, const int32_t* idx,
   if ((st = check_idx(p, idx, topk, s)) != LS_OK) return st;
   ls::SparseArgs a = {};
   fill_sparse(p, idx, topk, L, workspace, a);
-  char* w = (char*)workspace + L.phys_bytes;
+  char* w = (char*)workspace + L.fwd_bytes();
   float* delta = (float*)w;
   float* lse2 = (float*)(w + L.stat_bytes);
   a.delta = delta;
@@ -692,4 +711,16 @@ LS_API ls_status ls_topk_select(const float* scores, int64_t ld, const int32_t* 
   a.k = k;
   hipError_t e = ls::launch_topk(a, (hipStream_t)stream);
   return e == hipSuccess ? LS_OK : hip_fail(e, "top-k launch");
+}
+
+LS_API ls_status ls_hbm_read_probe(const void* buf, size_t bytes, uint32_t* out, void* stream) {
+  if (!buf || !out || !aligned16(buf) || ((uintptr_t)out & 3u))
+    return fail(LS_ERR_INVALID_ARG, "buf must be 16-byte and out 4-byte aligned device pointers");
+  if (bytes % 16) return fail(LS_ERR_INVALID_ARG, "bytes must be a multiple of 16");
+  std::vector<Range> ins{rng("buf", buf, bytes)}, outs{rng("out", out, 4)};
+  ls_status st = check_alias(outs, ins);
+  if (st != LS_OK) return st;
+  if (bytes == 0) return LS_OK;
+  hipError_t e = ls::launch_hbm_read(buf, (int64_t)(bytes / 16), out, (hipStream_t)stream);
+  return e == hipSuccess ? LS_OK : hip_fail(e, "hbm read probe launch");
 }

@@ -94,8 +94,9 @@ struct SparseArgs {
   const void* q;             // [n_q, H, 576] bf16
   const void* latent;        // pool [n_phys, S, 1, 576] bf16
   const int32_t* page_table;
-  const int32_t* idx;        // [n_q, topk] selected prefix positions
+  const int32_t* idx;        // [n_q, topk] selected prefix positions (others: no key)
   int32_t* phys;             // workspace [n_q, n_max] physical latent rows
+  int32_t* ntok;             // workspace [n_q] keys in each token's list
   float* out;                // [n_q, H, 512] fp32 normalized
   float* lse;                // [H, n_q]
   const void* d_out;         // [n_q, H, 512] bf16
@@ -125,6 +126,7 @@ hipError_t launch_merge(const float* out_part, const float* lse_part, int n_spli
                         int n_heads, int dv, bool out_bf16, bool bf16_numerator, void* out,
                         float* lse, hipStream_t stream);
 hipError_t launch_fwd_f32(const FwdArgs& a, hipStream_t stream);
+hipError_t launch_hbm_read(const void* buf, int64_t n16, uint32_t* out, hipStream_t stream);
 hipError_t launch_dsa_scores(const DsaArgs& a, hipStream_t stream);
 hipError_t launch_topk(const TopkArgs& a, hipStream_t stream);
 hipError_t launch_fwd_bf16_d256(const FwdArgs& a, hipStream_t stream);

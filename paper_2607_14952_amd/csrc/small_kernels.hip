@@ -1,5 +1,6 @@
 // Bandwidth-bound kernels of the replay path: the page-table gather, the
-// log-sum-exp merge of split results, and the backward row statistics.
+// log-sum-exp merge of split results, and the backward row statistics; and a
+// read-only streaming probe that measures the HBM read ceiling.
 #include <math.h>
 
 #include "ls_internal.h"
@@ -165,6 +166,32 @@ __global__ __launch_bounds__(256) void prep_kernel(const TD* __restrict__ d_out,
   }
 }
 
+// ---------------------------------------------------------------- HBM read probe
+// Reads n16 16-byte units once and XORs their 32-bit words: a read-only
+// streaming pass with no arithmetic to speak of, the measured read ceiling the
+// bandwidth-bound kernels are compared with.  Each thread keeps 8 loads of 16
+// bytes in flight; a wave's XOR goes to *out with one atomic.
+__global__ __launch_bounds__(256) void hbm_read_kernel(const u32x4* __restrict__ buf,
+                                                       int64_t n16, uint32_t* __restrict__ out) {
+  constexpr int kU = 8;
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  uint32_t x = 0;
+  int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  for (; i + (kU - 1) * stride < n16; i += kU * stride) {
+    u32x4 v[kU];
+#pragma unroll
+    for (int u = 0; u < kU; ++u) v[u] = __builtin_nontemporal_load(buf + i + u * stride);
+#pragma unroll
+    for (int u = 0; u < kU; ++u) x ^= v[u][0] ^ v[u][1] ^ v[u][2] ^ v[u][3];
+  }
+  for (; i < n16; i += stride) {
+    const u32x4 v = buf[i];
+    x ^= v[0] ^ v[1] ^ v[2] ^ v[3];
+  }
+  for (int off = 32; off > 0; off >>= 1) x ^= (uint32_t)__shfl_xor((int)x, off);
+  if ((threadIdx.x & 63) == 0) atomicXor(out, x);
+}
+
 }  // namespace
 
 hipError_t launch_gather(const void* k_pool, const void* v_pool, const int32_t* page_table,
@@ -225,6 +252,12 @@ hipError_t launch_bwd_prep(const void* d_out, const void* out, bool dout_bf16, b
   else if (out_bf16) LS_PREP(float, __bf16);
   else LS_PREP(float, float);
 #undef LS_PREP
+  return hipGetLastError();
+}
+
+hipError_t launch_hbm_read(const void* buf, int64_t n16, uint32_t* out, hipStream_t stream) {
+  hipLaunchKernelGGL(hbm_read_kernel, dim3(2048), dim3(256), 0, stream, (const u32x4*)buf, n16,
+                     out);
   return hipGetLastError();
 }
 

@@ -58,7 +58,7 @@ __global__ __launch_bounds__(256, 1) void sparse_fwd_kernel(SparseArgs a) {
   const int l32 = lane & 31, hh = lane >> 5;
   const int t = a.n_q - 1 - (int)blockIdx.x;
   const int head = blockIdx.y * 128 + w * 32 + l32;
-  const int n_t = a.topk + (int)a.window0 + t + 1;
+  const int n_t = a.ntok[t];
   const int n_tiles = (n_t + kKeys - 1) / kKeys;
   const __amdgpu_buffer_rsrc_t phys_t = phys_rsrc(a, t);
   const __amdgpu_buffer_rsrc_t pool = pool_rsrc(a.latent);

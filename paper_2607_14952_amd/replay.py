@@ -134,13 +134,16 @@ class ReplayStep:
 
     def backward_range(self, r: int):
         """dq contribution of shard range r (accumulated after the first range);
-        the response range also writes the response dK/dV."""
+        the response range also writes the response dK/dV.  Ranges after the
+        first reuse the Delta and lse * log2(e) the first one left in the
+        workspace, so ranges must run in order, starting at 0."""
         c = self.cfg
         b, e = self.shards[r]
         kv = self.shard_kv[r] if self.cyclic else self.kv
         B.prefix_attn_bwd(self.dev["q"], kv, self.dev["d_out"], self.out, self.lse,
                           prefix_len=c.prefix_len, q_pos0=c.q_pos0, scale=c.scale,
-                          kv_begin=b, kv_end=e, flags=B.FLAG_ACCUMULATE_DQ if r > 0 else 0,
+                          kv_begin=b, kv_end=e,
+                          flags=(B.FLAG_ACCUMULATE_DQ | B.FLAG_PREP_READY) if r > 0 else 0,
                           dq=self.dq, dk_resp=self.dk, dv_resp=self.dv, workspace=self.ws,
                           stream=self.stream)
 

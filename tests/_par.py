@@ -1,0 +1,138 @@
+"""Run the fp64 oracle over large inputs in a thread pool (test harness only).
+
+The oracle computes each call from its definition with full score rows; at
+2M keys one call would hold gigabytes of fp64 temporaries and run on one core.
+These helpers split the keys into ranges and the rows into chunks, call the
+oracle on each piece in a thread (BLAS limited to one thread per piece), and
+compose the pieces with the oracle's own rules:
+
+* forward ranges compose through ``O.lse_merge`` (Eq. qwen-lse-parts and
+  qwen-global-attn; pinned: split + merge equals unsplit);
+* dq contributions of a key partition add up (Eq. qwen-dq-reduce; pinned by the
+  partition pin), and response dK/dV come from the response range alone;
+* sparse rows are independent.
+"""
+from __future__ import annotations
+
+import os
+import time
+from concurrent.futures import ThreadPoolExecutor
+
+import numpy as np
+
+import oracle as O
+
+
+def workers() -> int:
+    return max(1, min(16, len(os.sched_getaffinity(0))))
+
+
+def _pool_map(fn, items):
+    """fn over items on the thread pool, in order; prints a line as each
+    eighth of the pieces completes."""
+    from concurrent.futures import as_completed
+    from threadpoolctl import threadpool_limits
+    items = list(items)
+    t0 = time.perf_counter()
+    with threadpool_limits(limits=1), ThreadPoolExecutor(max_workers=workers()) as ex:
+        futs = {ex.submit(fn, it): i for i, it in enumerate(items)}
+        res = [None] * len(items)
+        step = max(1, len(items) // 8)
+        for n, f in enumerate(as_completed(futs), 1):
+            res[futs[f]] = f.result()
+            if n % step == 0 or n == len(items):
+                print(f"[oracle]   {n}/{len(items)} pieces, {time.perf_counter() - t0:.1f} s",
+                      flush=True)
+    return res
+
+
+def key_ranges(begin, end, piece=65536):
+    b = np.arange(begin, end, piece)
+    return [(int(x), int(min(x + piece, end))) for x in b]
+
+
+def _chunks(rows, n):
+    rows = np.asarray(rows)
+    return [c for c in np.array_split(rows, max(1, min(n, rows.size))) if c.size]
+
+
+def dense_fwd(h, *, page_size, q_pos0, scale, rows, prefix_len, piece=65536):
+    """Full-row out and lse of ``rows`` (over every visible key): each chunk of
+    rows is the merge of per-range oracle results over prefix ranges of
+    ``piece`` keys and the response range."""
+    rows = np.asarray(rows)
+    kv_len = q_pos0 + h["q"].shape[0]
+    ranges = key_ranges(0, prefix_len, piece) + [(prefix_len, kv_len)]
+    n_chunks = max(1, (4 * workers()) // len(ranges))
+    chunks = _chunks(rows, n_chunks)
+    t0 = time.perf_counter()
+
+    def one(task):
+        r, c = task
+        return O.attn_fwd(h["q"], h["k_pool"], h["v_pool"], h["page_table"], page_size=page_size,
+                          q_pos0=q_pos0, scale=scale, kv_begin=r[0], kv_end=r[1], rows=c)
+
+    tasks = [(r, c) for c in chunks for r in ranges]
+    parts = _pool_map(one, tasks)
+    os_, ls_ = [], []
+    for i in range(len(chunks)):
+        p = parts[i * len(ranges):(i + 1) * len(ranges)]
+        o, lse = O.lse_merge([x[0] for x in p], [x[1] for x in p])
+        os_.append(o)
+        ls_.append(lse)
+    print(f"[oracle] dense fwd: {rows.size} rows x {kv_len} keys in {len(ranges)} ranges, "
+          f"{time.perf_counter() - t0:.1f} s", flush=True)
+    return np.concatenate(os_), np.concatenate(ls_, axis=1)
+
+
+def dense_bwd(h, *, page_size, q_pos0, scale, prefix_len, rows, resp_keys, out, lse,
+              piece=65536, resp_piece=512):
+    """dq of ``rows`` over every visible key and the dK/dV of the response keys
+    ``resp_keys``, given the oracle's full-row ``out``/``lse`` arrays ([R, Hq, Dv]
+    / [Hq, R], filled at least for the rows that need them).  The keys are cut
+    into prefix ranges of ``piece`` and response ranges of ``resp_piece``: dq is
+    the sum of the ranges' contributions, and a response key's dK/dV come from
+    the one range holding it (they depend only on that key's column of P and
+    dS)."""
+    rows = np.asarray(rows)
+    resp_keys = np.unique(np.asarray(resp_keys, np.int64))
+    kv_len = q_pos0 + h["q"].shape[0]
+    ranges = key_ranges(0, prefix_len, piece) + key_ranges(prefix_len, kv_len, resp_piece)
+    t0 = time.perf_counter()
+    kw = dict(page_size=page_size, prefix_len=prefix_len, q_pos0=q_pos0, scale=scale, out=out,
+              lse=lse, rows=rows)
+
+    def one(r):
+        keys = resp_keys[(resp_keys >= r[0]) & (resp_keys < r[1])]
+        return O.attn_bwd(h["q"], h["k_pool"], h["v_pool"], h["page_table"], h["d_out"],
+                          kv_begin=r[0], kv_end=r[1], resp_keys=keys, **kw)
+
+    parts = _pool_map(one, ranges)
+    dq = sum(p[0] for p in parts)
+    dk = np.concatenate([p[1] for p in parts])
+    dv = np.concatenate([p[2] for p in parts])
+    print(f"[oracle] dense bwd: {rows.size} dq rows, {resp_keys.size} response keys, "
+          f"{time.perf_counter() - t0:.1f} s", flush=True)
+    return dq, dk, dv
+
+
+def sparse(h, *, page_size, prefix_len, q_pos0, scale, rows, backward=True, head_dim_v=512):
+    """Sparse forward (and dq) of ``rows``, row chunks in parallel."""
+    kw = dict(page_size=page_size, prefix_len=prefix_len, q_pos0=q_pos0, scale=scale,
+              head_dim_v=head_dim_v)
+    t0 = time.perf_counter()
+    chunks = _chunks(rows, 4 * workers())
+
+    def one(c):
+        o, l = O.sparse_fwd(h["q"], h["latent_pool"], h["page_table"], h["idx"], rows=c, **kw)
+        dq = (O.sparse_bwd(h["q"], h["latent_pool"], h["page_table"], h["idx"], h["d_out"],
+                           rows=c, **kw) if backward else None)
+        return o, l, dq
+
+    parts = _pool_map(one, chunks)
+    o = np.concatenate([p[0] for p in parts])
+    lse = np.concatenate([p[1] for p in parts], axis=1)
+    dq = np.concatenate([p[2] for p in parts]) if backward else None
+    print(f"[oracle] sparse: {np.asarray(rows).size} rows in {time.perf_counter() - t0:.1f} s",
+          flush=True)
+    return o, lse, dq

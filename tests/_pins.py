@@ -338,6 +338,44 @@ def pin_sparse_subset(O):
     assert rel_l2(dq, num) < 1e-6, f"sparse dq vs finite differences {rel_l2(dq, num):.2e}"
 
 
+def pin_sparse_invalid_entries(O):
+    """Selection entries outside the prefix select nothing: a row whose entries
+    are all -1 pads sees only its response window (the first row: its own
+    latent row, so o = its first Dv channels and lse = s), and a selection with
+    pads or out-of-prefix entries equals brute force over its valid entries."""
+    t, Dv = _latent(P=20, R=4, seed=16)
+    idx = np.array([[-1, -1, -1, -1, -1],
+                    [3, -1, 11, -1, -1],
+                    [0, 19, 20, 22, -1],      # 20 and 22 are response positions: no key
+                    [5, 6, 7, 8, 9]], dtype=np.int32)
+    so, sl = O.sparse_fwd(t.q, t.k_pool, t.page_table, idx, page_size=t.S, prefix_len=t.P,
+                          q_pos0=t.P, scale=t.scale, head_dim_v=Dv)
+    own = t.k_pool[t.page_table[t.P // t.S], t.P % t.S, 0]
+    _close(so[0], np.broadcast_to(own[:Dv], so[0].shape), 1e-13, "pads only: o = own value")
+    _close(sl[:, 0], t.scale * (t.q[0] @ own), 1e-13, "pads only: lse = own score")
+    for i in range(t.R):
+        keys = [j for j in idx[i] if 0 <= j < t.P] + list(range(t.P, t.P + i + 1))
+        C = np.stack([t.k_pool[t.page_table[j // t.S], j % t.S, 0] for j in keys])
+        for h in range(t.q.shape[1]):
+            s = t.scale * C @ t.q[i, h]
+            w = np.exp(s - s.max())
+            _close(so[i, h], (w / w.sum()) @ C[:, :Dv], 1e-12, "sparse pads brute o")
+            _close(sl[h, i], s.max() + np.log(w.sum()), 1e-12, "sparse pads brute lse")
+    d_out = t.d_out[..., :Dv]
+    dq = O.sparse_bwd(t.q, t.k_pool, t.page_table, idx, d_out, page_size=t.S, prefix_len=t.P,
+                      q_pos0=t.P, scale=t.scale, head_dim_v=Dv)
+    for i in range(t.R):
+        keys = [j for j in idx[i] if 0 <= j < t.P] + list(range(t.P, t.P + i + 1))
+        C = np.stack([t.k_pool[t.page_table[j // t.S], j % t.S, 0] for j in keys])
+        for h in range(t.q.shape[1]):
+            s = t.scale * C @ t.q[i, h]
+            P_ = np.exp(s - s.max())
+            P_ /= P_.sum()
+            o = P_ @ C[:, :Dv]
+            dS = P_ * (C[:, :Dv] @ d_out[i, h] - d_out[i, h] @ o)
+            _close(dq[i, h], t.scale * dS @ C, 1e-12, "sparse pads brute dq")
+
+
 # ---------------------------------------------------------------- input decoding
 def pin_decode(O):
     """bf16 bit patterns decode to the values the bfloat16 format defines
@@ -520,6 +558,6 @@ def pin_topk_local_candidates_merge(O):
 ALL_PINS = [pin_single_key, pin_identical_keys, pin_zero_query, pin_scale_and_gqa,
             pin_merge_closed_form, pin_split_merge_invariance, pin_causal, pin_gather_bruteforce,
             pin_finite_differences, pin_bwd_partition, pin_torch_autograd, pin_sampled_rows,
-            pin_sparse_full_index_is_dense, pin_sparse_subset, pin_decode, pin_bf16_round,
+            pin_sparse_full_index_is_dense, pin_sparse_subset, pin_sparse_invalid_entries, pin_decode, pin_bf16_round,
             pin_bf16_numerator_merge, pin_cyclic_ownership, pin_dsa_index_closed_form,
             pin_topk_ties_and_order, pin_topk_local_candidates_merge]

@@ -14,6 +14,7 @@ import oracle as O
 from paper_2607_14952_amd import binding as B
 from paper_2607_14952_amd import configs, inputs
 from paper_2607_14952_amd.replay import ReplayStep, device_inputs
+from tests import _par
 from tests._gpu import announce, host, lse_err, oracle_bkw, oracle_kw, rel_l2, tol
 
 pytestmark = pytest.mark.gpu
@@ -227,6 +228,30 @@ def test_bf16_blockwise_q_pos0():
     assert rel_l2(host(dv), dv_ref) <= 1e-2
 
 
+def test_prep_ready_matches_fresh_prep():
+    """ReplayStep runs the prep (Delta, lse * log2(e)) once per backward and
+    passes LS_FLAG_PREP_READY for the later key ranges; the gradients are
+    bitwise those of calls that each compute their own prep."""
+    import torch
+    cfg = BF16_SMALL.scaled(name="bf16_prep", n_shards=3)
+    dev = device_inputs(inputs.dense_inputs(cfg))
+    step = ReplayStep(cfg, dev, backward=True)
+    announce("prep reuse: step")
+    step.step()
+    kv = _kv(dev)
+    dq = dk = dv = None
+    announce("prep reuse: fresh prep per range")
+    for r, (b, e) in enumerate(step.shards):
+        dq, dk, dv = B.prefix_attn_bwd(dev["q"], kv, dev["d_out"], step.out, step.lse,
+                                       prefix_len=cfg.prefix_len, q_pos0=cfg.q_pos0,
+                                       scale=cfg.scale, kv_begin=b, kv_end=e,
+                                       flags=B.FLAG_ACCUMULATE_DQ if r else 0, dq=dq, dk_resp=dk,
+                                       dv_resp=dv)
+    torch.cuda.synchronize()
+    assert len(step.shards) == 4
+    assert torch.equal(dq, step.dq) and torch.equal(dk, step.dk) and torch.equal(dv, step.dv)
+
+
 # ------------------------------------------------------------------ invariants
 def test_determinism_layout_and_causality():
     cfg = BF16_SMALL.scaled(name="bf16_inv", prefix_len=4096, resp_len=130)
@@ -284,7 +309,11 @@ def test_checked_mode_rejects_bad_page():
 
 
 # ------------------------------------------------------------------ full-size, sampled
-def _sampled_parity(cfg, rows, backward):
+def _sampled_parity(cfg, rows, backward, keys=()):
+    """The step as bench.py times it, against the oracle on sampled rows (and,
+    with backward, their dq plus the response keys ``keys`` (offsets from
+    prefix_len) and the last two, whose dK/dV need every row that sees them).
+    The oracle runs over key ranges in a thread pool (tests/_par.py)."""
     h = inputs.dense_inputs(cfg, with_dout=backward)
     if cfg.plant_frac:
         rows = sorted(set(rows) | set(int(r) for r in h["planted"][1][:2]))
@@ -294,39 +323,55 @@ def _sampled_parity(cfg, rows, backward):
     step.step()
     import torch
     torch.cuda.synchronize()
-    rows = np.array(rows)
-    o_ref, l_ref = O.attn_fwd(h["q"], h["k_pool"], h["v_pool"], h["page_table"], rows=rows,
-                              **oracle_kw(cfg))
-    assert rel_l2(host(step.out)[rows], o_ref) <= 5e-3
-    assert lse_err(host(step.lse)[:, rows], l_ref) <= 1e-3
+    R = cfg.resp_len
+    rows = np.unique(np.asarray(rows))
+    keys = np.unique(np.concatenate([np.asarray(keys, np.int64), [R - 2, R - 1]])) + cfg.prefix_len
+    need = np.union1d(rows, np.arange(int(keys.min()) - cfg.prefix_len, R)) if backward else rows
+    kw = dict(oracle_kw(cfg), prefix_len=cfg.prefix_len)
+    o_n, l_n = _par.dense_fwd(h, rows=need, **kw)
+    assert rel_l2(host(step.out)[need], o_n) <= 5e-3, "out"
+    assert lse_err(host(step.lse)[:, need], l_n) <= 1e-3, "lse"
     if backward:
-        R = cfg.resp_len
-        keys = np.array([cfg.kv_len - 2, cfg.kv_len - 1])
-        need = np.union1d(rows, [R - 2, R - 1])
         o_full = np.zeros((R, cfg.n_q_heads, cfg.head_dim_v))
         l_full = np.zeros((cfg.n_q_heads, R))
-        o_n, l_n = O.attn_fwd(h["q"], h["k_pool"], h["v_pool"], h["page_table"], rows=need,
-                              **oracle_kw(cfg))
         o_full[need], l_full[:, need] = o_n, l_n
-        dq_ref, dk_ref, dv_ref = O.attn_bwd(h["q"], h["k_pool"], h["v_pool"], h["page_table"],
-                                            h["d_out"], rows=rows, resp_keys=keys, out=o_full,
-                                            lse=l_full, **oracle_bkw(cfg))
-        assert rel_l2(host(step.dq)[rows], dq_ref) <= 1e-2
-        assert rel_l2(host(step.dk)[keys - cfg.prefix_len], dk_ref) <= 1e-2
-        assert rel_l2(host(step.dv)[keys - cfg.prefix_len], dv_ref) <= 1e-2
+        dq_ref, dk_ref, dv_ref = _par.dense_bwd(h, rows=rows, resp_keys=keys, out=o_full,
+                                                lse=l_full, **kw)
+        assert rel_l2(host(step.dq)[rows], dq_ref) <= 1e-2, "dq"
+        for j, k in enumerate(keys - cfg.prefix_len):
+            assert rel_l2(host(step.dk)[k], dk_ref[j]) <= 1e-2, f"dk of response key {k}"
+            assert rel_l2(host(step.dv)[k], dv_ref[j]) <= 1e-2, f"dv of response key {k}"
+
+
+def _wg_boundary_rows(n_tokens, tokens_per_wg, every=1, inner=()):
+    """First and last token of every `every`-th workgroup (plus `inner` offsets)."""
+    out = []
+    for b in range(0, n_tokens, tokens_per_wg * every):
+        out += [b, b + tokens_per_wg - 1] + [b + o for o in inner]
+    return [r for r in out if r < n_tokens]
 
 
 @pytest.mark.timeout(900)
 def test_c2_full_size_sampled():
-    _sampled_parity(configs.C2, [0, 1, 1000, 2047, 4095], backward=False)
+    """512 rows: the first and last token of each of the 128 forward
+    workgroups of a (KV head, split) stream (32 tokens x 8 heads = 256 packed
+    rows each), and 256 seeded rows."""
+    R = configs.C2.resp_len
+    rows = _wg_boundary_rows(R, 32)
+    rows += list(np.random.default_rng(22).choice(R, 256, replace=False))
+    _sampled_parity(configs.C2, rows, backward=False)
 
 
 @pytest.mark.timeout(900)
 def test_c3_full_size_sampled():
-    """c3 as bench.py times it; rows on both sides of the dq (16-token) and
-    forward (32-token) workgroup boundaries, the middle, the last, and planted
-    targets."""
-    _sampled_parity(configs.C3, [0, 15, 16, 31, 32, 2048, 4095], backward=True)
+    """c3 as bench.py times it.  dq on 64+ rows: both sides of the dq (16-token)
+    and forward (32-token) workgroup boundaries in every 8th forward workgroup,
+    the last row, and planted targets.  Response key 3838 is seen by tokens
+    3838 .. 4095, which span the dK/dV row chunks 14 and 15 (256 tokens x 8
+    heads = 2048 packed rows each), so its gradient goes through the ordered
+    chunk reduction at full size; those 258 rows' out and lse are compared too."""
+    rows = _wg_boundary_rows(configs.C3.resp_len, 32, every=8, inner=(15, 16)) + [4095]
+    _sampled_parity(configs.C3, rows, backward=True, keys=[3838])
 
 
 @pytest.mark.timeout(900)
@@ -336,3 +381,30 @@ def test_c3_cyclic_bf16_numerator_full_size_sampled():
     bf16; sampled rows and response keys against the unsharded fp64 oracle."""
     _sampled_parity(configs.C3.scaled(ownership="cyclic", bf16_numerator=True), [1, 3000, 4094],
                     backward=True)
+
+
+def test_response_full_chunk_reduction():
+    """The c3 response geometry (4,096 tokens, 16 query heads on 2 KV heads: 16
+    dK/dV row chunks x 32 key blocks x 2 heads) over a 2,048-position prefix:
+    every response key's dK/dV, and every row's out, lse and dq, in full."""
+    cfg = configs.C3.scaled(name="c3_resp_geometry", prefix_len=2048, n_shards=1,
+                            splits_per_shard=1, plant_frac=0.0)
+    h = inputs.dense_inputs(cfg)
+    dev = device_inputs(h)
+    announce(cfg.name)
+    step = ReplayStep(cfg, dev, backward=True)
+    step.step()
+    import torch
+    torch.cuda.synchronize()
+    R = cfg.resp_len
+    rows = np.arange(R)
+    kw = dict(oracle_kw(cfg), prefix_len=cfg.prefix_len)
+    o_n, l_n = _par.dense_fwd(h, rows=rows, piece=1024, **kw)
+    assert rel_l2(host(step.out), o_n) <= 5e-3
+    assert lse_err(host(step.lse), l_n) <= 1e-3
+    keys = cfg.prefix_len + np.arange(R)
+    dq_ref, dk_ref, dv_ref = _par.dense_bwd(h, rows=rows, resp_keys=keys, out=o_n, lse=l_n,
+                                            piece=1024, **kw)
+    assert rel_l2(host(step.dq), dq_ref) <= 1e-2
+    assert rel_l2(host(step.dk), dk_ref) <= 1e-2
+    assert rel_l2(host(step.dv), dv_ref) <= 1e-2

@@ -6,10 +6,10 @@ from __future__ import annotations
 import numpy as np
 import pytest
 
-import oracle as O
 from paper_2607_14952_amd import binding as B
 from paper_2607_14952_amd import configs, inputs
 from paper_2607_14952_amd.replay import to_device
+from tests import _par
 from tests._gpu import announce, host, lse_err, rel_l2
 
 pytestmark = pytest.mark.gpu
@@ -39,15 +39,12 @@ def run(cfg, h, *, q_pos0=None, rows=None, backward=True):
         dq = B.sparse_attn_bwd(q, kv, idx, to_device(h["d_out"]), out_b, lse,
                                prefix_len=cfg.prefix_len, q_pos0=q_pos0, scale=cfg.scale)
     torch.cuda.synchronize()
-    kw = dict(page_size=cfg.page_size, prefix_len=cfg.prefix_len, q_pos0=q_pos0,
-              scale=cfg.scale, head_dim_v=512)
+    kw = dict(page_size=cfg.page_size, prefix_len=cfg.prefix_len, q_pos0=q_pos0, scale=cfg.scale)
     r = np.arange(h["q"].shape[0]) if rows is None else np.asarray(rows)
-    o_ref, l_ref = O.sparse_fwd(h["q"], h["latent_pool"], h["page_table"], h["idx"], rows=r, **kw)
+    o_ref, l_ref, dq_ref = _par.sparse(h, rows=r, backward=backward, **kw)
     assert rel_l2(host(out)[r], o_ref) <= 5e-3, "sparse out"
     assert lse_err(host(lse)[:, r], l_ref) <= 1e-3, "sparse lse"
     if backward:
-        dq_ref = O.sparse_bwd(h["q"], h["latent_pool"], h["page_table"], h["idx"], h["d_out"],
-                              rows=r, **kw)
         assert rel_l2(host(dq)[r], dq_ref) <= 1e-2, f"sparse dq {rel_l2(host(dq)[r], dq_ref):.2e}"
 
 
@@ -86,7 +83,55 @@ def test_sparse_two_to_four_tiles():
     run(cfg, inputs.sparse_inputs(cfg))
 
 
+def test_sparse_invalid_entries_select_nothing():
+    """Selections padded with -1 (what the top-k writes for a row with fewer
+    candidates than k) and entries at or past the prefix select no key: a row
+    of pads only, rows with pads interleaved, rows whose pads fill whole tiles,
+    and response positions inside the selection.  The oracle drops the same
+    entries."""
+    cfg = SMALL.scaled(name="c5_pads", resp_len=40, topk=160)
+    h = inputs.sparse_inputs(cfg)
+    idx = h["idx"].copy()
+    rng = np.random.default_rng(9)
+    idx[0] = -1                                    # only the response window
+    idx[1, 100:] = -1                              # a short selection, padded at the end
+    idx[2, ::3] = -1                               # pads interleaved
+    idx[3, :64] = -1                               # two whole tiles of pads first
+    idx[4, 10:20] = cfg.prefix_len + np.arange(10) # response positions: no key
+    idx[5, 5] = cfg.prefix_len + 39                # a position past this row's window
+    idx[6, 7] = -7                                 # another negative value
+    idx[7] = np.sort(rng.choice(cfg.prefix_len, cfg.topk, replace=False))
+    h = dict(h, idx=idx)
+    run(cfg, h)
+
+
+def test_sparse_checked_mode_index_validation():
+    """Checked mode accepts -1 pads and rejects duplicates and other values
+    outside the prefix, before launching anything."""
+    import torch
+    cfg = SMALL.scaled(name="c5_checked", resp_len=8, topk=64)
+    h = inputs.sparse_inputs(cfg)
+    q = to_device(h["q"])
+    lat = to_device(h["latent_pool"])
+    kv = B.PagedKV(lat, lat, to_device(h["page_table"]))
+    kw = dict(prefix_len=cfg.prefix_len, q_pos0=cfg.q_pos0, scale=cfg.scale, flags=B.FLAG_CHECKED)
+    announce("sparse checked mode")
+    ok = h["idx"].copy()
+    ok[2, 40:] = -1
+    B.sparse_attn_fwd(q, kv, to_device(ok), **kw)
+    torch.cuda.synchronize()
+    for bad, what in ((lambda a: a.__setitem__((3, 5), a[3, 4]), "duplicate"),
+                      (lambda a: a.__setitem__((1, 0), -2), "-2"),
+                      (lambda a: a.__setitem__((0, 9), cfg.prefix_len), "prefix_len")):
+        x = h["idx"].copy()
+        bad(x)
+        with pytest.raises(B.LongStrawError) as ei:
+            B.sparse_attn_fwd(q, kv, to_device(x), **kw)
+        assert ei.value.name == "LS_ERR_INVALID_ARG", what
+
+
 @pytest.mark.timeout(900)
-def test_c5_full_size_sampled():
+def test_c5_full_size():
+    """c5 as bench.py times it: every row's out, lse and dq."""
     cfg = configs.C5
-    run(cfg, inputs.sparse_inputs(cfg), rows=[0, 1, 1023, 2047])
+    run(cfg, inputs.sparse_inputs(cfg))

@@ -39,6 +39,9 @@ MUTATIONS = [
     ("sparse_values_tail", "o[k_] = (w / z[:, None]) @ C[:, :head_dim_v]",
      "o[k_] = (w / z[:, None]) @ C[:, -head_dim_v:]"),
     ("sparse_dq_no_delta", "dS = P * (dP - delta[:, None])\n        dq[k_]", "dS = P * dP\n        dq[k_]"),
+    ("sparse_pads_clamped", "sel = sel[(sel >= 0) & (sel < prefix_len)]",
+     "sel = np.clip(sel, 0, prefix_len - 1)"),
+    ("sparse_pads_kept_past_prefix", "sel = sel[(sel >= 0) & (sel < prefix_len)]", "sel = sel[sel >= 0]"),
     ("decode_shift_15", "return (x.astype(np.uint32) << np.uint32(16))",
      "return (x.astype(np.uint32) << np.uint32(15))"),
     ("decode_as_fp16", "return (x.astype(np.uint32) << np.uint32(16)).view(np.float32).astype(np.float64)",
