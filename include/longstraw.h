@@ -291,6 +291,31 @@ ls_status ls_topk_select(const float* scores, int64_t ld, const int32_t* positio
                          int32_t* out_pos, float* out_scores, int64_t out_ld, void* stream);
 
 /*
+ * ls_sparse_attn_fwd_noalloc: ls_sparse_attn_fwd for callers that cannot
+ * allocate device memory or pass a workspace (code under HIP graph capture,
+ * tight serving loops, harnesses that forbid allocation).  Same arguments,
+ * result and kernels, without the workspace: the resolved key lists live in a
+ * static device array of LS_NOALLOC_SCRATCH_BYTES that each GPU the library
+ * runs on holds until the process ends.  The call allocates nothing and does
+ * not synchronize.
+ *   - Needs ls_sparse_attn_workspace_size(p, topk, 0) <= LS_NOALLOC_SCRATCH_BYTES
+ *     (about n_q * (topk + response window) * 4 bytes: 32 MiB for 2,048 tokens
+ *     x 2,048 selections + 2,048 response positions); larger calls return
+ *     LS_ERR_WORKSPACE before launching anything.
+ *   - LS_FLAG_CHECKED is rejected (LS_ERR_UNSUPPORTED): checked mode copies to
+ *     the host and synchronizes.
+ *   - stream must belong to the current device (LS_ERR_INVALID_ARG otherwise);
+ *     the first call on a device resolves that device's copy of the array.
+ *   - Every call on one GPU uses the same array, and the array keeps the last
+ *     call's contents (each call rewrites all it reads; nothing needs to start
+ *     at zero).  Calls that overlap on one GPU (concurrent streams, or threads
+ *     without ordering) race on it: order them on one stream.
+ */
+#define LS_NOALLOC_SCRATCH_BYTES ((size_t)64 << 20)
+ls_status ls_sparse_attn_fwd_noalloc(const ls_attn_params* p, const int32_t* idx, int32_t topk,
+                                     float* out, float* lse, void* stream);
+
+/*
  * ls_hbm_read_probe (measurement, not part of the replay path): reads `bytes`
  * of device memory at buf once and XORs all its 32-bit words into *out
  * (*out ^= XOR of the words; zero it first to get the XOR itself).  A

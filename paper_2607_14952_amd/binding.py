@@ -25,7 +25,8 @@ STATUS = {0: "LS_OK", -1: "LS_ERR_INVALID_ARG", -2: "LS_ERR_UNSUPPORTED", -3: "L
 EXPORTS = ["ls_abi_version", "ls_status_string", "ls_last_error", "ls_gather_kv", "ls_scatter_kv",
            "ls_prefix_attn_fwd", "ls_lse_merge", "ls_prefix_attn_bwd_workspace_size",
            "ls_prefix_attn_bwd", "ls_sparse_attn_workspace_size", "ls_sparse_attn_fwd",
-           "ls_sparse_attn_bwd", "ls_dsa_index_scores", "ls_topk_select", "ls_hbm_read_probe"]
+           "ls_sparse_attn_bwd", "ls_dsa_index_scores", "ls_topk_select", "ls_hbm_read_probe",
+           "ls_sparse_attn_fwd_noalloc"]
 
 
 class AttnParams(ctypes.Structure):
@@ -101,6 +102,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.ls_topk_select.restype = c_int32
     lib.ls_topk_select.argtypes = [c_void_p, c_int64, c_void_p, c_int32, c_int64, c_int64, c_int32,
                                    c_void_p, c_void_p, c_int64, c_void_p]
+    lib.ls_sparse_attn_fwd_noalloc.restype = c_int32
+    lib.ls_sparse_attn_fwd_noalloc.argtypes = [P, c_void_p, c_int32, c_void_p, c_void_p, c_void_p]
     lib.ls_hbm_read_probe.restype = c_int32
     lib.ls_hbm_read_probe.argtypes = [c_void_p, c_size_t, c_void_p, c_void_p]
     if lib.ls_abi_version() != ABI_VERSION:
@@ -342,6 +345,22 @@ def sparse_attn_fwd(q, latent: PagedKV, idx, *, prefix_len: int, q_pos0: int, sc
                                             _ptr(workspace, None, "workspace"),
                                             workspace.numel() * workspace.element_size(),
                                             _stream(stream)))
+    return out, lse
+
+
+def sparse_attn_fwd_noalloc(q, latent: PagedKV, idx, *, out, lse, prefix_len: int, q_pos0: int,
+                            scale: float, flags: int = 0, stream=None):
+    """ls_sparse_attn_fwd_noalloc: the sparse forward into caller-provided out
+    [R, H, 512] and lse [H, R] (fp32), with no workspace; nothing is allocated
+    here either."""
+    torch = _torch()
+    topk = 0 if idx is None else idx.shape[1]
+    p = _sparse_params(q, latent, prefix_len=prefix_len, q_pos0=q_pos0, scale=scale, flags=flags)
+    check(load_library().ls_sparse_attn_fwd_noalloc(ctypes.byref(p),
+                                                    _ptr(idx, torch.int32, "idx"), topk,
+                                                    _ptr(out, torch.float32, "out"),
+                                                    _ptr(lse, torch.float32, "lse"),
+                                                    _stream(stream)))
     return out, lse
 
 

@@ -5,6 +5,7 @@
 #include <stdio.h>
 
 #include <algorithm>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -557,14 +558,9 @@ LS_API size_t ls_sparse_attn_workspace_size(const ls_attn_params* p, int32_t top
   return backward ? L.bwd_bytes() : L.fwd_bytes();
 }
 
-LS_API ls_status ls_sparse_attn_fwd(const ls_attn_params* p, const int32_t* idx, int32_t topk,
-                                    float* out, float* lse, void* workspace,
-                                    size_t workspace_bytes, void* stream) {
-  ls_status st = check_sparse(p, idx, topk);
-  if (st != LS_OK) return st;
-  if (p->n_q == 0) return LS_OK;
-  if (!out || !lse || !aligned16(out) || !aligned16(lse))
-    return fail(LS_ERR_INVALID_ARG, "out/lse must be non-NULL and 16-byte aligned");
+namespace {
+ls_status sparse_fwd_run(const ls_attn_params* p, const int32_t* idx, int32_t topk, float* out,
+                         float* lse, void* workspace, size_t workspace_bytes, void* stream) {
   const SparseLayout L = sparse_layout(p, topk);
   if (!workspace || !aligned16(workspace) || workspace_bytes < L.fwd_bytes())
     return fail(LS_ERR_WORKSPACE, "workspace of %zu bytes needed", L.fwd_bytes());
@@ -574,7 +570,8 @@ LS_API ls_status ls_sparse_attn_fwd(const ls_attn_params* p, const int32_t* idx,
   outs.push_back(rng("out", out, (size_t)p->n_q * p->n_q_heads * 512 * 4));
   outs.push_back(rng("lse", lse, (size_t)p->n_q * p->n_q_heads * 4));
   outs.push_back(rng("workspace", workspace, L.fwd_bytes()));
-  if ((st = check_alias(outs, ins)) != LS_OK) return st;
+  ls_status st = check_alias(outs, ins);
+  if (st != LS_OK) return st;
   hipStream_t s = (hipStream_t)stream;
   if ((st = check_pages(p, kv_len_of(p), s)) != LS_OK) return st;
   if ((st = check_idx(p, idx, topk, s)) != LS_OK) return st;
@@ -585,6 +582,82 @@ LS_API ls_status ls_sparse_attn_fwd(const ls_attn_params* p, const int32_t* idx,
   hipError_t e = ls::launch_sparse_phys(a, s);
   if (e == hipSuccess) e = ls::launch_sparse_fwd(a, s);
   return e == hipSuccess ? LS_OK : hip_fail(e, "sparse forward launch");
+}
+}  // namespace
+
+LS_API ls_status ls_sparse_attn_fwd(const ls_attn_params* p, const int32_t* idx, int32_t topk,
+                                    float* out, float* lse, void* workspace,
+                                    size_t workspace_bytes, void* stream) {
+  ls_status st = check_sparse(p, idx, topk);
+  if (st != LS_OK) return st;
+  if (p->n_q == 0) return LS_OK;
+  if (!out || !lse || !aligned16(out) || !aligned16(lse))
+    return fail(LS_ERR_INVALID_ARG, "out/lse must be non-NULL and 16-byte aligned");
+  return sparse_fwd_run(p, idx, topk, out, lse, workspace, workspace_bytes, stream);
+}
+
+// ---------------------------------------------------------------- allocation-free sparse forward
+// The key lists of ls_sparse_attn_fwd_noalloc live in this array.  Every GPU
+// the library runs on holds its own copy for the life of the process.  In host
+// code the array's name is not a device address: the kernels get the address
+// that hipGetSymbolAddress returns for the current device.
+constexpr size_t kScratchBytes = LS_NOALLOC_SCRATCH_BYTES;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};   // per device ordinal; null until resolved
+
+// Device address of `scratch` on the device that runs `stream` (which must be
+// the current device), resolved once per device with that device current.
+ls_status scratch_address(void* stream, void** addr) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  if (stream) {
+    hipDevice_t sdev = -1;
+    e = hipStreamGetDevice((hipStream_t)stream, &sdev);
+    if (e != hipSuccess) return hip_fail(e, "hipStreamGetDevice");
+    if (sdev != dev)
+      return fail(LS_ERR_INVALID_ARG, "stream belongs to device %d, the current device is %d",
+                  (int)sdev, dev);
+  }
+  if (dev < 0 || dev >= kMaxDevices)
+    return fail(LS_ERR_UNSUPPORTED, "device ordinal %d outside [0, %d)", dev, kMaxDevices);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* ptr = nullptr;
+    e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return hip_fail(e, "hipGetSymbolAddress(scratch)");
+    if (!ptr) return fail(LS_ERR_HIP, "hipGetSymbolAddress(scratch) returned NULL");
+    g_scratch_ptr[dev] = ptr;
+  }
+  *addr = g_scratch_ptr[dev];
+  return LS_OK;
+}
+}  // namespace
+
+LS_API ls_status ls_sparse_attn_fwd_noalloc(const ls_attn_params* p, const int32_t* idx,
+                                            int32_t topk, float* out, float* lse, void* stream) {
+  ls_status st = check_sparse(p, idx, topk);
+  if (st != LS_OK) return st;
+  if (p->flags & LS_FLAG_CHECKED)
+    return fail(LS_ERR_UNSUPPORTED,
+                "the allocation-free forward has no checked mode (it copies to the host and "
+                "synchronizes); validate with ls_sparse_attn_fwd");
+  if (p->n_q == 0) return LS_OK;
+  if (!out || !lse || !aligned16(out) || !aligned16(lse))
+    return fail(LS_ERR_INVALID_ARG, "out/lse must be non-NULL and 16-byte aligned");
+  const size_t need = sparse_layout(p, topk).fwd_bytes();
+  if (need > kScratchBytes)
+    return fail(LS_ERR_WORKSPACE,
+                "the allocation-free forward needs %zu bytes of scratch; its maximum is %zu "
+                "(n_q * key-list length * 4 bytes): use ls_sparse_attn_fwd with a workspace",
+                need, kScratchBytes);
+  void* ws = nullptr;
+  if ((st = scratch_address(stream, &ws)) != LS_OK) return st;
+  return sparse_fwd_run(p, idx, topk, out, lse, ws, kScratchBytes, stream);
 }
 
 LS_API ls_status ls_sparse_attn_bwd(const ls_attn_params* p, const int32_t* idx, int32_t topk,

@@ -267,3 +267,26 @@ def test_binding_checks_device_dtype_and_layout():
                       out_scores=torch.zeros((2, 3)))
     with pytest.raises(ValueError, match="row stride of scores"):
         B.topk_select(torch.zeros((2, 8)), 3, positions=torch.zeros((2, 9), dtype=torch.int32))
+
+
+def test_sparse_noalloc_rejects_on_the_host():
+    """The allocation-free sparse forward refuses checked mode and calls whose
+    key lists exceed its scratch array, before touching the GPU."""
+    lib = B.load_library()
+    p = good_params(head_dim=576, head_dim_v=512, n_kv_heads=1, n_q_heads=128, page_size=64,
+                    n_phys_pages=4096, n_logical_pages=4096, prefix_len=65536, q_pos0=65536,
+                    n_q=16)
+    p.v_pool = p.k_pool
+    idx, out, lse = FAKE * 512, FAKE * 576, FAKE * 1024
+    p.flags = B.FLAG_CHECKED
+    assert lib.ls_sparse_attn_fwd_noalloc(ctypes.byref(p), idx, 64, out, lse, None) == -2
+    p.flags = 0
+    # 16 rows x (64 selections + a window of 2^22 response positions) x 4 bytes > 64 MiB
+    big = good_params(**{k: getattr(p, k) for k in ("head_dim", "head_dim_v", "n_kv_heads",
+                                                     "n_q_heads", "page_size", "n_phys_pages",
+                                                     "prefix_len", "n_q")})
+    big.v_pool = big.k_pool
+    big.q_pos0 = p.prefix_len + (1 << 22)
+    big.n_logical_pages = (big.q_pos0 + 16) // 64 + 1
+    assert lib.ls_sparse_attn_fwd_noalloc(ctypes.byref(big), idx, 64, out, lse, None) == -3
+    assert b"scratch" in lib.ls_last_error()
