@@ -198,18 +198,22 @@ def make_params(q, kv: PagedKV, *, n_q=None, n_q_heads=None, prefix_len: int, q_
 
 
 # ----------------------------------------------------------------- entry points
-def gather_kv(kv: PagedKV, pos_begin: int, pos_end: int, *, flags: int = 0, stream=None):
+def gather_kv(kv: PagedKV, pos_begin: int, pos_end: int, *, flags: int = 0, k_out=None,
+              v_out=None, stream=None):
     """ls_gather_kv: dense copies of logical positions [pos_begin, pos_end)."""
     torch = _torch()
     n = pos_end - pos_begin
-    k = torch.empty((n,) + tuple(kv.k_pool.shape[2:]), dtype=kv.k_pool.dtype, device=kv.k_pool.device)
-    v = torch.empty((n,) + tuple(kv.v_pool.shape[2:]), dtype=kv.v_pool.dtype, device=kv.v_pool.device)
+    k = k_out if k_out is not None else torch.empty(
+        (n,) + tuple(kv.k_pool.shape[2:]), dtype=kv.k_pool.dtype, device=kv.k_pool.device)
+    v = v_out if v_out is not None else torch.empty(
+        (n,) + tuple(kv.v_pool.shape[2:]), dtype=kv.v_pool.dtype, device=kv.v_pool.device)
     dummy_q = torch.empty((0, 1, 1), dtype=kv.k_pool.dtype, device=kv.k_pool.device)
     p = make_params(dummy_q, kv, n_q=0, n_q_heads=kv.k_pool.shape[2], prefix_len=0, q_pos0=0,
                     scale=1.0, flags=flags)
     p.q = None
-    check(load_library().ls_gather_kv(ctypes.byref(p), pos_begin, pos_end, _ptr(k), _ptr(v),
-                                      _stream(stream)))
+    check(load_library().ls_gather_kv(ctypes.byref(p), pos_begin, pos_end,
+                                      _ptr(k, kv.k_pool.dtype, "k_out"),
+                                      _ptr(v, kv.v_pool.dtype, "v_out"), _stream(stream)))
     return k, v
 
 
