@@ -92,9 +92,18 @@ __device__ __forceinline__ void pv(const char* Vs, const bf16x8& p0, const bf16x
   }
 }
 
+#ifndef LS_FWD_LAZY
+#define LS_FWD_LAZY 1
+#endif
+constexpr float kLazyFwd = 8.f;
+
 // Online softmax step over one tile (base-2, scale folded in): s becomes
 // exp2(s*c - m_new), alpha = exp2(m_old - m_new) rescales earlier partial
 // sums, and a row with no visible key so far keeps m = -inf and P = 0.  The
+// running reference m moves lazily: only when the tile's row max exceeds it by
+// more than kLazyFwd.  Output, sum and log-normalizer stay relative to the
+// same m, so the result is the same softmax, with P <= 2^kLazyFwd before its
+// bf16 rounding (the same relative rounding at any magnitude).  The
 // step is cut into pieces issued between the score MFMAs of the next tile so
 // that its VALU work overlaps the MFMA chain: pieces 0-1 the row max and
 // alpha, 2-9 two exponentials each, 10 the running sum and P's first half, 11
@@ -114,8 +123,14 @@ struct OnlineSoftmax {
     } else if (k == 1) {
 #pragma unroll
       for (int r = 8; r < 16; ++r) mx = fmaxf(mx, s[r]);
-      mx = half_max(mx);
-      const float m_new = fmaxf(m_run, mx * c);
+      mx = half_max(mx) * c;
+#if LS_FWD_LAZY
+      // the reference moves only when the tile's max exceeds it by more than
+      // kLazyFwd (base 2), so P <= 2^kLazyFwd and most tiles leave O unscaled
+      const float m_new = mx > m_run + kLazyFwd ? mx : m_run;
+#else
+      const float m_new = fmaxf(m_run, mx);
+#endif
       m_use = m_new == -INFINITY ? 0.f : m_new;
       alpha = __builtin_amdgcn_exp2f(m_run - m_use);
       m_run = m_new;
