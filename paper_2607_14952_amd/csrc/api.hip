@@ -14,6 +14,11 @@
 
 #define LS_API extern "C" __attribute__((visibility("default")))
 
+// The sparse backward runs as one fused pass (sparse_fused.hip) unless this is 0.
+#ifndef LS_SPARSE_FUSED
+#define LS_SPARSE_FUSED 1
+#endif
+
 namespace {
 
 thread_local std::string g_last_error;
@@ -702,7 +707,11 @@ LS_API ls_status ls_sparse_attn_bwd(const ls_attn_params* p, const int32_t* idx,
   if (e == hipSuccess)
     e = ls::launch_bwd_prep(d_out, out, true, out_dtype == LS_BF16, lse, p->n_q, p->n_q_heads,
                             512, delta, lse2, s);
+#if LS_SPARSE_FUSED
+  if (e == hipSuccess) e = ls::launch_sparse_bwd_fused(a, s);
+#else
   if (e == hipSuccess) e = ls::launch_sparse_bwd(a, s);
+#endif
   return e == hipSuccess ? LS_OK : hip_fail(e, "sparse backward launch");
 }
 

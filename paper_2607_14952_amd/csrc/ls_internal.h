@@ -114,6 +114,7 @@ struct SparseArgs {
 hipError_t launch_sparse_phys(const SparseArgs& a, hipStream_t stream);
 hipError_t launch_sparse_fwd(const SparseArgs& a, hipStream_t stream);
 hipError_t launch_sparse_bwd(const SparseArgs& a, hipStream_t stream);
+hipError_t launch_sparse_bwd_fused(const SparseArgs& a, hipStream_t stream);
 hipError_t launch_gather(const void* k_pool, const void* v_pool, const int32_t* page_table,
                          int64_t pos_begin, int64_t pos_end, int log2_page, int64_t k_row_elems,
                          int64_t v_row_elems, int esize, void* k_out, void* v_out,

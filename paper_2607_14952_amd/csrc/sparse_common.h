@@ -40,6 +40,20 @@ constexpr int kChunks = kRow / 16;            // 72
 // 4 chunks cover all 16 bank groups).
 __host__ __device__ inline int s_swz(int k) { return (((k >> 1) & 1) << 2) | ((k >> 2) & 3); }
 
+// Chunk swizzle of the fused backward's tiles (16x16x32 operands): bits 1, 2, 3
+// of the row go to bits 1, 2, 0.  Like s_swz it is a bijection on the even and
+// on the odd rows of any 16 consecutive aligned rows (a 16-lane phase of row
+// reads covers all 16 bank groups).  Its transposed reads take 4 consecutive
+// aligned rows x 2 chunks per 16 lanes, and a 32-lane phase pairs row quads
+// (0, 5), (4, 1), (2, 7) and (6, 3) of the tile (b_offsets): in every pair the
+// four even rows have distinct b_swz >> 1 and so do the four odd rows, so the
+// phase's 8 rows x 2 chunks cover all 16 bank groups.
+__host__ __device__ inline int b_swz(int k) {
+  return (((k >> 1) & 1) << 1) | (((k >> 2) & 1) << 2) | ((k >> 3) & 1);
+}
+template <bool kAlt>
+__host__ __device__ inline int tile_swz(int k) { return kAlt ? b_swz(k) : s_swz(k); }
+
 // Lane-constant LDS offsets, one register each: the swizzle only flips bits
 // that the compile-time operand index selects, so the row operand of step ks
 // sits at row_off(ks & 3) + 128 * (ks >> 2) with row_off(q) = row0 ^ 32q, and
@@ -103,7 +117,8 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t phys_rsrc(const SparseArgs& a,
 // 32 physical rows (lane k: key row k) serves all nine instructions through
 // two lane reads and a select.  Row and chunk offsets are recomputed per
 // instruction (a few integer ops) rather than kept in registers.
-struct SFetch {
+template <bool kAlt>
+struct SFetchT {
   int q0;   // (9w) * 64 + lane
   __host__ __device__ inline void init(int lane, int w) { q0 = 9 * w * 64 + lane; }
   // (q0 passes through an empty asm so that the per-instruction offsets are
@@ -120,7 +135,7 @@ struct SFetch {
   __host__ __device__ inline int coff(int i) const {
     const int q = qi(i), r = q / kChunks;
     const int c = q - r * kChunks;
-    return ((c & ~7) | ((c & 7) ^ s_swz(r))) * 16;
+    return ((c & ~7) | ((c & 7) ^ tile_swz<kAlt>(r))) * 16;
   }
   // first key row of instruction i of wave w (its other lanes: the next row)
   __host__ __device__ static inline int first_row(int w, int i) {
@@ -149,7 +164,7 @@ struct SFetch {
     const int c = q - rw * kChunks;
     const int phys = rw > ra ? pb : pa;
     const uint32_t off =
-        (uint32_t)phys * (uint32_t)kRow + (uint32_t)(((c & ~7) | ((c & 7) ^ s_swz(rw))) * 16);
+        (uint32_t)phys * (uint32_t)kRow + (uint32_t)(((c & ~7) | ((c & 7) ^ tile_swz<kAlt>(rw))) * 16);
     __builtin_amdgcn_raw_ptr_buffer_load_lds(r, LS_LDS(tile + (9 * w + i) * 1024), 16, (int)off, 0,
                                              0, 0);
   }
@@ -159,6 +174,43 @@ struct SFetch {
     for (int i = 0; i < 9; ++i) issue_one(tile, r, rows, w, i);
   }
 };
+using SFetch = SFetchT<false>;
+
+// Lane offsets of the fused backward's operand reads (b_swz tiles), one
+// register each.  Lane l = 16g + c:
+//  - row operand (A of S^T = C Q^T and dP^T = V dO^T, 16 keys x 32 channels):
+//    key 16mb + c, channels 32ks + 8g .. +7, at
+//    (row0 ^ 64 (ks & 1)) + 128 (ks >> 1) + 16 kRow mb;
+//  - transposed operand (A of dq^T += C^T dS^T, 16 channels x 32 keys):
+//    channel 16db + c of eight keys, two transposing reads at
+//    (col[k] ^ 32 (db & 3)) + 128 (db >> 2); read k of lane group g takes the
+//    rows key_base(g, k) .. +3 (key_base: 4g, plus 16 on read 0 for odd g and
+//    on read 1 for even g), so the operand's elements are keys
+//    key_base(g, 0) + {0..3}, then key_base(g, 1) + {0..3}.
+struct BOffsets {
+  int row0;
+  int col[2];
+  __host__ __device__ inline int row_off(int mb, int ks) const {
+    return (row0 ^ (64 * (ks & 1))) + 128 * (ks >> 1) + 16 * kRow * mb;
+  }
+  __host__ __device__ inline int col_off(int k, int db) const {
+    return (col[k] ^ (32 * (db & 3))) + 128 * (db >> 2);
+  }
+};
+
+__host__ __device__ inline int key_base(int g, int k) { return 4 * g + 16 * ((g & 1) ^ k); }
+
+__host__ __device__ inline BOffsets b_offsets(int lane) {
+  BOffsets o;
+  const int c = lane & 15, g = lane >> 4;
+  o.row0 = c * kRow + 16 * (g ^ b_swz(c));
+  const int x = (c & 3) >> 1;                       // chunk within the 2-chunk column block
+  const int sw = b_swz(4 * g + (c >> 2));            // rows key_base + (c >> 2): same bits 1-3
+  const int col0 = (c >> 2) * kRow + 16 * (x ^ sw) + 8 * (c & 1);
+#pragma unroll
+  for (int k = 0; k < 2; ++k) o.col[k] = key_base(g, k) * kRow + col0;
+  return o;
+}
 
 // Online softmax step over one tile (base 2, scale c folded in) with a lazily
 // moved reference: m_run moves to the tile's row max only when that exceeds it
@@ -228,6 +280,16 @@ __device__ __forceinline__ void s_pv(const char* tile, const bf16x8& p0, const b
     oacc[i >> 1] = mfma32(vr[i], (i & 1) ? p1 : p0, oacc[i >> 1]);
     mfma_fence();
   }
+}
+
+// Fused backward operands (16x16x32 MFMA).
+__device__ __forceinline__ bf16x8 b_row16(const char* tile, const BOffsets& o, int mb, int ks) {
+  return *reinterpret_cast<const bf16x8*>(tile + o.row_off(mb, ks));
+}
+__device__ __forceinline__ bf16x8 b_col8(const char* tile, const BOffsets& o, int db) {
+  const i16x4 a = __builtin_amdgcn_ds_read_tr16_b64_v4i16(LS_LDS4(tile + o.col_off(0, db)));
+  const i16x4 b = __builtin_amdgcn_ds_read_tr16_b64_v4i16(LS_LDS4(tile + o.col_off(1, db)));
+  return __builtin_bit_cast(bf16x8, __builtin_shufflevector(a, b, 0, 1, 2, 3, 4, 5, 6, 7));
 }
 
 }  // namespace sparse

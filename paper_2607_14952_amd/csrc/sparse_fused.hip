@@ -1,0 +1,170 @@
+// Sparse latent replay, backward (dq only) in one pass over the gathered rows
+// (Eq. dsa-attention; latent rows get no gradient).
+//
+// Workgroup = 4 waves = 64 heads of one token (two workgroups per token; grid
+// y = groups of 128 heads).  Wave w takes heads 16w .. 16w+15 of its half,
+// lane 16g + c head c, and works with v_mfma_f32_16x16x32_bf16, so Q (72
+// registers), dO (64) and the dq accumulator (144) of its heads fit one wave
+// per SIMD.  Per 32-key tile of gathered latent rows:
+//   S^T  = C Q^T   (2 key blocks x 18 channel steps)   } one C-row operand
+//   dP^T = V dO^T  (2 key blocks x 16 channel steps)   } read serves both
+//   dS   = P (dP - Delta),  P = exp2(s * scale * log2(e) - lse2), 0 past the list
+//   dq^T += C^T dS^T       (36 channel blocks, transposed reads of the same tile)
+// dS stays in registers: the lane's S^T results are already the B operand of
+// the dq product (keys in the order the transposed reads deliver them), so no
+// dS buffer goes through HBM and each row is gathered once per workgroup.
+// The two workgroups of a token are the 8th-apart linear ids 16k + x and
+// 16k + 8 + x, which land on the same XCD one after the other, so the second
+// gather of a row mostly hits that XCD's L2.  Tokens with more keys go first.
+// Rows stream into a three-slot LDS ring by direct loads, two tiles ahead,
+// in the b_swz tile layout (sparse_common.h).
+#include "sparse_common.h"
+
+namespace ls {
+namespace {
+using namespace sparse;
+
+constexpr int kFBSlots = 3;
+constexpr int kFAhead = 4;    // row operands in flight
+constexpr int kFTAhead = 3;   // transposed operands in flight (two reads each)
+
+__device__ __forceinline__ f32x4 mfma16(const bf16x8& a, const bf16x8& b, const f32x4& c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+
+__device__ __forceinline__ f32x4 zero4() { return f32x4{0.f, 0.f, 0.f, 0.f}; }
+
+__device__ __forceinline__ bf16x8 pack_halves(const f32x4& lo, const f32x4& hi) {
+  bf16x8 o;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    o[e] = (__bf16)lo[e];
+    o[4 + e] = (__bf16)hi[e];
+  }
+  return o;
+}
+
+// One tile: S^T, dP^T (the next stage's direct loads after the first nine
+// steps), dS, and the dq product.  `next` and `tile` are distinct ring slots
+// (restrict: the compiler need not wait for the loads before reading `tile`).
+__device__ __forceinline__ void fused_tile(const SparseArgs& a, char* __restrict__ next,
+                                           const char* __restrict__ tile,
+                                           const SFetchT<true>& f, __amdgpu_buffer_rsrc_t pool,
+                                           int32_t pr, int w, const bf16x8* qreg,
+                                           const bf16x8* dreg, const BOffsets& bo, int T, int n_t,
+                                           int g, float lse2, float delta, f32x4* acc) {
+  // step i = 2 ks + mb reads the row operand of key block mb, channel step ks
+  bf16x8 kr[36];
+#pragma unroll
+  for (int i = 0; i < kFAhead; ++i) kr[i] = b_row16(tile, bo, i & 1, i >> 1);
+  mfma_fence();
+  f32x4 s[2] = {zero4(), zero4()}, dp[2] = {zero4(), zero4()};
+#pragma unroll
+  for (int i = 0; i < 36; ++i) {
+    if (i + kFAhead < 36) kr[i + kFAhead] = b_row16(tile, bo, (i + kFAhead) & 1, (i + kFAhead) >> 1);
+    const int mb = i & 1, ks = i >> 1;
+    s[mb] = mfma16(kr[i], qreg[ks], s[mb]);
+    if (ks < 16) dp[mb] = mfma16(kr[i], dreg[ks], dp[mb]);
+    if (i < 9) f.issue_one(next, pool, pr, w, i);
+    mfma_fence();
+  }
+  // dS of keys T*32 + 16 mb + 4 g + r (lane: head c), zero past the key list
+  f32x4 ds[2];
+#pragma unroll
+  for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      float p = __builtin_amdgcn_exp2f(fmaf(s[mb][r], a.scale_log2, -lse2));
+      if (T * kKeys + 16 * mb + 4 * g + r >= n_t) p = 0.f;
+      ds[mb][r] = p * (dp[mb][r] - delta);
+    }
+  // B operand: keys key_base(g, 0) + {0..3}, then key_base(g, 1) + {0..3}
+  const bf16x8 dsb = (g & 1) ? pack_halves(ds[1], ds[0]) : pack_halves(ds[0], ds[1]);
+  bf16x8 kt[36];
+#pragma unroll
+  for (int i = 0; i < kFTAhead; ++i) kt[i] = b_col8(tile, bo, i);
+  mfma_fence();
+#pragma unroll
+  for (int db = 0; db < 36; ++db) {
+    if (db + kFTAhead < 36) kt[db + kFTAhead] = b_col8(tile, bo, db + kFTAhead);
+    acc[db] = mfma16(kt[db], dsb, acc[db]);
+    mfma_fence();
+  }
+}
+
+__global__ __launch_bounds__(256, 1) void sparse_bwd_fused_kernel(SparseArgs a) {
+  __shared__ __attribute__((aligned(1024))) char smem[kFBSlots * kTile];
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int c = lane & 15, g = lane >> 4;
+  // linear ids 16k + x and 16k + 8 + x: the two head halves of token 8k + x
+  const int b = (int)blockIdx.x;
+  const int tk = 8 * (b >> 4) + (b & 7), half = (b >> 3) & 1;
+  if (tk >= a.n_q) return;
+  const int t = a.n_q - 1 - tk;
+  const int head = (int)blockIdx.y * 128 + 64 * half + 16 * w + c;
+  const int n_t = a.ntok[t];
+  const int n_tiles = (n_t + kKeys - 1) / kKeys;
+  const __amdgpu_buffer_rsrc_t phys_t = phys_rsrc(a, t);
+  const __amdgpu_buffer_rsrc_t pool = pool_rsrc(a.latent);
+  auto clamp = [&](int T) { return T < n_tiles ? T : n_tiles - 1; };
+
+  SFetchT<true> f;
+  f.init(lane, w);
+  const BOffsets bo = b_offsets(lane);
+  // the row lists of the first three tiles load before any tile does
+  const int32_t r0 = f.rows_of(phys_t, 0, lane), r1 = f.rows_of(phys_t, clamp(1), lane);
+  int32_t pr = f.rows_of(phys_t, clamp(2), lane), pn;
+  f.issue(smem, pool, r0, w);
+  f.issue(smem + kTile, pool, r1, w);
+
+  bf16x8 qreg[18], dreg[16];   // B operands: head c, channels 32 ks + 8 g .. +7
+  {
+    const int64_t rh = (int64_t)t * a.n_heads + head;
+    const __bf16* qrow = static_cast<const __bf16*>(a.q) + rh * kDk + 8 * g;
+    const __bf16* drow = static_cast<const __bf16*>(a.d_out) + rh * kDv + 8 * g;
+#pragma unroll
+    for (int ks = 0; ks < 18; ++ks) qreg[ks] = *reinterpret_cast<const bf16x8*>(qrow + 32 * ks);
+#pragma unroll
+    for (int ks = 0; ks < 16; ++ks) dreg[ks] = *reinterpret_cast<const bf16x8*>(drow + 32 * ks);
+  }
+  const int64_t stat = (int64_t)head * a.n_q + t;
+  const float lse2 = a.lse2[stat], delta = a.delta[stat];
+  f32x4 acc[36];
+#pragma unroll
+  for (int i = 0; i < 36; ++i) acc[i] = zero4();
+  wait_fetch();
+  tile_barrier();
+
+  for (int T = 0; T < n_tiles; ++T) {
+    pn = f.rows_of(phys_t, clamp(T + 3), lane);
+    __builtin_amdgcn_sched_barrier(0);   // the row list loads ahead of this stage's direct loads
+    fused_tile(a, smem + ((T + 2) % kFBSlots) * kTile, smem + (T % kFBSlots) * kTile, f, pool,
+               pr, w, qreg, dreg, bo, T, n_t, g, lse2, delta, acc);
+    pr = pn;
+    __builtin_amdgcn_s_waitcnt(0x0F79);   // vmcnt(9): only this iteration's stage may be in flight
+    tile_barrier();
+  }
+  wait_fetch();   // no direct load is left in flight when the waves end
+
+  // dq^T block db: channels 16 db + 4 g + {0..3} of head c
+  float* dq = a.dq + ((int64_t)t * a.n_heads + head) * kDk + 4 * g;
+#pragma unroll
+  for (int db = 0; db < 36; ++db) {
+    f32x4* dst = reinterpret_cast<f32x4*>(dq + 16 * db);
+    f32x4 v = acc[db] * a.scale;
+    if (a.accumulate_dq) v += *dst;
+    *dst = v;
+  }
+}
+
+}  // namespace
+
+hipError_t launch_sparse_bwd_fused(const SparseArgs& a, hipStream_t stream) {
+  const unsigned tokens8 = (unsigned)((a.n_q + 7) / 8 * 8);
+  hipLaunchKernelGGL(sparse_bwd_fused_kernel, dim3(2 * tokens8, a.n_heads / 128), dim3(256), 0,
+                     stream, a);
+  return hipGetLastError();
+}
+
+}  // namespace ls

@@ -180,9 +180,64 @@ static void sparse() {
     }
 }
 
+// The fused sparse backward's tiles (b_swz, 16x16x32 operands).
+static void fused() {
+  using namespace ls::sparse;
+  const int cols = kRow / 2;
+  std::vector<int> tag(kTile / 2, -1);
+  for (int w = 0; w < 4; ++w)
+    for (int lane = 0; lane < 64; ++lane) {
+      SFetchT<true> f;
+      f.init(lane, w);
+      for (int i = 0; i < 9; ++i) {
+        const int dst = (9 * w + i) * 1024 + 16 * lane;
+        for (int e = 0; e < 8; ++e) {
+          CHECK(tag[dst / 2 + e] == -1, "fused fetch writes slot %d twice", dst / 2 + e);
+          tag[dst / 2 + e] = f.row(i) * cols + f.coff(i) / 2 + e;
+        }
+      }
+    }
+  for (int v : tag) CHECK(v >= 0, "fused fetch leaves a slot unwritten");
+  BOffsets o[64];
+  for (int l = 0; l < 64; ++l) o[l] = b_offsets(l);
+  for (int mb = 0; mb < 2; ++mb)
+    for (int ks = 0; ks < 18; ++ks) {
+      int off[64];
+      for (int l = 0; l < 64; ++l) {
+        off[l] = o[l].row_off(mb, ks);
+        const int key = 16 * mb + (l & 15), c0 = 32 * ks + 8 * (l >> 4);
+        for (int e = 0; e < 8; ++e)
+          CHECK(tag[off[l] / 2 + e] == key * cols + c0 + e, "fused row operand mb=%d ks=%d lane=%d e=%d",
+                mb, ks, l, e);
+      }
+      check_b128_phases(off, "fused row operand");
+    }
+  for (int db = 0; db < 36; ++db)
+    for (int k = 0; k < 2; ++k) {
+      int off[64];
+      for (int l = 0; l < 64; ++l) off[l] = o[l].col_off(k, db);
+      for (int l = 0; l < 64; ++l)
+        for (int j = 0; j < 4; ++j) {
+          const int want = (key_base(l >> 4, k) + j) * cols + 16 * db + (l & 15);
+          CHECK(tr_elem(tag, off, l, j) == want, "fused transposed operand db=%d k=%d lane=%d j=%d",
+                db, k, l, j);
+        }
+      check_b64_phases(off, "fused transposed operand");
+    }
+  // the two reads of each lane group cover the tile's 32 keys once
+  for (int g = 0; g < 4; ++g) {
+    unsigned keys = 0;
+    for (int g2 = 0; g2 < 4; ++g2)
+      for (int k = 0; k < 2; ++k)
+        for (int j = 0; j < 4; ++j) keys |= 1u << (key_base(g2, k) + j);
+    CHECK(keys == 0xFFFFFFFFu, "fused transposed operands miss a key");
+  }
+}
+
 int main() {
   dense();
   sparse();
+  fused();
   if (failures) {
     printf("%d failures\n", failures);
     return 1;
