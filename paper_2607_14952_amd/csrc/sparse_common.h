@@ -154,6 +154,12 @@ struct SFetchT {
     __builtin_amdgcn_raw_ptr_buffer_load_lds(phys_t, LS_LDS(dst), 4, (T * kKeys + (lane & 31)) * 4,
                                              0, 0, 0);
   }
+  // Lanes at or past second_lane(i) of instruction i carry chunks of its
+  // second row, whatever the wave: chunk q = 576 w + 64 i + lane lies in row
+  // 8 w + (64 i + lane) / 72.
+  __host__ __device__ static constexpr int second_lane(int i) {
+    return 72 * ((8 * i) / 9 + 1) - 64 * i;
+  }
   // w: the wave (uniform)
   __device__ __forceinline__ void issue_one(char* tile, __amdgpu_buffer_rsrc_t r, int32_t rows,
                                             int w, int i) const {
@@ -175,6 +181,32 @@ struct SFetchT {
   }
 };
 using SFetch = SFetchT<false>;
+
+// The same direct loads with each lane's byte offsets inside a latent row
+// (chunk and swizzle, one per instruction) computed once and kept in
+// registers: per instruction the loop then reads the two physical rows of the
+// instruction from the tile's row list, selects one by a constant lane mask,
+// and adds phys * kRow (a 24-bit multiply; rows < 2^24).
+template <bool kAlt>
+struct SFetchPre {
+  int off[9];
+  __host__ __device__ inline void init(int lane, int w) {
+    SFetchT<kAlt> f;
+    f.init(lane, w);
+#pragma unroll
+    for (int i = 0; i < 9; ++i) off[i] = f.coff(i);
+  }
+  __device__ __forceinline__ void issue_one(char* tile, __amdgpu_buffer_rsrc_t r, int32_t rows,
+                                            int w, int i, int lane) const {
+    const int ra = 8 * w + (8 * i) / 9;   // = SFetchT::first_row(w, i)
+    const int pa = __builtin_amdgcn_readlane(rows, ra);
+    const int pb = __builtin_amdgcn_readlane(rows, min(ra + 1, kKeys - 1));
+    const int phys = lane >= SFetchT<kAlt>::second_lane(i) ? pb : pa;
+    const uint32_t o = __umul24((uint32_t)phys, (uint32_t)kRow) + (uint32_t)off[i];
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, LS_LDS(tile + (9 * w + i) * 1024), 16, (int)o, 0,
+                                             0, 0);
+  }
+};
 
 // Lane offsets of the fused backward's operand reads (b_swz tiles), one
 // register each.  Lane l = 16g + c:

@@ -24,6 +24,10 @@ namespace ls {
 namespace {
 using namespace sparse;
 
+#ifndef LS_SPARSE_PIPE
+#define LS_SPARSE_PIPE 1
+#endif
+
 constexpr int kFBSlots = 3;
 constexpr int kFAhead = 4;    // row operands in flight
 constexpr int kFTAhead = 3;   // transposed operands in flight (two reads each)
@@ -49,8 +53,8 @@ __device__ __forceinline__ bf16x8 pack_halves(const f32x4& lo, const f32x4& hi) 
 // (restrict: the compiler need not wait for the loads before reading `tile`).
 __device__ __forceinline__ void fused_tile(const SparseArgs& a, char* __restrict__ next,
                                            const char* __restrict__ tile,
-                                           const SFetchT<true>& f, __amdgpu_buffer_rsrc_t pool,
-                                           int32_t pr, int w, const bf16x8* qreg,
+                                           const SFetchPre<true>& f, __amdgpu_buffer_rsrc_t pool,
+                                           int32_t pr, int w, int lane, const bf16x8* qreg,
                                            const bf16x8* dreg, const BOffsets& bo, int T, int n_t,
                                            int g, float lse2, float delta, f32x4* acc) {
   // step i = 2 ks + mb reads the row operand of key block mb, channel step ks
@@ -65,7 +69,7 @@ __device__ __forceinline__ void fused_tile(const SparseArgs& a, char* __restrict
     const int mb = i & 1, ks = i >> 1;
     s[mb] = mfma16(kr[i], qreg[ks], s[mb]);
     if (ks < 16) dp[mb] = mfma16(kr[i], dreg[ks], dp[mb]);
-    if (i < 9) f.issue_one(next, pool, pr, w, i);
+    if (i < 9) f.issue_one(next, pool, pr, w, i, lane);
     mfma_fence();
   }
   // dS of keys T*32 + 16 mb + 4 g + r (lane: head c), zero past the key list
@@ -92,8 +96,69 @@ __device__ __forceinline__ void fused_tile(const SparseArgs& a, char* __restrict
   }
 }
 
+// Pipelined form: step T issues the S^T / dP^T MFMAs of tile T (C-row
+// operands from `tile`) interleaved with the dq product of tile T - 1
+// (transposed operands from `prev`, dS operand `dsb` from the previous step),
+// so both halves' LDS reads spread over the step; the dq product runs kPLag
+// MFMA steps behind, and tile T's dS is formed between its last MFMAs.  On
+// return dsb holds tile T's dS operand.  kFirst: no previous tile.
+constexpr int kPSlots = 4;
+constexpr int kPTAhead = 4;   // transposed operands in flight
+constexpr int kPLag = 8;      // the dq product of tile T - 1 starts at step kPLag
+
+template <bool kFirst>
+__device__ __forceinline__ void fused_step(const SparseArgs& a, char* __restrict__ next,
+                                           const char* __restrict__ tile,
+                                           const char* __restrict__ prev,
+                                           const SFetchPre<true>& f, __amdgpu_buffer_rsrc_t pool,
+                                           int32_t pr, int w, int lane, const bf16x8* qreg,
+                                           const bf16x8* dreg, const BOffsets& bo, int T, int n_t,
+                                           int g, float lse2, float delta, f32x4* acc,
+                                           bf16x8& dsb) {
+  bf16x8 kr[36], kt[36];
+  float dsv[8];
+#pragma unroll
+  for (int i = 0; i < kFAhead; ++i) kr[i] = b_row16(tile, bo, i & 1, i >> 1);
+  mfma_fence();
+  f32x4 s[2] = {zero4(), zero4()}, dp[2] = {zero4(), zero4()};
+#pragma unroll
+  for (int i = 0; i < 36 + kPLag; ++i) {
+    if (i < 36) {
+      if (i + kFAhead < 36)
+        kr[i + kFAhead] = b_row16(tile, bo, (i + kFAhead) & 1, (i + kFAhead) >> 1);
+      const int mb = i & 1, ks = i >> 1;
+      s[mb] = mfma16(kr[i], qreg[ks], s[mb]);
+      if (ks < 16) dp[mb] = mfma16(kr[i], dreg[ks], dp[mb]);
+    }
+    if (i < 9) f.issue_one(next, pool, pr, w, i, lane);
+    if (!kFirst) {
+      // transposed operands run kPTAhead MFMAs ahead of the dq product
+      if (i >= kPLag - kPTAhead && i - (kPLag - kPTAhead) < 36) {
+        const int db = i - (kPLag - kPTAhead);
+        kt[db] = b_col8(prev, bo, db);
+      }
+      if (i >= kPLag) {
+        const int db = i - kPLag;
+        acc[db] = mfma16(kt[db], dsb, acc[db]);
+      }
+    }
+    if (i >= 36) {
+      // dS of key T*32 + 16 mb + 4 g + r, element i - 36 = 4 mb + r
+      const int e = i - 36, mb = e >> 2, r = e & 3;
+      float p = __builtin_amdgcn_exp2f(fmaf(s[mb][r], a.scale_log2, -lse2));
+      if (T * kKeys + 16 * mb + 4 * g + r >= n_t) p = 0.f;
+      dsv[e] = p * (dp[mb][r] - delta);
+    }
+    mfma_fence();
+  }
+  f32x4 lo = {dsv[0], dsv[1], dsv[2], dsv[3]}, hi = {dsv[4], dsv[5], dsv[6], dsv[7]};
+  dsb = (g & 1) ? pack_halves(hi, lo) : pack_halves(lo, hi);
+}
+
+template <bool kPipe>
 __global__ __launch_bounds__(256, 1) void sparse_bwd_fused_kernel(SparseArgs a) {
-  __shared__ __attribute__((aligned(1024))) char smem[kFBSlots * kTile];
+  constexpr int kSl = kPipe ? kPSlots : kFBSlots;
+  __shared__ __attribute__((aligned(1024))) char smem[kSl * kTile];
   const int tid = threadIdx.x, lane = tid & 63;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int c = lane & 15, g = lane >> 4;
@@ -109,14 +174,17 @@ __global__ __launch_bounds__(256, 1) void sparse_bwd_fused_kernel(SparseArgs a) 
   const __amdgpu_buffer_rsrc_t pool = pool_rsrc(a.latent);
   auto clamp = [&](int T) { return T < n_tiles ? T : n_tiles - 1; };
 
-  SFetchT<true> f;
+  SFetchT<true> fr;   // row lists
+  SFetchPre<true> f;
   f.init(lane, w);
   const BOffsets bo = b_offsets(lane);
   // the row lists of the first three tiles load before any tile does
-  const int32_t r0 = f.rows_of(phys_t, 0, lane), r1 = f.rows_of(phys_t, clamp(1), lane);
-  int32_t pr = f.rows_of(phys_t, clamp(2), lane), pn;
-  f.issue(smem, pool, r0, w);
-  f.issue(smem + kTile, pool, r1, w);
+  const int32_t r0 = fr.rows_of(phys_t, 0, lane), r1 = fr.rows_of(phys_t, clamp(1), lane);
+  int32_t pr = fr.rows_of(phys_t, clamp(2), lane), pn;
+#pragma unroll
+  for (int i = 0; i < 9; ++i) f.issue_one(smem, pool, r0, w, i, lane);
+#pragma unroll
+  for (int i = 0; i < 9; ++i) f.issue_one(smem + kTile, pool, r1, w, i, lane);
 
   bf16x8 qreg[18], dreg[16];   // B operands: head c, channels 32 ks + 8 g .. +7
   {
@@ -136,16 +204,42 @@ __global__ __launch_bounds__(256, 1) void sparse_bwd_fused_kernel(SparseArgs a) 
   wait_fetch();
   tile_barrier();
 
-  for (int T = 0; T < n_tiles; ++T) {
-    pn = f.rows_of(phys_t, clamp(T + 3), lane);
+  if (kPipe) {
+    bf16x8 dsb;
+    pn = fr.rows_of(phys_t, clamp(3), lane);
     __builtin_amdgcn_sched_barrier(0);   // the row list loads ahead of this stage's direct loads
-    fused_tile(a, smem + ((T + 2) % kFBSlots) * kTile, smem + (T % kFBSlots) * kTile, f, pool,
-               pr, w, qreg, dreg, bo, T, n_t, g, lse2, delta, acc);
+    fused_step<true>(a, smem + 2 * kTile, smem, smem, f, pool, pr, w, lane, qreg, dreg, bo, 0, n_t, g,
+                     lse2, delta, acc, dsb);
     pr = pn;
-    __builtin_amdgcn_s_waitcnt(0x0F79);   // vmcnt(9): only this iteration's stage may be in flight
+    __builtin_amdgcn_s_waitcnt(0x0F79);   // vmcnt(9): only this iteration's stage in flight
     tile_barrier();
+    for (int T = 1; T < n_tiles; ++T) {
+      pn = fr.rows_of(phys_t, clamp(T + 3), lane);
+      __builtin_amdgcn_sched_barrier(0);
+      fused_step<false>(a, smem + ((T + 2) % kSl) * kTile, smem + (T % kSl) * kTile,
+                        smem + ((T + kSl - 1) % kSl) * kTile, f, pool, pr, w, lane, qreg, dreg, bo, T,
+                        n_t, g, lse2, delta, acc, dsb);
+      pr = pn;
+      __builtin_amdgcn_s_waitcnt(0x0F79);
+      tile_barrier();
+    }
+    wait_fetch();   // no direct load is left in flight (the last tile's slot was never a target)
+    // the last tile's dq product
+    const char* last = smem + ((n_tiles - 1) % kSl) * kTile;
+#pragma unroll
+    for (int db = 0; db < 36; ++db) acc[db] = mfma16(b_col8(last, bo, db), dsb, acc[db]);
+  } else {
+    for (int T = 0; T < n_tiles; ++T) {
+      pn = fr.rows_of(phys_t, clamp(T + 3), lane);
+      __builtin_amdgcn_sched_barrier(0);   // the row list loads ahead of this stage's direct loads
+      fused_tile(a, smem + ((T + 2) % kSl) * kTile, smem + (T % kSl) * kTile, f, pool, pr, w,
+                 lane, qreg, dreg, bo, T, n_t, g, lse2, delta, acc);
+      pr = pn;
+      __builtin_amdgcn_s_waitcnt(0x0F79);   // vmcnt(9): only this iteration's stage in flight
+      tile_barrier();
+    }
+    wait_fetch();   // no direct load is left in flight when the waves end
   }
-  wait_fetch();   // no direct load is left in flight when the waves end
 
   // dq^T block db: channels 16 db + 4 g + {0..3} of head c
   float* dq = a.dq + ((int64_t)t * a.n_heads + head) * kDk + 4 * g;
@@ -162,8 +256,8 @@ __global__ __launch_bounds__(256, 1) void sparse_bwd_fused_kernel(SparseArgs a) 
 
 hipError_t launch_sparse_bwd_fused(const SparseArgs& a, hipStream_t stream) {
   const unsigned tokens8 = (unsigned)((a.n_q + 7) / 8 * 8);
-  hipLaunchKernelGGL(sparse_bwd_fused_kernel, dim3(2 * tokens8, a.n_heads / 128), dim3(256), 0,
-                     stream, a);
+  hipLaunchKernelGGL((sparse_bwd_fused_kernel<LS_SPARSE_PIPE != 0>), dim3(2 * tokens8, a.n_heads / 128),
+                     dim3(256), 0, stream, a);
   return hipGetLastError();
 }
 

@@ -151,6 +151,9 @@ static void sparse() {
               "sparse fetch row %d outside the two rows of instruction %d of wave %d", f.row(i), i, w);
         CHECK(SFetch::first_row(w, i) + 1 < kKeys || f.row(i) == SFetch::first_row(w, i),
               "sparse fetch of wave %d instruction %d needs a row past the tile", w, i);
+        CHECK(SFetch::first_row(w, i) == 8 * w + (8 * i) / 9, "first row of wave %d instruction %d", w, i);
+        CHECK((f.row(i) != SFetch::first_row(w, i)) == (lane >= SFetch::second_lane(i)),
+              "second-row lanes of wave %d instruction %d lane %d", w, i, lane);
       }
     }
   for (int v : tag) CHECK(v >= 0, "sparse fetch leaves a slot unwritten");
