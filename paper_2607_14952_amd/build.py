@@ -16,7 +16,7 @@ CSRC = os.path.join(PKG, "csrc")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "liblongstraw.so")
 SOURCES = ["api.hip", "small_kernels.hip", "f32_generic.hip", "fwd_bf16.hip", "bwd_bf16.hip",
-           "sparse_fwd.hip", "sparse_bwd.hip", "sparse_fused.hip", "dsa_select.hip"]
+           "sparse_fwd.hip", "sparse_bwd.hip", "sparse_keys.hip", "dsa_select.hip"]
 # Per-source extra flags.  The MFMA kernels keep their accumulators in arch VGPRs
 # (AGPRs only as overflow), which avoids VGPR<->AGPR copies of the output tile.
 EXTRA = {"fwd_bf16.hip": ["-mllvm", "--amdgpu-mfma-vgpr-form=1"],
@@ -25,8 +25,6 @@ EXTRA = {"fwd_bf16.hip": ["-mllvm", "--amdgpu-mfma-vgpr-form=1"],
                             "-mllvm", "-disable-promote-alloca-to-lds"],
          "sparse_bwd.hip": ["-mllvm", "--amdgpu-mfma-vgpr-form=1",
                             "-mllvm", "-disable-promote-alloca-to-lds"],
-         "sparse_fused.hip": ["-mllvm", "--amdgpu-mfma-vgpr-form=1",
-                              "-mllvm", "-disable-promote-alloca-to-lds"],
          "dsa_select.hip": ["-mllvm", "-disable-promote-alloca-to-lds"]}
 ARCH = os.environ.get("LS_OFFLOAD_ARCH", "gfx950")
 

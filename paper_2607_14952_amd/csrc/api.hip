@@ -14,10 +14,6 @@
 
 #define LS_API extern "C" __attribute__((visibility("default")))
 
-// The sparse backward runs as one fused pass (sparse_fused.hip) unless this is 0.
-#ifndef LS_SPARSE_FUSED
-#define LS_SPARSE_FUSED 1
-#endif
 
 namespace {
 
@@ -465,12 +461,12 @@ namespace {
 
 // Sparse workspace: the resolved key lists [n_q, n_max] int32 and their
 // lengths [n_q] int32 (both passes), then for the backward Delta and
-// lse * log2(e) [H, n_q] fp32 and dS [n_q, H, n_max] bf16; each padded to 256 B.
+// lse * log2(e) [H, n_q] fp32; each padded to 256 B.
 struct SparseLayout {
   int64_t n_max;      // key-list length padded to a whole 32-key tile
-  size_t phys_bytes, ntok_bytes, stat_bytes, ds_bytes;
+  size_t phys_bytes, ntok_bytes, stat_bytes;
   size_t fwd_bytes() const { return phys_bytes + ntok_bytes; }
-  size_t bwd_bytes() const { return fwd_bytes() + 2 * stat_bytes + ds_bytes; }
+  size_t bwd_bytes() const { return fwd_bytes() + 2 * stat_bytes; }
 };
 
 size_t pad256(size_t x) { return (x + 255) / 256 * 256; }
@@ -482,7 +478,6 @@ SparseLayout sparse_layout(const ls_attn_params* p, int32_t topk) {
   L.phys_bytes = pad256((size_t)p->n_q * L.n_max * 4);
   L.ntok_bytes = pad256((size_t)p->n_q * 4);
   L.stat_bytes = pad256((size_t)p->n_q * p->n_q_heads * 4);
-  L.ds_bytes = pad256((size_t)p->n_q * p->n_q_heads * L.n_max * 2);
   return L;
 }
 
@@ -700,18 +695,13 @@ LS_API ls_status ls_sparse_attn_bwd(const ls_attn_params* p, const int32_t* idx,
   float* lse2 = (float*)(w + L.stat_bytes);
   a.delta = delta;
   a.lse2 = lse2;
-  a.ds = (__bf16*)(w + 2 * L.stat_bytes);
   a.d_out = d_out;
   a.dq = dq;
   hipError_t e = ls::launch_sparse_phys(a, s);
   if (e == hipSuccess)
     e = ls::launch_bwd_prep(d_out, out, true, out_dtype == LS_BF16, lse, p->n_q, p->n_q_heads,
                             512, delta, lse2, s);
-#if LS_SPARSE_FUSED
-  if (e == hipSuccess) e = ls::launch_sparse_bwd_fused(a, s);
-#else
   if (e == hipSuccess) e = ls::launch_sparse_bwd(a, s);
-#endif
   return e == hipSuccess ? LS_OK : hip_fail(e, "sparse backward launch");
 }
 

@@ -102,7 +102,6 @@ struct SparseArgs {
   const void* d_out;         // [n_q, H, 512] bf16
   const float* delta;        // [H, n_q]
   const float* lse2;         // [H, n_q]
-  __bf16* ds;                // workspace [n_q, H, n_max]
   float* dq;                 // [n_q, H, 576]
   int64_t prefix_len, kv_len, window0;   // window0 = q_pos0 - prefix_len
   int32_t n_q, n_heads, topk, n_max, log2_page;
@@ -114,7 +113,6 @@ struct SparseArgs {
 hipError_t launch_sparse_phys(const SparseArgs& a, hipStream_t stream);
 hipError_t launch_sparse_fwd(const SparseArgs& a, hipStream_t stream);
 hipError_t launch_sparse_bwd(const SparseArgs& a, hipStream_t stream);
-hipError_t launch_sparse_bwd_fused(const SparseArgs& a, hipStream_t stream);
 hipError_t launch_gather(const void* k_pool, const void* v_pool, const int32_t* page_table,
                          int64_t pos_begin, int64_t pos_end, int log2_page, int64_t k_row_elems,
                          int64_t v_row_elems, int esize, void* k_out, void* v_out,

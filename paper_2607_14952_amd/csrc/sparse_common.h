@@ -5,12 +5,15 @@
 // 576-wide latent row, values its first 512 channels).  All heads share one
 // latent row per position (one KV head).
 //
-// Key lists are resolved to physical latent rows once per call.  A workgroup
-// owns one token, lanes own heads (scores computed transposed, S^T = K Q^T).
-// Gathered rows (1152 bytes) stream by direct global->LDS loads into a ring
-// of tiles (four slots in the forward, three in the backward); 16-byte chunks are permuted inside aligned 8-chunk groups
-// so row reads and transposing column reads are bank-conflict free.
-// The forward kernel is in sparse_fwd.hip, the dq backward in sparse_bwd.hip.
+// Key lists are resolved to physical latent rows once per call
+// (sparse_keys.hip).  A workgroup owns one token (the forward, all heads) or
+// half of its heads (the backward); lanes own heads (scores computed
+// transposed, S^T = K Q^T).  Gathered rows (1152 bytes) stream by direct
+// global->LDS loads into a ring of four tile slots; 16-byte chunks are
+// permuted inside aligned 8-chunk groups so row reads and transposing column
+// reads are bank-conflict free (s_swz for the forward's 32x32x16 operands,
+// b_swz for the backward's 16x16x32 ones).  The forward kernel is in
+// sparse_fwd.hip, the dq backward in sparse_bwd.hip.
 #pragma once
 #include <math.h>
 
@@ -25,7 +28,6 @@ constexpr int kDv = 512;
 constexpr int kRow = kDk * 2;                 // 1152 bytes per latent row
 constexpr int kKeys = 32;                     // keys per tile
 constexpr int kTile = kKeys * kRow;           // 36 KiB
-constexpr int kSlots = 3;
 constexpr int kChunks = kRow / 16;            // 72
 
 // Chunk swizzle of a 1152-byte-row tile: chunk c of row k is stored at
