@@ -211,6 +211,58 @@ def write_util_md(directory: str, out_path: str, command: str, title: str,
         f.write("\n".join(lines) + "\n")
 
 
+WAIT_COUNTERS = ["SQ_WAVE_CYCLES", "SQ_WAIT_ANY", "SQ_WAIT_INST_ANY", "SQ_ACTIVE_INST_ANY",
+                 "SQ_ACTIVE_INST_VALU", "SQ_INSTS_VALU", "SQ_INSTS_LDS", "SQ_WAIT_INST_LDS"]
+
+
+def write_waits_md(directory: str, out_path: str, command: str, title: str,
+                   min_ms: float = 1.0) -> None:
+    """Per kernel (median dispatch longer than min_ms): where the waves' cycles
+    go, as shares of SQ_WAVE_CYCLES (issuing any instruction, issuing VALU
+    instructions, waiting on a counter before the next instruction, waiting at
+    all), and the VALU and LDS instructions per dispatch."""
+    files = _find(directory, "counter_collection.csv")
+    if not files:
+        raise FileNotFoundError(f"no counter_collection.csv under {directory}")
+    disp = defaultdict(dict)
+    meta = {}
+    with open(files[0]) as f:
+        for row in csv.DictReader(f):
+            d = _col(row, "Dispatch_Id", "DispatchId", "Correlation_Id")
+            c = _col(row, "Counter_Name", "CounterName")
+            disp[d][c] = disp[d].get(c, 0.0) + float(_col(row, "Counter_Value", "CounterValue"))
+            ns = int(_col(row, "End_Timestamp", "EndTimestamp")) - int(
+                _col(row, "Start_Timestamp", "StartTimestamp"))
+            meta[d] = (_col(row, "Kernel_Name", "KernelName", "Name"), ns)
+    per = defaultdict(list)
+    for d, c in disp.items():
+        name, ns = meta[d]
+        if ns / 1e6 >= min_ms and c.get("SQ_WAVE_CYCLES"):
+            per[name].append((ns, c))
+    lines = [f"# {title}", "", "Command (run from the repository root on one MI355X):", "",
+             "```", command, "```", "",
+             f"Kernel sources: `{source_hash()}` (sha256/16 of `paper_2607_14952_amd/csrc`).", "",
+             f"Per kernel, the dispatch with the median duration among those longer than {min_ms} "
+             "ms. Shares are of SQ_WAVE_CYCLES: issuing any instruction (SQ_ACTIVE_INST_ANY), "
+             "issuing VALU instructions including MFMAs (SQ_ACTIVE_INST_VALU), waiting for a "
+             "counter before the next instruction (SQ_WAIT_INST_ANY), waiting at all (SQ_WAIT_ANY), "
+             "and waiting for LDS (SQ_WAIT_INST_LDS).", "",
+             "| kernel | ms | issue any % | issue VALU % | wait for counter % | wait any % | "
+             "wait LDS % | VALU instructions | LDS instructions |",
+             "|---|---:|---:|---:|---:|---:|---:|---:|---:|"]
+    for name, lst in sorted(per.items(), key=lambda kv: -sum(ns for ns, _ in kv[1])):
+        lst.sort(key=lambda t: t[0])
+        ns, c = lst[len(lst) // 2]
+        wc = c["SQ_WAVE_CYCLES"]
+        pct = lambda k: 100 * c.get(k, 0) / wc  # noqa: E731
+        lines.append(f"| `{name[:90]}` | {ns / 1e6:.3f} | {pct('SQ_ACTIVE_INST_ANY'):.1f} | "
+                     f"{pct('SQ_ACTIVE_INST_VALU'):.1f} | {pct('SQ_WAIT_INST_ANY'):.1f} | "
+                     f"{pct('SQ_WAIT_ANY'):.1f} | {pct('SQ_WAIT_INST_LDS'):.1f} | "
+                     f"{c.get('SQ_INSTS_VALU', 0):.3g} | {c.get('SQ_INSTS_LDS', 0):.3g} |")
+    with open(out_path, "w") as f:
+        f.write("\n".join(lines) + "\n")
+
+
 def write_traffic(fetch_dir: str, write_dir: str, out_path: str, calib_bytes: int,
                   command: str) -> dict:
     fetch = counter_per_dispatch(fetch_dir, "FETCH_SIZE")
@@ -283,6 +335,13 @@ def main():
     u.add_argument("out")
     u.add_argument("--command", required=True)
     u.add_argument("--title", default="rocprofv3 MFMA and LDS utilization")
+    u.add_argument("--min-ms", type=float, default=1.0)
+    wt = sub.add_parser("waits")
+    wt.add_argument("directory")
+    wt.add_argument("out")
+    wt.add_argument("--command", required=True)
+    wt.add_argument("--title", default="rocprofv3 issue and wait counters")
+    wt.add_argument("--min-ms", type=float, default=1.0)
     b = sub.add_parser("traffic")
     b.add_argument("fetch_dir")
     b.add_argument("write_dir")
@@ -293,7 +352,9 @@ def main():
     if args.cmd == "stats":
         write_stats_md(args.directory, args.out, args.command, args.title)
     elif args.cmd == "util":
-        write_util_md(args.directory, args.out, args.command, args.title)
+        write_util_md(args.directory, args.out, args.command, args.title, args.min_ms)
+    elif args.cmd == "waits":
+        write_waits_md(args.directory, args.out, args.command, args.title, args.min_ms)
     else:
         write_traffic(args.fetch_dir, args.write_dir, args.out, args.calib_bytes, args.command)
 
