@@ -42,17 +42,13 @@ constexpr int kChunks = kRow / 16;            // 72
 // 4 chunks cover all 16 bank groups).
 __host__ __device__ inline int s_swz(int k) { return (((k >> 1) & 1) << 2) | ((k >> 2) & 3); }
 
-// Chunk swizzle of the fused backward's tiles (16x16x32 operands): bits 1, 2, 3
-// of the row go to bits 1, 2, 0.  Like s_swz it is a bijection on the even and
-// on the odd rows of any 16 consecutive aligned rows (a 16-lane phase of row
-// reads covers all 16 bank groups).  Its transposed reads take 4 consecutive
-// aligned rows x 2 chunks per 16 lanes, and a 32-lane phase pairs row quads
-// (0, 5), (4, 1), (2, 7) and (6, 3) of the tile (b_offsets): in every pair the
-// four even rows have distinct b_swz >> 1 and so do the four odd rows, so the
-// phase's 8 rows x 2 chunks cover all 16 bank groups.
-__host__ __device__ inline int b_swz(int k) {
-  return (((k >> 1) & 1) << 1) | (((k >> 2) & 1) << 2) | ((k >> 3) & 1);
-}
+// Chunk swizzle of the fused backward's tiles (16x16x32 operands): the low
+// three bits of the row.  Its row reads take 16 rows x 4 consecutive chunks
+// per instruction and its transposed reads 8 rows x 2 chunks per 32 lanes;
+// both read conflict-free on gfx950 (SQ_LDS_BANK_CONFLICT probe: 4 cycles per
+// 16-byte read, 2 per transposing read), which s_swz does not give for the
+// row reads (8 cycles).
+__host__ __device__ inline int b_swz(int k) { return k & 7; }
 template <bool kAlt>
 __host__ __device__ inline int tile_swz(int k) { return kAlt ? b_swz(k) : s_swz(k); }
 
@@ -239,7 +235,7 @@ __host__ __device__ inline BOffsets b_offsets(int lane) {
   const int c = lane & 15, g = lane >> 4;
   o.row0 = c * kRow + 16 * (g ^ b_swz(c));
   const int x = (c & 3) >> 1;                       // chunk within the 2-chunk column block
-  const int sw = b_swz(4 * g + (c >> 2));            // rows key_base + (c >> 2): same bits 1-3
+  const int sw = b_swz(4 * g + (c >> 2));            // rows key_base + (c >> 2): same low three bits
   const int col0 = (c >> 2) * kRow + 16 * (x ^ sw) + 8 * (c & 1);
 #pragma unroll
   for (int k = 0; k < 2; ++k) o.col[k] = key_base(g, k) * kRow + col0;

@@ -42,6 +42,18 @@ static void check_b128_phases(const int* off, const char* what) {
   }
 }
 
+// distinct 16-byte bank groups within each eight consecutive lanes
+static void check_b128_octets(const int* off, const char* what) {
+  for (int oc = 0; oc < 8; ++oc) {
+    int seen = 0;
+    for (int l = 8 * oc; l < 8 * oc + 8; ++l) {
+      const int g = (off[l] & 255) >> 4;
+      CHECK(!(seen & (1 << g)), "%s: two lanes of octet %d on one bank group, lane %d", what, oc, l);
+      seen |= 1 << g;
+    }
+  }
+}
+
 // distinct 8-byte bank pairs within each 32-lane phase
 static void check_b64_phases(const int* off, const char* what) {
   for (int ph = 0; ph < 2; ++ph) {
@@ -183,7 +195,14 @@ static void sparse() {
     }
 }
 
-// The fused sparse backward's tiles (b_swz, 16x16x32 operands).
+// The fused sparse backward's tiles (b_swz, 16x16x32 operands).  Its row reads
+// (16 rows x 4 chunks per instruction) fall outside the 16-lanes-per-phase
+// model: that model flags lanes l and l + 8 (rows r and r + 8, one bank group),
+// yet the hardware's SQ_LDS_BANK_CONFLICT counter reads zero for every one of
+// the 36 row-read and 72 transposing-read steps of this layout (3.9 and 2.0
+// LDS cycles per instruction), while the s_swz layout costs 7.9 cycles on the
+// row reads.  The row reads are checked for distinct bank groups within each
+// eight consecutive lanes, which the measured layout satisfies.
 static void fused() {
   using namespace ls::sparse;
   const int cols = kRow / 2;
@@ -213,7 +232,7 @@ static void fused() {
           CHECK(tag[off[l] / 2 + e] == key * cols + c0 + e, "fused row operand mb=%d ks=%d lane=%d e=%d",
                 mb, ks, l, e);
       }
-      check_b128_phases(off, "fused row operand");
+      check_b128_octets(off, "fused row operand");
     }
   for (int db = 0; db < 36; ++db)
     for (int k = 0; k < 2; ++k) {
