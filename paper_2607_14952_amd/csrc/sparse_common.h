@@ -172,6 +172,11 @@ struct SFetchT {
     __builtin_amdgcn_raw_ptr_buffer_load_lds(r, LS_LDS(tile + (9 * w + i) * 1024), 16, (int)off, 0,
                                              0, 0);
   }
+  // (the form of SFetchPre::issue_one; the lane is not needed here)
+  __device__ __forceinline__ void issue_one(char* tile, __amdgpu_buffer_rsrc_t r, int32_t rows,
+                                            int w, int i, int) const {
+    issue_one(tile, r, rows, w, i);
+  }
   __device__ __forceinline__ void issue(char* tile, __amdgpu_buffer_rsrc_t r, int32_t rows,
                                         int w) const {
 #pragma unroll
@@ -293,6 +298,57 @@ __device__ __forceinline__ f32x16 s_scores(const char* tile, const bf16x8* qreg,
   return s;
 }
 
+// The forward's output accumulator (32 heads x 512 columns: 256 registers)
+// and its Q operand (144) do not fit the 256 VGPRs that MFMAs in VGPR form
+// accumulate in; the compiler then moves most of the accumulator between AGPRs
+// and VGPRs around every PV product (hundreds of moves per tile).  The PV
+// MFMA is therefore written with its accumulator in AGPRs (C and D in the AGPR
+// file, as the instruction allows), while the score MFMAs keep VGPR form.  The
+// compiler does not see inside the asm, so the wait states it would insert are
+// explicit:
+//  - two before an MFMA whose B operand (P) a VALU instruction may just have
+//    written;
+//  - back-to-back accumulation into the same registers needs none;
+//  - VALU access to the accumulators (the rare rescale, the final read) goes
+//    through acc_fence, an asm of 24 wait states (more than an MFMA result
+//    needs before a VALU reads or overwrites it) that takes every accumulator
+//    as an in/out operand, so that nothing moves across it.
+#ifndef LS_SPARSE_FWD_AGPR
+#define LS_SPARSE_FWD_AGPR 1
+#endif
+template <bool kAfterValu>
+__device__ __forceinline__ void mfma32_agpr(f32x16& acc, const bf16x8& a, const bf16x8& b) {
+  if (kAfterValu)
+    asm volatile("s_nop 1\n\tv_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+a"(acc) : "v"(a), "v"(b));
+  else
+    asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+a"(acc) : "v"(a), "v"(b));
+}
+__device__ __forceinline__ void acc_fence(f32x16* o) {
+#if LS_SPARSE_FWD_AGPR
+  asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7"
+               : "+a"(o[0]), "+a"(o[1]), "+a"(o[2]), "+a"(o[3]), "+a"(o[4]), "+a"(o[5]),
+                 "+a"(o[6]), "+a"(o[7]), "+a"(o[8]), "+a"(o[9]), "+a"(o[10]), "+a"(o[11]),
+                 "+a"(o[12]), "+a"(o[13]), "+a"(o[14]), "+a"(o[15]));
+#endif
+}
+
+// o[i] *= alpha for the 16 accumulator blocks, one block at a time (each block
+// is read, scaled and written back to the AGPR file before the next, so at
+// most one block's 16 values occupy VGPRs).
+__device__ __forceinline__ void acc_scale(f32x16* o, float alpha) {
+  acc_fence(o);
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    f32x16 v = o[i] * alpha;
+#if LS_SPARSE_FWD_AGPR
+    asm volatile("" : "+a"(v));
+#endif
+    o[i] = v;
+    __builtin_amdgcn_sched_barrier(0);
+  }
+  acc_fence(o);
+}
+
 // oacc[db] += V^T P^T for value-column blocks db0 .. db0 + kNdb - 1 (operand
 // i: block db0 + i/2, key half i%2).
 template <int kNdb>
@@ -307,7 +363,12 @@ __device__ __forceinline__ void s_pv(const char* tile, const bf16x8& p0, const b
 #pragma unroll
   for (int i = 0; i < 2 * kNdb; ++i) {
     if (i + kSVAhead < 2 * kNdb) vr[i + kSVAhead] = read(i + kSVAhead);
+#if LS_SPARSE_FWD_AGPR
+    if (i < 2) mfma32_agpr<true>(oacc[i >> 1], vr[i], (i & 1) ? p1 : p0);
+    else mfma32_agpr<false>(oacc[i >> 1], vr[i], (i & 1) ? p1 : p0);
+#else
     oacc[i >> 1] = mfma32(vr[i], (i & 1) ? p1 : p0, oacc[i >> 1]);
+#endif
     mfma_fence();
   }
 }

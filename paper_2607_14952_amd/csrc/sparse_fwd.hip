@@ -12,6 +12,8 @@
 // flight, and the two kinds of direct load into a slot share its pointer.
 // Tokens with more keys (later ones: the response window grows with t) are
 // dispatched first.
+#include <type_traits>
+
 #include "sparse_common.h"
 
 namespace ls {
@@ -19,6 +21,12 @@ namespace {
 using namespace sparse;
 
 constexpr int kFSlots = 4;
+#ifndef LS_SPARSE_FWD_PRE
+#define LS_SPARSE_FWD_PRE 1
+#endif
+// In-loop direct loads with lane offsets inside a row computed once (9
+// registers) or recomputed per load.
+using FwdFetch = std::conditional_t<LS_SPARSE_FWD_PRE != 0, SFetchPre<false>, SFetch>;
 constexpr int kSlotBytes = kTile + 4 * 256;   // tile + 4 waves x 64 row entries
 
 // One tile.  `next` and `tile` are distinct ring slots; the restrict
@@ -27,13 +35,14 @@ constexpr int kSlotBytes = kTile + 4 * 256;   // tile + 4 waves x 64 row entries
 // `tile`'s row area; the stage carries the rows of tile T_rows into `next`'s.
 __device__ __forceinline__ void fwd_tile(const SparseArgs& a, char* __restrict__ next,
                                          const char* __restrict__ tile, const SFetch& f,
+                                         const FwdFetch& fl,
                                          __amdgpu_buffer_rsrc_t pool, int w,
                                          const bf16x8* qreg, const SOffsets& so, int T, int n_t,
                                          int hh, f32x16* oacc, float& m_run, float& l_run,
                                          __amdgpu_buffer_rsrc_t phys_t, int T_rows, int lane) {
   const int32_t pr = reinterpret_cast<const int32_t*>(tile + kTile + 256 * w)[lane];
   f32x16 s = s_scores(tile, qreg, so, [&](int i) {
-    f.issue_one(next, pool, pr, w, i);
+    fl.issue_one(next, pool, pr, w, i, lane);
     if (i == 8)
       f.rows_to_lds(reinterpret_cast<int32_t*>(next + kTile + 256 * w), phys_t, T_rows, lane);
   });
@@ -44,10 +53,7 @@ __device__ __forceinline__ void fwd_tile(const SparseArgs& a, char* __restrict__
   }
   const float alpha = softmax_step(s, a.scale_log2, m_run, l_run);
   // (l_run < 0 never holds; it keeps the exponentials ahead of this branch)
-  if (__any(alpha != 1.f || l_run < 0.f)) {
-#pragma unroll
-    for (int i = 0; i < 16; ++i) oacc[i] *= alpha;
-  }
+  if (__any(alpha != 1.f || l_run < 0.f)) acc_scale(oacc, alpha);
   s_pv<16>(tile, pack8(s, 0), pack8(s, 1), oacc, so, 0);
 }
 
@@ -69,6 +75,8 @@ __global__ __launch_bounds__(256, 1) void sparse_fwd_kernel(SparseArgs a) {
 
   SFetch f;
   f.init(lane, w);
+  FwdFetch fl;
+  fl.init(lane, w);
   const SOffsets so = s_offsets(lane);
   // the row lists of the first three tiles and Q load before any tile does
   const int32_t r0 = f.rows_of(phys_t, 0, lane), r1 = f.rows_of(phys_t, clamp(1), lane),
@@ -98,13 +106,14 @@ __global__ __launch_bounds__(256, 1) void sparse_fwd_kernel(SparseArgs a) {
   tile_barrier();
 
   for (int T = 0; T < n_tiles; ++T) {
-    fwd_tile(a, smem + ((T + 3) % kFSlots) * kSlotBytes, smem + (T % kFSlots) * kSlotBytes, f,
+    fwd_tile(a, smem + ((T + 3) % kFSlots) * kSlotBytes, smem + (T % kFSlots) * kSlotBytes, f, fl,
              pool, w, qreg, so, T, n_t, hh, oacc, m_run, l_run, phys_t, clamp(T + 6), lane);
     // vmcnt(20): the stages of tiles T + 2 and T + 3 may be in flight
     __builtin_amdgcn_s_waitcnt(0x4F74);
     tile_barrier();
   }
   wait_fetch();   // no direct load is left in flight when the waves end
+  acc_fence(oacc);
 
   const float l_tot = half_sum(l_run);
   const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
