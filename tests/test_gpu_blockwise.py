@@ -107,11 +107,16 @@ def test_blockwise_c4_block_geometry():
 
 @pytest.mark.timeout(1200)
 def test_c4_full_size_sampled():
-    """c4 at full size: sampled rows and the last two response keys.  A key that
-    a second block also reaches is seen by at least 2,049 rows, whose fp64
-    forward over the 4.46M prefix (~150 TFLOP) is beyond the oracle's reach
-    here; the block geometry case above covers that accumulation."""
+    """c4 at full size: in each of the four 2,048-token blocks, both sides of
+    the block edge and of the dq (16-token) and forward (32-token) workgroup
+    boundaries at its start, middle and end (48 rows), and the last two response
+    keys.  A key that a second block also reaches is seen by at least 2,049
+    rows, whose fp64 forward over the 4.46M prefix (~150 TFLOP) is beyond the
+    oracle's reach here; the block geometry case above covers that
+    accumulation."""
     cfg = configs.C4
     R = cfg.resp_len
-    rows = [0, 2047, 2048, 6000, R - 1]
+    rows = sorted({b + o for b in range(0, R, cfg.rows_per_call)
+                   for o in (0, 1, 15, 16, 31, 32, 1023, 1024, 2015, 2016, 2046, 2047)
+                   if b + o < R})
     run_members(cfg, members=[0], rows=rows, keys=[R - 2, R - 1])

@@ -352,25 +352,22 @@ def _wg_boundary_rows(n_tokens, tokens_per_wg, every=1, inner=()):
 
 
 @pytest.mark.timeout(900)
-def test_c2_full_size_sampled():
-    """512 rows: the first and last token of each of the 128 forward
-    workgroups of a (KV head, split) stream (32 tokens x 8 heads = 256 packed
-    rows each), and 256 seeded rows."""
-    R = configs.C2.resp_len
-    rows = _wg_boundary_rows(R, 32)
-    rows += list(np.random.default_rng(22).choice(R, 256, replace=False))
-    _sampled_parity(configs.C2, rows, backward=False)
+def test_c2_full_size():
+    """c2 as bench.py's forward-only configuration runs it: every one of the
+    4,096 tokens' out and lse (16 heads over 262,144 prefix keys), against the
+    fp64 oracle composed over key ranges."""
+    _sampled_parity(configs.C2, np.arange(configs.C2.resp_len), backward=False)
 
 
 @pytest.mark.timeout(900)
 def test_c3_full_size_sampled():
-    """c3 as bench.py times it.  dq on 64+ rows: both sides of the dq (16-token)
-    and forward (32-token) workgroup boundaries in every 8th forward workgroup,
-    the last row, and planted targets.  Response key 3838 is seen by tokens
+    """c3 as bench.py times it.  dq on 512+ rows: both sides of the dq (16-token)
+    and forward (32-token) workgroup boundaries in every forward workgroup, the
+    last row, and planted targets.  Response key 3838 is seen by tokens
     3838 .. 4095, which span the dK/dV row chunks 14 and 15 (256 tokens x 8
     heads = 2048 packed rows each), so its gradient goes through the ordered
     chunk reduction at full size; those 258 rows' out and lse are compared too."""
-    rows = _wg_boundary_rows(configs.C3.resp_len, 32, every=8, inner=(15, 16)) + [4095]
+    rows = _wg_boundary_rows(configs.C3.resp_len, 32, every=1, inner=(15, 16)) + [4095]
     _sampled_parity(configs.C3, rows, backward=True, keys=[3838])
 
 
