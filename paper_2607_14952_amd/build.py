@@ -15,7 +15,8 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "liblongstraw.so")
-SOURCES = ["api.hip", "small_kernels.hip", "f32_generic.hip", "fwd_bf16.hip", "bwd_bf16.hip",
+SOURCES = ["api.hip", "small_kernels.hip", "f32_generic.hip", "fwd_f32_mfma.hip", "fwd_bf16.hip",
+           "bwd_bf16.hip",
            "sparse_fwd.hip", "sparse_bwd.hip", "sparse_keys.hip", "dsa_select.hip"]
 # Per-source extra flags.  The MFMA kernels keep their accumulators in arch VGPRs
 # (AGPRs only as overflow), which avoids VGPR<->AGPR copies of the output tile.

@@ -1,4 +1,6 @@
-// fp32 replay kernels for any head_dim <= 256 and any GQA group.  One wave
+// fp32 replay kernels for any head_dim <= 256 and any GQA group (the forward
+// for head_dim = head_dim_v in {64, 128} runs on the matrix cores instead,
+// fwd_f32_mfma.hip).  One wave
 // owns one (query row, head) -- or, for the response-key gradients, one
 // (key, KV head) -- and walks its keys one at a time with an online softmax;
 // lane l holds channels l, l+64, l+128, l+192.  These serve the fp32
@@ -30,7 +32,7 @@ __global__ __launch_bounds__(256) void fwd_f32_kernel(FwdArgs a) {
   const int64_t pair = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);  // row * Hq + head
   if (pair >= (int64_t)a.n_q * a.n_q_heads) return;
   const int row = (int)(pair / a.n_q_heads), head = (int)(pair - (int64_t)row * a.n_q_heads);
-  const int g = head >> a.log2_group;
+  const int g = head / a.group;   // any group size, not only powers of two
   const int sp = blockIdx.z;
   const int64_t kb = a.split_begin[sp];
   const int64_t ke = min(a.split_end[sp], a.q_pos0 + row + 1);
@@ -87,7 +89,7 @@ __global__ __launch_bounds__(256) void bwd_dq_f32_kernel(BwdArgs a) {
   const int64_t pair = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
   if (pair >= (int64_t)a.n_q * a.n_q_heads) return;
   const int row = (int)(pair / a.n_q_heads), head = (int)(pair - (int64_t)row * a.n_q_heads);
-  const int g = head >> a.log2_group;
+  const int g = head / a.group;   // any group size, not only powers of two
   const int64_t ke = min(a.kv_end, a.q_pos0 + row + 1);
   const float* q = static_cast<const float*>(a.q) + pair * a.head_dim;
   const float* dO = static_cast<const float*>(a.d_out) + pair * a.head_dim_v;
@@ -195,6 +197,7 @@ __global__ __launch_bounds__(256) void bwd_dkdv_f32_kernel(BwdArgs a, int64_t ke
 }  // namespace
 
 hipError_t launch_fwd_f32(const FwdArgs& a, hipStream_t stream) {
+  if (fwd_f32_mfma_fits(a)) return launch_fwd_f32_mfma(a, stream);
   const unsigned blocks = (unsigned)(((int64_t)a.n_q * a.n_q_heads + 3) / 4);
   hipLaunchKernelGGL(fwd_f32_kernel, dim3(blocks, 1, a.n_splits), dim3(256), 0, stream, a);
   return hipGetLastError();

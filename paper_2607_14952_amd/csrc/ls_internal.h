@@ -125,6 +125,10 @@ hipError_t launch_merge(const float* out_part, const float* lse_part, int n_spli
                         int n_heads, int dv, bool out_bf16, bool bf16_numerator, void* out,
                         float* lse, hipStream_t stream);
 hipError_t launch_fwd_f32(const FwdArgs& a, hipStream_t stream);
+// fp32 forward on the matrix cores, for the shapes fwd_f32_mfma_fits accepts
+// (launch_fwd_f32 takes it for them and the generic kernel for the others)
+bool fwd_f32_mfma_fits(const FwdArgs& a);
+hipError_t launch_fwd_f32_mfma(const FwdArgs& a, hipStream_t stream);
 hipError_t launch_hbm_read(const void* buf, int64_t n16, uint32_t* out, hipStream_t stream);
 hipError_t launch_dsa_scores(const DsaArgs& a, hipStream_t stream);
 hipError_t launch_topk(const TopkArgs& a, hipStream_t stream);

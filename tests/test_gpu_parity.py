@@ -112,6 +112,35 @@ def test_c1_tiny_f32():
     full_case(configs.C1)
 
 
+F32_CASES = [
+    # the matrix-core forward (head_dim = head_dim_v in {64, 128}, group a power of two):
+    # 16-position pages, unaligned splits, partial row tiles, planted keys
+    configs.C1.scaled(name="f32_mfma_d64_g4", n_q_heads=8, n_kv_heads=2, resp_len=77,
+                      prefix_len=1000, page_size=16, n_shards=3, splits_per_shard=2,
+                      table="perm", plant_frac=0.01),
+    configs.C1.scaled(name="f32_mfma_d128_g1", n_q_heads=3, n_kv_heads=3, head_dim=128,
+                      head_dim_v=128, resp_len=130, prefix_len=2085, n_shards=2,
+                      splits_per_shard=3, table="perm"),
+    configs.C1.scaled(name="f32_mfma_d64_g16", n_q_heads=16, n_kv_heads=1, resp_len=9,
+                      prefix_len=300, page_size=32, n_shards=1, table="perm"),
+    # the generic kernel: other head dims, and a group of three
+    configs.C1.scaled(name="f32_generic_d96_g3", n_q_heads=6, n_kv_heads=2, head_dim=96,
+                      head_dim_v=96, resp_len=40, prefix_len=700, page_size=16, n_shards=2,
+                      table="perm"),
+    configs.C1.scaled(name="f32_generic_d64_dv128", head_dim=64, head_dim_v=128, resp_len=50,
+                      prefix_len=520, n_shards=2, table="perm"),
+    configs.C1.scaled(name="f32_generic_d64_g3", n_q_heads=3, n_kv_heads=1, resp_len=35,
+                      prefix_len=400, n_shards=2, table="perm"),
+]
+
+
+@pytest.mark.parametrize("cfg", F32_CASES, ids=lambda c: c.name)
+def test_f32_kernels(cfg):
+    """fp32 forward on the matrix cores and on the generic kernel, and the
+    generic backward, against the oracle at the fp32 tolerance."""
+    full_case(cfg)
+
+
 BF16_SMALL = configs.C3.scaled(name="bf16_small", prefix_len=8192, resp_len=300, n_shards=2,
                                splits_per_shard=2, plant_frac=0.01)
 
