@@ -44,7 +44,10 @@
  *   undefined behaviour.
  *
  * Supported shapes: dtype LS_F32 with head_dim, head_dim_v <= 256 (any GQA
- * group); dtype LS_BF16 with head_dim = head_dim_v = 256, n_q_heads /
+ * group; the forward of head_dim = head_dim_v in {64, 128} with a power-of-two
+ * group runs on the matrix cores, the other shapes on a scalar kernel, both
+ * with fp32 products and sums, so results differ in rounding order only);
+ * dtype LS_BF16 with head_dim = head_dim_v = 256, n_q_heads /
  * n_kv_heads dividing 32, n_q * n_q_heads * 512 < 2^31 bytes of queries,
  * fewer than 2^29 logical pages and q_pos0 + n_q < 2^31 (the kernels use
  * 32-bit buffer offsets and 32-bit key positions within a split).
