@@ -178,7 +178,7 @@ def cyclic_owned_positions(prefix_len, page_size, n_shards, shard):
 # --------------------------------------------------------------------------
 def attn_bwd(q, k_pool, v_pool, page_table, d_out, *, page_size, prefix_len, q_pos0, scale,
              kv_begin=0, kv_end=None, out=None, lse=None, rows=None, resp_keys=None,
-             head_dim_v=None, row_block=64):
+             head_dim_v=None, row_block=64, kv_heads=None):
     """Gradients of L = sum(d_out * O) where O is the full replay output.
 
     * ``dq [n_rows, Hq, D]``: contribution of the keys in ``[kv_begin, kv_end)``
@@ -190,7 +190,10 @@ def attn_bwd(q, k_pool, v_pool, page_table, d_out, *, page_size, prefix_len, q_p
 
     ``out``/``lse`` are the full forward over every visible key for all rows
     (computed here in fp64 when not given).  ``rows`` restricts dq to a subset of
-    rows; dk/dv always use every row that sees the key."""
+    rows; dk/dv always use every row that sees the key.  ``kv_heads`` restricts
+    the computation to those KV heads and the query heads of their groups: dq
+    then holds those query heads (in order) and dk/dv those KV heads.  A KV
+    head's gradient sums over its own group only, so its dk/dv are complete."""
     R, Hq, D = q.shape
     Hkv = k_pool.shape[2]
     G = Hq // Hkv
@@ -221,15 +224,17 @@ def attn_bwd(q, k_pool, v_pool, page_table, d_out, *, page_size, prefix_len, q_p
     # Delta_ih = dO_ih . o_ih  (the oracle's own fp64 output)
     delta = np.einsum("rhd,rhd->hr", dO_all[need_rows], o_n)
 
-    dq = np.zeros((dq_rows.size, Hq, D))
-    dk = np.zeros((resp_keys.size, Hkv, D))
-    dv = np.zeros((resp_keys.size, Hkv, Dv))
+    kvh = np.arange(Hkv) if kv_heads is None else np.asarray(kv_heads)
+    dq = np.zeros((dq_rows.size, kvh.size * G, D))
+    dk = np.zeros((resp_keys.size, kvh.size, D))
+    dv = np.zeros((resp_keys.size, kvh.size, Dv))
     keys = np.arange(kv_begin, kv_end)
     resp_col = resp_keys - kv_begin                     # columns of the range holding resp keys
-    for g in range(Hkv):
+    for gi, g in enumerate(kvh):
         K = _kv(k_pool, page_table, page_size, keys, g)
         V = _kv(v_pool, page_table, page_size, keys, g, Dv)
         for h in range(g * G, (g + 1) * G):
+            hl = gi * G + h - g * G                     # this head's slot in dq
             for r0 in range(0, need_rows.size, row_block):
                 rr = need_rows[r0:r0 + row_block]
                 idx = np.array([row_at[int(r)] for r in rr])
@@ -245,10 +250,10 @@ def attn_bwd(q, k_pool, v_pool, page_table, d_out, *, page_size, prefix_len, q_p
                 sel = np.isin(rr, dq_rows)
                 if sel.any():
                     pos = np.searchsorted(dq_rows, rr[sel])
-                    dq[pos, h] += scale * (dS[sel] @ K)
+                    dq[pos, hl] += scale * (dS[sel] @ K)
                 if resp_keys.size:
-                    dk[:, g] += scale * (dS[:, resp_col].T @ Q)
-                    dv[:, g] += P[:, resp_col].T @ dO
+                    dk[:, gi] += scale * (dS[:, resp_col].T @ Q)
+                    dv[:, gi] += P[:, resp_col].T @ dO
     return dq, dk, dv
 
 

@@ -56,10 +56,11 @@ def _chunks(rows, n):
     return [c for c in np.array_split(rows, max(1, min(n, rows.size))) if c.size]
 
 
-def dense_fwd(h, *, page_size, q_pos0, scale, rows, prefix_len, piece=65536):
-    """Full-row out and lse of ``rows`` (over every visible key): each chunk of
-    rows is the merge of per-range oracle results over prefix ranges of
-    ``piece`` keys and the response range."""
+def dense_fwd(h, *, page_size, q_pos0, scale, rows, prefix_len, piece=65536, heads=None):
+    """Full-row out and lse of ``rows`` (over every visible key; of the query
+    heads ``heads`` only, when given): each chunk of rows is the merge of
+    per-range oracle results over prefix ranges of ``piece`` keys and the
+    response range."""
     rows = np.asarray(rows)
     kv_len = q_pos0 + h["q"].shape[0]
     ranges = key_ranges(0, prefix_len, piece) + [(prefix_len, kv_len)]
@@ -70,7 +71,8 @@ def dense_fwd(h, *, page_size, q_pos0, scale, rows, prefix_len, piece=65536):
     def one(task):
         r, c = task
         return O.attn_fwd(h["q"], h["k_pool"], h["v_pool"], h["page_table"], page_size=page_size,
-                          q_pos0=q_pos0, scale=scale, kv_begin=r[0], kv_end=r[1], rows=c)
+                          q_pos0=q_pos0, scale=scale, kv_begin=r[0], kv_end=r[1], rows=c,
+                          heads=heads)
 
     tasks = [(r, c) for c in chunks for r in ranges]
     parts = _pool_map(one, tasks)
@@ -86,21 +88,22 @@ def dense_fwd(h, *, page_size, q_pos0, scale, rows, prefix_len, piece=65536):
 
 
 def dense_bwd(h, *, page_size, q_pos0, scale, prefix_len, rows, resp_keys, out, lse,
-              piece=65536, resp_piece=512):
+              piece=65536, resp_piece=512, kv_heads=None):
     """dq of ``rows`` over every visible key and the dK/dV of the response keys
     ``resp_keys``, given the oracle's full-row ``out``/``lse`` arrays ([R, Hq, Dv]
     / [Hq, R], filled at least for the rows that need them).  The keys are cut
     into prefix ranges of ``piece`` and response ranges of ``resp_piece``: dq is
     the sum of the ranges' contributions, and a response key's dK/dV come from
     the one range holding it (they depend only on that key's column of P and
-    dS)."""
+    dS).  ``kv_heads`` restricts dq to those KV heads' query heads and dK/dV to
+    those KV heads (oracle.attn_bwd)."""
     rows = np.asarray(rows)
     resp_keys = np.unique(np.asarray(resp_keys, np.int64))
     kv_len = q_pos0 + h["q"].shape[0]
     ranges = key_ranges(0, prefix_len, piece) + key_ranges(prefix_len, kv_len, resp_piece)
     t0 = time.perf_counter()
     kw = dict(page_size=page_size, prefix_len=prefix_len, q_pos0=q_pos0, scale=scale, out=out,
-              lse=lse, rows=rows)
+              lse=lse, rows=rows, kv_heads=kv_heads)
 
     def one(r):
         keys = resp_keys[(resp_keys >= r[0]) & (resp_keys < r[1])]

@@ -278,6 +278,12 @@ def pin_sampled_rows(O):
     _close(dq2, dq[rows], 1e-12, "row subset dq")
     _close(dk2, dk[[9, 11]], 1e-12, "key subset dk")
     _close(dv2, dv[[9, 11]], 1e-12, "key subset dv")
+    # one KV head: its group's query heads in dq, its own dK/dV, all unchanged
+    dq3, dk3, dv3 = O.attn_bwd(t.q, t.k_pool, t.v_pool, t.page_table, t.d_out, rows=rows,
+                               resp_keys=keys, kv_heads=[1], **t.bkw())
+    _close(dq3, dq[rows][:, [2, 3]], 1e-12, "KV head subset dq")
+    _close(dk3, dk[[9, 11]][:, [1]], 1e-12, "KV head subset dk")
+    _close(dv3, dv[[9, 11]][:, [1]], 1e-12, "KV head subset dv")
 
 
 # ---------------------------------------------------------------- sparse latent replay

@@ -34,10 +34,12 @@ def logical_store(cfg, store, resp, pages):
     return kp, vp, table
 
 
-def run_members(cfg, members, rows=None, keys=None, dq_rows=None):
+def run_members(cfg, members, rows=None, keys=None, dq_rows=None, kv_head=None):
     """Replay each member blockwise and compare out/lse on ``rows``, dq on
     ``dq_rows`` (default: ``rows``) and dK/dV on ``keys`` (default: all response
-    keys) with the oracle of the unblocked response over the same logical store."""
+    keys) with the oracle of the unblocked response over the same logical store.
+    ``kv_head`` restricts every comparison to that KV head and its group's query
+    heads (the oracle then computes only those)."""
     import torch
     store = inputs.prefix_store(cfg)
     prefix = ResidentPrefix(cfg, store)
@@ -49,7 +51,7 @@ def run_members(cfg, members, rows=None, keys=None, dq_rows=None):
     t_snap = prefix.table[:cfg.n_prefix_pages].clone()
     R = cfg.resp_len
     r_sel = np.arange(R) if rows is None else np.unique(rows)
-    dq_sel = r_sel if dq_rows is None else np.unique(dq_rows)
+    dq_sel = r_sel if dq_rows is None else np.unique(np.asarray(dq_rows, np.int64))
     key_off = np.arange(R) if keys is None else np.unique(keys)
     for m in members:
         resp = inputs.response_inputs(cfg, m)
@@ -63,21 +65,28 @@ def run_members(cfg, members, rows=None, keys=None, dq_rows=None):
         hh = dict(q=resp["q"], k_pool=kp, v_pool=vp, page_table=table, d_out=resp["d_out"])
         kw = dict(page_size=cfg.page_size, q_pos0=cfg.prefix_len, scale=cfg.scale,
                   prefix_len=cfg.prefix_len)
+        G = cfg.n_q_heads // cfg.n_kv_heads
+        heads = (np.arange(cfg.n_q_heads) if kv_head is None
+                 else np.arange(kv_head * G, (kv_head + 1) * G))
+        kvh = np.arange(cfg.n_kv_heads) if kv_head is None else np.array([kv_head])
         need = np.union1d(np.union1d(r_sel, dq_sel), np.arange(int(key_off.min()), R))
-        o_n, l_n = _par.dense_fwd(hh, rows=need, **kw)
+        o_n, l_n = _par.dense_fwd(hh, rows=need, heads=None if kv_head is None else heads, **kw)
         at = np.searchsorted(need, r_sel)
         out = np.concatenate([host(keep[b][0]) for b in range(cfg.blocks)])
         lse = np.concatenate([host(keep[b][1]) for b in range(cfg.blocks)], axis=1)
-        assert rel_l2(out[r_sel], o_n[at]) <= 5e-3, f"member {m} out"
-        assert lse_err(lse[:, r_sel], l_n[:, at]) <= 1e-3, f"member {m} lse"
+        assert rel_l2(out[r_sel][:, heads], o_n[at]) <= 5e-3, f"member {m} out"
+        assert lse_err(lse[heads][:, r_sel], l_n[:, at]) <= 1e-3, f"member {m} lse"
         o_full = np.zeros((R, cfg.n_q_heads, cfg.head_dim_v))
         l_full = np.zeros((cfg.n_q_heads, R))
-        o_full[need], l_full[:, need] = o_n, l_n
-        dq_ref, dk_ref, dv_ref = _par.dense_bwd(hh, rows=dq_sel, resp_keys=cfg.prefix_len + key_off,
-                                                out=o_full, lse=l_full, **kw)
-        assert rel_l2(host(dq)[dq_sel], dq_ref) <= 1e-2, f"member {m} dq"
-        assert rel_l2(host(dk)[key_off], dk_ref) <= 1e-2, f"member {m} dk"
-        assert rel_l2(host(dv)[key_off], dv_ref) <= 1e-2, f"member {m} dv"
+        o_full[np.ix_(need, heads)] = o_n
+        l_full[np.ix_(heads, need)] = l_n
+        dq_ref, dk_ref, dv_ref = _par.dense_bwd(
+            hh, rows=dq_sel, resp_keys=cfg.prefix_len + key_off, out=o_full, lse=l_full,
+            kv_heads=None if kv_head is None else kvh, **kw)
+        if dq_sel.size:
+            assert rel_l2(host(dq)[dq_sel][:, heads], dq_ref) <= 1e-2, f"member {m} dq"
+        assert rel_l2(host(dk)[key_off][:, kvh], dk_ref) <= 1e-2, f"member {m} dk"
+        assert rel_l2(host(dv)[key_off][:, kvh], dv_ref) <= 1e-2, f"member {m} dv"
         # the prefix pages and the table's prefix entries were never written
         assert torch.equal(prefix.k_pool.index_select(0, pp), k_snap), "prefix K pages written"
         assert torch.equal(prefix.v_pool.index_select(0, pp), v_snap), "prefix V pages written"
@@ -110,13 +119,23 @@ def test_c4_full_size_sampled():
     """c4 at full size: in each of the four 2,048-token blocks, both sides of
     the block edge and of the dq (16-token) and forward (32-token) workgroup
     boundaries at its start, middle and end (48 rows), and the last two response
-    keys.  A key that a second block also reaches is seen by at least 2,049
-    rows, whose fp64 forward over the 4.46M prefix (~150 TFLOP) is beyond the
-    oracle's reach here; the block geometry case above covers that
-    accumulation."""
+    keys (test_c4_key_across_blocks covers a key reached by two blocks)."""
     cfg = configs.C4
     R = cfg.resp_len
     rows = sorted({b + o for b in range(0, R, cfg.rows_per_call)
                    for o in (0, 1, 15, 16, 31, 32, 1023, 1024, 2015, 2016, 2046, 2047)
                    if b + o < R})
     run_members(cfg, members=[0], rows=rows, keys=[R - 2, R - 1])
+
+
+@pytest.mark.timeout(1200)
+def test_c4_key_across_blocks():
+    """c4 at full size: response key 6,143, the last of block 2, is seen by its
+    own row and by every row of block 3, so its dK/dV add up the contributions
+    of two block launches.  Checked on KV head 0 and its group's eight query
+    heads (the oracle's forward over the 4.46M prefix for those 2,049 rows is
+    ~75 TFLOP of fp64): those rows' out and lse and the key's dK/dV."""
+    cfg = configs.C4
+    key = 3 * cfg.rows_per_call - 1
+    run_members(cfg, members=[0], rows=[key, key + 1, cfg.resp_len - 1], keys=[key], dq_rows=[],
+                kv_head=0)

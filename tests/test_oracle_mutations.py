@@ -28,9 +28,9 @@ MUTATIONS = [
     ("table_ignored", "pages = page_table[positions // page_size].astype(np.int64)",
      "pages = (positions // page_size).astype(np.int64)"),
     ("bwd_no_delta", "dS = P * (dP - delta[h, idx][:, None])", "dS = P * dP"),
-    ("bwd_dq_no_scale", "dq[pos, h] += scale * (dS[sel] @ K)", "dq[pos, h] += (dS[sel] @ K)"),
-    ("bwd_dv_uses_dS", "dv[:, g] += P[:, resp_col].T @ dO", "dv[:, g] += dS[:, resp_col].T @ dO"),
-    ("bwd_dk_uses_P", "dk[:, g] += scale * (dS[:, resp_col].T @ Q)", "dk[:, g] += scale * (P[:, resp_col].T @ Q)"),
+    ("bwd_dq_no_scale", "dq[pos, hl] += scale * (dS[sel] @ K)", "dq[pos, hl] += (dS[sel] @ K)"),
+    ("bwd_dv_uses_dS", "dv[:, gi] += P[:, resp_col].T @ dO", "dv[:, gi] += dS[:, resp_col].T @ dO"),
+    ("bwd_dk_uses_P", "dk[:, gi] += scale * (dS[:, resp_col].T @ Q)", "dk[:, gi] += scale * (P[:, resp_col].T @ Q)"),
     ("bwd_resp_shift", "resp_col = resp_keys - kv_begin", "resp_col = resp_keys - kv_begin - 1"),
     ("bwd_P_no_lse", "np.exp(np.where(visible, s, 0.0) - ell[:, None])", "np.exp(np.where(visible, s, 0.0))"),
     ("bwd_delta_dO_sq", 'delta = np.einsum("rhd,rhd->hr", dO_all[need_rows], o_n)',

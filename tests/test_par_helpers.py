@@ -23,6 +23,13 @@ def test_dense_ranges_compose_to_the_unsplit_oracle():
                                         prefix_len=t.P, rows=rows, resp_keys=keys, **kw)
     for a, b in ((dq, dq_ref), (dk, dk_ref), (dv, dv_ref)):
         assert rel_l2(a, b) < 1e-12
+    # one KV head's group: out/lse of its query heads, its dq heads and dK/dV
+    o1, l1 = _par.dense_fwd(h, rows=rows, prefix_len=t.P, piece=64, heads=[2, 3], **kw)
+    assert rel_l2(o1, o_ref[:, [2, 3]]) < 1e-12 and np.max(np.abs(l1 - l_ref[[2, 3]])) < 1e-12
+    dq1, dk1, dv1 = _par.dense_bwd(h, prefix_len=t.P, rows=rows, resp_keys=keys, out=o_all,
+                                   lse=l_all, piece=64, resp_piece=4, kv_heads=[1], **kw)
+    for a, b in ((dq1, dq_ref[:, [2, 3]]), (dk1, dk_ref[:, [1]]), (dv1, dv_ref[:, [1]])):
+        assert rel_l2(a, b) < 1e-12
 
 
 def test_sparse_row_chunks_compose():
