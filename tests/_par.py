@@ -97,23 +97,38 @@ def dense_bwd(h, *, page_size, q_pos0, scale, prefix_len, rows, resp_keys, out, 
     the one range holding it (they depend only on that key's column of P and
     dS).  ``kv_heads`` restricts dq to those KV heads' query heads and dK/dV to
     those KV heads (oracle.attn_bwd)."""
-    rows = np.asarray(rows)
+    rows = np.asarray(rows, np.int64)
+    assert np.all(np.diff(rows) > 0), "rows must be sorted and distinct"
     resp_keys = np.unique(np.asarray(resp_keys, np.int64))
     kv_len = q_pos0 + h["q"].shape[0]
-    ranges = key_ranges(0, prefix_len, piece) + key_ranges(prefix_len, kv_len, resp_piece)
+    pre = key_ranges(0, prefix_len, piece)
+    resp = key_ranges(prefix_len, kv_len, resp_piece)
+    # prefix ranges hold no response key, so their dq rows split into chunks
+    # (dq adds up over a row partition); a response range keeps every row,
+    # since a key's dK/dV needs each row that sees it
+    chunks = _chunks(rows, max(1, (4 * workers()) // max(1, len(pre))))
+    tasks = [(r, c, False) for r in pre for c in chunks] + [(r, rows, True) for r in resp]
     t0 = time.perf_counter()
     kw = dict(page_size=page_size, prefix_len=prefix_len, q_pos0=q_pos0, scale=scale, out=out,
-              lse=lse, rows=rows, kv_heads=kv_heads)
+              lse=lse, kv_heads=kv_heads)
 
-    def one(r):
-        keys = resp_keys[(resp_keys >= r[0]) & (resp_keys < r[1])]
+    def one(task):
+        r, c, has_resp = task
+        keys = resp_keys[(resp_keys >= r[0]) & (resp_keys < r[1])] if has_resp else resp_keys[:0]
         return O.attn_bwd(h["q"], h["k_pool"], h["v_pool"], h["page_table"], h["d_out"],
-                          kv_begin=r[0], kv_end=r[1], resp_keys=keys, **kw)
+                          kv_begin=r[0], kv_end=r[1], resp_keys=keys, rows=c, **kw)
 
-    parts = _pool_map(one, ranges)
-    dq = sum(p[0] for p in parts)
-    dk = np.concatenate([p[1] for p in parts])
-    dv = np.concatenate([p[2] for p in parts])
+    parts = _pool_map(one, tasks)
+    resp_parts = [p for p, t in zip(parts, tasks) if t[2]]
+    dq = sum(p[0] for p in resp_parts) if resp_parts else None
+    for p, (r, c, has_resp) in zip(parts, tasks):
+        if has_resp:
+            continue
+        if dq is None:
+            dq = np.zeros((rows.size,) + p[0].shape[1:])
+        dq[np.searchsorted(rows, c)] += p[0]
+    dk = np.concatenate([p[1] for p in resp_parts])
+    dv = np.concatenate([p[2] for p in resp_parts])
     print(f"[oracle] dense bwd: {rows.size} dq rows, {resp_keys.size} response keys, "
           f"{time.perf_counter() - t0:.1f} s", flush=True)
     return dq, dk, dv
