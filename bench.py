@@ -31,6 +31,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 METRIC = "replay attention TFLOP/s (fwd+bwd) & % of bf16 MFMA peak at 2M-position prefix"
+METRIC_FWD = "replay attention forward TFLOP/s & % of bf16 MFMA peak (one 262,144-position shard)"
 PEAK_BF16_TFLOPS = 2500.0
 PEAK_HBM_GBS = 8000.0
 
@@ -519,8 +520,13 @@ def main():
         print(json.dumps({"page_streaming": ps, "read_ceiling": ceil,
                           "gpu": torch.cuda.get_device_name(0)}), flush=True)
         return
-    step = ReplayStep(cfg, dev, backward=True, stream=stream)
+    # a forward-only configuration (c2: one shard of c3, out and lse) times the
+    # forward and the merge alone
+    with_bwd = cfg.backward
+    step = ReplayStep(cfg, dev, backward=with_bwd, stream=stream)
     fwd_fl, bwd_fl = flops(cfg)
+    if not with_bwd:
+        bwd_fl = 0
 
     for w in range(args.warmup):
         step.step()
@@ -528,7 +534,7 @@ def main():
         log(f"warmup {w + 1}/{args.warmup} done")
 
     E = lambda: torch.cuda.Event(enable_timing=True)  # noqa: E731
-    n_r = len(step.shards)
+    n_r = len(step.shards) if with_bwd else 0
     ev = [[E() for _ in range(3 + n_r + 1)] for _ in range(args.steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
@@ -555,13 +561,17 @@ def main():
 
     avg = lambda xs: sum(xs) / len(xs)  # noqa: E731
     fwd_avg = avg(fwd_ms)
-    pre_ranges = [r for r, (b, e) in enumerate(step.shards) if e <= cfg.prefix_len]
-    dq_launch_ms = avg([bwd_ms[s][r] for s in range(args.steps) for r in pre_ranges])
-    shard_len = step.shards[pre_ranges[0]][1] - step.shards[pre_ranges[0]][0]
-    dq_launch_fl = 6 * cfg.n_q_heads * cfg.head_dim * cfg.resp_len * shard_len
     fwd_tf = fwd_fl / (fwd_avg * 1e-3) / 1e12
-    dq_tf = dq_launch_fl / (dq_launch_ms * 1e-3) / 1e12
-    fwd_total, dq_total = fwd_avg, dq_launch_ms * len(pre_ranges)
+    if with_bwd:
+        pre_ranges = [r for r, (b, e) in enumerate(step.shards) if e <= cfg.prefix_len]
+        dq_launch_ms = avg([bwd_ms[s][r] for s in range(args.steps) for r in pre_ranges])
+        shard_len = step.shards[pre_ranges[0]][1] - step.shards[pre_ranges[0]][0]
+        dq_launch_fl = 6 * cfg.n_q_heads * cfg.head_dim * cfg.resp_len * shard_len
+        dq_tf = dq_launch_fl / (dq_launch_ms * 1e-3) / 1e12
+        fwd_total, dq_total = fwd_avg, dq_launch_ms * len(pre_ranges)
+    else:
+        dq_tf = None
+        fwd_total, dq_total = fwd_avg, 0.0
     if fwd_total >= dq_total:
         roof = {"kernel": "fwd_bf16_d256_kernel (all splits: one launch, one per shard "
                           "when cyclic)",
@@ -584,7 +594,7 @@ def main():
     merge_bytes = (ns * R * Hq * (Dv + 1) * 4 + nsh * R * Hq * (Dv + 1) * 4 * 2
                    + R * Hq * (Dv * 2 + 4))
     result = {
-        "metric": METRIC,
+        "metric": METRIC if with_bwd else METRIC_FWD,
         "value": round(value, 2),
         "unit": "TFLOP/s",
         "n_gpus": 1,
@@ -601,7 +611,7 @@ def main():
                                f"{cfg.page_size}-position pages (seeded permutation), "
                                f"{cfg.n_shards} {cfg.ownership} shards x "
                                f"{cfg.splits_per_shard} splits + response split, response "
-                               f"{cfg.resp_len} causal, fwd+bwd"
+                               f"{cfg.resp_len} causal, " + ("fwd+bwd" if with_bwd else "fwd only")
                                + (", bf16-numerator merge" if cfg.bf16_numerator else ""),
                    "ownership": cfg.ownership, "bf16_numerator": cfg.bf16_numerator,
                    "prefix_len": cfg.prefix_len, "resp_len": cfg.resp_len,
@@ -616,12 +626,13 @@ def main():
                       "step_events_median": round(sorted(step_ms)[len(step_ms) // 2], 3),
                       "step_events_min": round(min(step_ms), 3)},
         "fwd_tflops": round(fwd_tf, 2),
-        "dq_tflops": round(dq_tf, 2),
+        "dq_tflops": None if dq_tf is None else round(dq_tf, 2),
         "merge_gbs": round(merge_bytes / (avg(merge_ms) * 1e-3) / 1e9, 1),
         "flop_per_step": {"fwd": fwd_fl, "bwd": bwd_fl},
         "gpu": torch.cuda.get_device_name(0),
     }
-    result["useful_tflops"] = round(useful_flops(cfg) / (ms_per_step * 1e-3) / 1e12, 2)
+    useful = useful_flops(cfg) if with_bwd else fwd_fl
+    result["useful_tflops"] = round(useful / (ms_per_step * 1e-3) / 1e12, 2)
     if not args.skip_extras:
         log("bf16-numerator merge cost")
         result["bf16_numerator"] = bf16_numerator_cost(step, stream)

@@ -144,10 +144,11 @@ C1 = ReplayConfig(name="c1_tiny_f32", seed=1, dtype="f32", n_q_heads=2, n_kv_hea
                   head_dim=64, head_dim_v=64, page_size=64, prefix_len=4096, resp_len=128,
                   n_shards=2, splits_per_shard=1, table="identity")
 
-# Forward-only single shard: one eighth of a 2M prefix.
+# Forward-only single shard: one eighth of a 2M prefix, cut into 4 splits like
+# each shard of c3 (a single split leaves half the workgroups short).
 C2 = ReplayConfig(name="c2_fwd_262k", seed=2, dtype="bf16", n_q_heads=16, n_kv_heads=2,
                   head_dim=256, head_dim_v=256, page_size=256, prefix_len=262_144,
-                  resp_len=4096, n_shards=1, splits_per_shard=1, table="perm", backward=False)
+                  resp_len=4096, n_shards=1, splits_per_shard=4, table="perm", backward=False)
 
 # Full 2M replay, 8 contiguous shards x 4-way split-KV + the response split.
 C3 = ReplayConfig(name="c3_replay_2m", seed=3, dtype="bf16", n_q_heads=16, n_kv_heads=2,

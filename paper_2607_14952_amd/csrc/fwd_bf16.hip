@@ -237,7 +237,7 @@ __global__ __launch_bounds__(64 * kWaves, 1) void fwd_bf16_d256_kernel(FwdArgs a
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave-uniform (scalar)
   const int l32 = lane & 31, hh = lane >> 5;
 #if LS_XCD_MAP
-  const WorkItem wi = xcd_work_item();
+  const WorkItem wi = xcd_work_item_tail_spread();   // z: split, the last one the response's
 #else
   const WorkItem wi{(int)blockIdx.x, (int)blockIdx.y, (int)blockIdx.z};
 #endif

@@ -361,6 +361,40 @@ __device__ __forceinline__ WorkItem xcd_work_item() {
   return it;
 }
 
+// The same dealing for a grid whose last z slice holds short workgroups (the
+// forward's response split: causal keys only, a few percent of a prefix
+// split's work).  Contiguous ranges would put that whole slice on the last
+// XCD, which then idles for a fifth of the launch while the others run only
+// long workgroups.  Here the other slices (the long items) are dealt in
+// contiguous x-fastest ranges as above, and each XCD's remaining slots take
+// the next items of the last slice, after its long ones.  XCD k has
+// q + (k < r) slots (q, r = n / 8, n % 8) and q_l + (k < r_l) long items
+// (q_l, r_l for the long count), so the difference, its short count, is never
+// negative and the short counts add up to the slice.  With one slice it is
+// xcd_work_item.
+__device__ __forceinline__ WorkItem xcd_work_item_tail_spread() {
+  const uint32_t nx = gridDim.x, ny = gridDim.y, nz = gridDim.z;
+  const uint32_t n = nx * ny * nz, nl = nx * ny * (nz - 1);
+  const uint32_t id = blockIdx.x + nx * (blockIdx.y + ny * blockIdx.z);
+  const uint32_t xcd = id % 8, slot = id / 8;
+  const uint32_t q = n / 8, r = n % 8, ql = nl / 8, rl = nl % 8;
+  const uint32_t long_begin = xcd * ql + min(xcd, rl);
+  const uint32_t long_cnt = ql + (xcd < rl ? 1u : 0u);
+  WorkItem it;
+  if (slot < long_cnt) {
+    const uint32_t w = long_begin + slot;
+    it.x = (int)(w % nx);
+    it.y = (int)((w / nx) % ny);
+    it.z = (int)(w / (nx * ny));
+  } else {
+    const uint32_t w = (xcd * q + min(xcd, r)) - long_begin + (slot - long_cnt);
+    it.x = (int)(w % nx);
+    it.y = (int)(w / nx);
+    it.z = (int)(nz - 1);
+  }
+  return it;
+}
+
 // Wait for this wave's direct loads (vmcnt = 0).
 __device__ __forceinline__ void wait_fetch() { __builtin_amdgcn_s_waitcnt(0x0F70); }
 
