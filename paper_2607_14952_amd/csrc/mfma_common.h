@@ -372,13 +372,12 @@ __device__ __forceinline__ WorkItem xcd_work_item() {
 // (q_l, r_l for the long count), so the difference, its short count, is never
 // negative and the short counts add up to the slice.  With one slice it is
 // xcd_work_item.
-__device__ __forceinline__ WorkItem xcd_work_item_tail_spread() {
-  const uint32_t nx = gridDim.x, ny = gridDim.y, nz = gridDim.z;
+__host__ __device__ inline WorkItem tail_spread_item(uint32_t id, uint32_t nx, uint32_t ny,
+                                                     uint32_t nz) {
   const uint32_t n = nx * ny * nz, nl = nx * ny * (nz - 1);
-  const uint32_t id = blockIdx.x + nx * (blockIdx.y + ny * blockIdx.z);
   const uint32_t xcd = id % 8, slot = id / 8;
   const uint32_t q = n / 8, r = n % 8, ql = nl / 8, rl = nl % 8;
-  const uint32_t long_begin = xcd * ql + min(xcd, rl);
+  const uint32_t long_begin = xcd * ql + (xcd < rl ? xcd : rl);
   const uint32_t long_cnt = ql + (xcd < rl ? 1u : 0u);
   WorkItem it;
   if (slot < long_cnt) {
@@ -387,12 +386,16 @@ __device__ __forceinline__ WorkItem xcd_work_item_tail_spread() {
     it.y = (int)((w / nx) % ny);
     it.z = (int)(w / (nx * ny));
   } else {
-    const uint32_t w = (xcd * q + min(xcd, r)) - long_begin + (slot - long_cnt);
+    const uint32_t w = (xcd * q + (xcd < r ? xcd : r)) - long_begin + (slot - long_cnt);
     it.x = (int)(w % nx);
     it.y = (int)(w / nx);
     it.z = (int)(nz - 1);
   }
   return it;
+}
+__device__ __forceinline__ WorkItem xcd_work_item_tail_spread() {
+  const uint32_t nx = gridDim.x, ny = gridDim.y, nz = gridDim.z;
+  return tail_spread_item(blockIdx.x + nx * (blockIdx.y + ny * blockIdx.z), nx, ny, nz);
 }
 
 // Wait for this wave's direct loads (vmcnt = 0).

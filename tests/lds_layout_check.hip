@@ -256,10 +256,43 @@ static void fused() {
   }
 }
 
+// The forward's XCD dealing (tail_spread_item): every work item exactly once,
+// and the last z slice spread so that no XCD holds two more of its items than
+// another.
+static void xcd_dealing() {
+  using namespace ls;
+  for (uint32_t nx = 1; nx <= 40; ++nx)
+    for (uint32_t ny = 1; ny <= 3; ++ny)
+      for (uint32_t nz = 1; nz <= 12; ++nz) {
+        const uint32_t n = nx * ny * nz;
+        std::vector<int> seen(n, 0);
+        int tail[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+        for (uint32_t id = 0; id < n; ++id) {
+          const WorkItem it = tail_spread_item(id, nx, ny, nz);
+          CHECK(it.x >= 0 && it.x < (int)nx && it.y >= 0 && it.y < (int)ny && it.z >= 0 &&
+                    it.z < (int)nz,
+                "xcd dealing %u x %u x %u: item out of range", nx, ny, nz);
+          if (it.x < 0 || it.x >= (int)nx || it.y < 0 || it.y >= (int)ny || it.z < 0 || it.z >= (int)nz)
+            continue;
+          ++seen[it.x + nx * (it.y + ny * it.z)];
+          if (it.z == (int)nz - 1) ++tail[id % 8];
+        }
+        for (uint32_t w = 0; w < n; ++w)
+          CHECK(seen[w] == 1, "xcd dealing %u x %u x %u: item %u dealt %d times", nx, ny, nz, w, seen[w]);
+        int lo = tail[0], hi = tail[0];
+        for (int k = 1; k < 8; ++k) {
+          lo = tail[k] < lo ? tail[k] : lo;
+          hi = tail[k] > hi ? tail[k] : hi;
+        }
+        if (nz > 1) CHECK(hi - lo <= 2, "xcd dealing %u x %u x %u: last slice %d..%d per XCD", nx, ny, nz, lo, hi);
+      }
+}
+
 int main() {
   dense();
   sparse();
   fused();
+  xcd_dealing();
   if (failures) {
     printf("%d failures\n", failures);
     return 1;
