@@ -134,8 +134,9 @@ struct DsPieces {
 // previous tile (s_prev / dp_prev) computed between their MFMAs, then that
 // tile's dq product (K in `prev_k`).  Ring slots are distinct (see the forward
 // kernel).  `pe` holds the page-table entry of t0_next on entry and that of
-// t0_after on return; on return s_prev / dp_prev hold this tile's masked
-// scores and dP.
+// t0_after on return.  This tile's masked scores and dP go to s_out / dp_out,
+// a register set other than s_prev / dp_prev: the loop alternates two sets, so
+// no step copies its results into place.
 template <bool kPerKey, bool kFirst>
 __device__ __forceinline__ void dq_step(const BwdArgs& a, char* __restrict__ next,
                                         const char* __restrict__ cur,
@@ -145,12 +146,12 @@ __device__ __forceinline__ void dq_step(const BwdArgs& a, char* __restrict__ nex
                                         int64_t t0, int64_t kb, int64_t k_all, int64_t my_lim,
                                         const bf16x8* qreg, const bf16x8* dreg,
                                         const TileOffsets& to, int hh, float lse2, float delta,
-                                        f32x16* acc, f32x16& s_prev, f32x16& dp_prev) {
+                                        f32x16* acc, f32x16& s_prev, f32x16& dp_prev,
+                                        f32x16& s, f32x16& dp) {
   DsPieces ds{s_prev, dp_prev, a.scale_log2, lse2, delta};
   auto valu = [&](int k) {
     if (!kFirst) ds.piece(k);
   };
-  f32x16 s, dp;
   constexpr bool kEarly = LS_DQ_KT_EARLY && !kFirst;
   bf16x8 kt0[kKTAhead];
   auto late = [&](int i) {
@@ -173,8 +174,6 @@ __device__ __forceinline__ void dq_step(const BwdArgs& a, char* __restrict__ nex
   }
   if (t0 < kb || t0 + kQBN > k_all) mask_keys(s, t0, kb, my_lim, hh);
   if (!kFirst) dq_update(prev_k, ds.d0, ds.d1, acc, to, kEarly ? kt0 : nullptr);
-  s_prev = s;
-  dp_prev = dp;
 }
 
 template <bool kPerKey>
@@ -262,34 +261,49 @@ __global__ __launch_bounds__(256, 1) void bwd_dq_bf16_d256_kernel(BwdArgs a) {
   f32x16 acc[8];
 #pragma unroll
   for (int i = 0; i < 8; ++i) acc[i] = zero16();
-  f32x16 s_prev, dp_prev;   // masked scores and dP of the previous tile
+  // masked scores and dP of a tile, in two sets that the steps alternate
+  f32x16 s_a, dp_a, s_b, dp_b;
 
   // (a full wait here: the Q/dO loads may have been scheduled after the stages)
   wait_fetch();
   tile_barrier();
   // Iteration t fetches tile t + kQAhead and, before its barrier, waits for
-  // the loads of tile t + 1.
+  // the loads of tile t + 1.  Tile t's scores land in set a for even t and in
+  // set b for odd t.
   {
     dq_step<kPerKey, true>(a, smem + kQAhead * kQStage, smem, smem, kf, vf, pl, pe, tile0(kQAhead),
                            tile0(kQAhead + 1), k_hi, k_lo, kb, k_all, my_lim, qreg, dreg, to, hh,
-                           lse2, delta, acc, s_prev, dp_prev);
+                           lse2, delta, acc, s_b, dp_b, s_a, dp_a);
     wait_vmcnt<(kQAhead - 1) * 8>();
     tile_barrier();
   }
-  for (int t = 1; t < n_tiles; ++t) {
+  auto step = [&](int t, f32x16& s_in, f32x16& dp_in, f32x16& s_out, f32x16& dp_out) {
     const int64_t t0 = k_lo + (int64_t)t * kQBN;
     dq_step<kPerKey, false>(a, smem + ((t + kQAhead) % kQSlots) * kQStage,
                             smem + (t % kQSlots) * kQStage, smem + ((t - 1) % kQSlots) * kQStage,
                             kf, vf, pl, pe, tile0(t + kQAhead), tile0(t + kQAhead + 1), k_hi, t0,
-                            kb, k_all, my_lim, qreg, dreg, to, hh, lse2, delta, acc, s_prev,
-                            dp_prev);
+                            kb, k_all, my_lim, qreg, dreg, to, hh, lse2, delta, acc, s_in, dp_in,
+                            s_out, dp_out);
     wait_vmcnt<(kQAhead - 1) * 8>();
     tile_barrier();
+  };
+  int t = 1;
+  for (; t + 1 < n_tiles; t += 2) {
+    step(t, s_a, dp_a, s_b, dp_b);
+    step(t + 1, s_b, dp_b, s_a, dp_a);
   }
-  {
-    DsPieces ds{s_prev, dp_prev, a.scale_log2, lse2, delta};
+  // the last tile's dS and dq product (its scores are in set b when a tile
+  // was left over for one more step, else in set a)
+  auto finish = [&](f32x16& s_last, f32x16& dp_last) {
+    DsPieces ds{s_last, dp_last, a.scale_log2, lse2, delta};
     ds.all();
     dq_update(smem + ((n_tiles - 1) % kQSlots) * kQStage, ds.d0, ds.d1, acc, to);
+  };
+  if (t < n_tiles) {
+    step(t, s_a, dp_a, s_b, dp_b);
+    finish(s_b, dp_b);
+  } else {
+    finish(s_a, dp_a);
   }
   wait_fetch();   // no direct load is left in flight when the waves end
 
