@@ -173,8 +173,10 @@ __device__ __forceinline__ void rescale_pv(const char* Vs, const OnlineSoftmax& 
 // One step: the scores of the tile in `ks_cur` while the tile at t0_next
 // streams into `next`.  With kOverlap (one wave per SIMD) the online softmax of
 // the previous tile's scores (`s_prev`) is spread between the score MFMAs, then
-// the previous tile's rescale and PV product follow (V in `vs_prev`), and on
-// return s_prev holds this tile's masked scores.  Without it (two waves per
+// the previous tile's rescale and PV product follow (V in `vs_prev`), and this
+// tile's masked scores go to `s_out`, a register set other than s_prev (the
+// loop alternates two sets, so no step copies its scores into place).
+// Without it (two waves per
 // SIMD, whose MFMAs and VALU work interleave) the step finishes its own tile:
 // softmax, rescale and PV with the V half of `ks_cur`.  The LDS regions are
 // distinct ring slots; the restrict qualifiers tell the compiler so, which
@@ -190,6 +192,7 @@ __device__ __forceinline__ void step(const FwdArgs& a, char* __restrict__ next,
                                      int64_t k_lo, int64_t kb, int64_t k_all, int lim_rel,
                                      const bf16x8* qreg,
                                      const TileBase& to, int hh, f32x16* oacc, f32x16& s_prev,
+                                     f32x16& s_out,
                                      float& m_run, float& l_run) {
   OnlineSoftmax sm{s_prev, a.scale_log2, m_run, l_run};
   auto valu = [&](int k) {
@@ -214,7 +217,7 @@ __device__ __forceinline__ void step(const FwdArgs& a, char* __restrict__ next,
   if (t0 < kb || t0 + kBN > k_all) mask_keys_rel(s, (int)(t0 - k_lo), (int)(kb - k_lo), lim_rel, hh);
   if (kOverlap) {
     if (!kFirst) rescale_pv<kAheadV>(vs_prev, sm, l_run, oacc, to);
-    s_prev = s;
+    s_out = s;
   } else {
     OnlineSoftmax cur{s, a.scale_log2, m_run, l_run};
     cur.all();
@@ -317,7 +320,9 @@ __global__ __launch_bounds__(64 * kWaves, 1) void fwd_bf16_d256_kernel(FwdArgs a
 #pragma unroll
   for (int i = 0; i < 8; ++i) oacc[i] = zero16();
   float m_run = -INFINITY, l_run = 0.f;
-  f32x16 s_prev;   // masked scores of the previous tile, before its softmax
+  // masked scores of a tile before its softmax (one wave per SIMD, pipelined):
+  // two sets that the steps alternate
+  f32x16 s_a, s_b;
 
   // (a full wait here: the Q loads may have been scheduled after the stages)
   wait_fetch();
@@ -325,30 +330,43 @@ __global__ __launch_bounds__(64 * kWaves, 1) void fwd_bf16_d256_kernel(FwdArgs a
 
   // Iteration t fetches tile t + kAhead and, before its barrier, waits for
   // the loads of tile t + 1.  With kOverlap tile 0 is peeled (no previous
-  // tile) and the last tile's softmax and PV follow the loop.
-  int t = 0;
-  if (kOverlap) {
-    step<kPerKey, true, kOverlap, kInstr, kAK, kAV>(
-        a, smem + kAhead * kStage, smem, smem + kTileBytes, kf, vf, pl, pe, tile0(kAhead),
-        tile0(kAhead + 1), k_hi, k_lo, k_lo, kb, k_all, lim_rel, qreg, to, hh, oacc, s_prev, m_run, l_run);
-    wait_vmcnt<(kAhead - 1) * 2 * kInstr>();
-    tile_barrier();
-    t = 1;
-  }
-  for (; t < n_tiles; ++t) {
+  // tile), tile t's scores land in set a for even t and in set b for odd t,
+  // and the last tile's softmax and PV follow the loop.
+  auto st = [&](int t, f32x16& s_in, f32x16& s_out) {
     const int64_t t0 = k_lo + (int64_t)t * kBN;
     step<kPerKey, false, kOverlap, kInstr, kAK, kAV>(
         a, smem + ((t + kAhead) % kSlots) * kStage, smem + (t % kSlots) * kStage,
         smem + ((t + kSlots - 1) % kSlots) * kStage + kTileBytes, kf, vf, pl, pe, tile0(t + kAhead),
-        tile0(t + kAhead + 1), k_hi, t0, k_lo, kb, k_all, lim_rel, qreg, to, hh, oacc, s_prev, m_run,
-        l_run);
+        tile0(t + kAhead + 1), k_hi, t0, k_lo, kb, k_all, lim_rel, qreg, to, hh, oacc, s_in, s_out,
+        m_run, l_run);
     wait_vmcnt<(kAhead - 1) * 2 * kInstr>();
     tile_barrier();
-  }
-  if (kOverlap) {
-    OnlineSoftmax sm{s_prev, a.scale_log2, m_run, l_run};
-    sm.all();
-    rescale_pv<kAV>(smem + ((n_tiles - 1) % kSlots) * kStage + kTileBytes, sm, l_run, oacc, to);
+  };
+  if constexpr (kOverlap) {
+    step<kPerKey, true, kOverlap, kInstr, kAK, kAV>(
+        a, smem + kAhead * kStage, smem, smem + kTileBytes, kf, vf, pl, pe, tile0(kAhead),
+        tile0(kAhead + 1), k_hi, k_lo, k_lo, kb, k_all, lim_rel, qreg, to, hh, oacc, s_b, s_a,
+        m_run, l_run);
+    wait_vmcnt<(kAhead - 1) * 2 * kInstr>();
+    tile_barrier();
+    int t = 1;
+    for (; t + 1 < n_tiles; t += 2) {
+      st(t, s_a, s_b);
+      st(t + 1, s_b, s_a);
+    }
+    auto finish = [&](f32x16& s_last) {
+      OnlineSoftmax sm{s_last, a.scale_log2, m_run, l_run};
+      sm.all();
+      rescale_pv<kAV>(smem + ((n_tiles - 1) % kSlots) * kStage + kTileBytes, sm, l_run, oacc, to);
+    };
+    if (t < n_tiles) {
+      st(t, s_a, s_b);
+      finish(s_b);
+    } else {
+      finish(s_a);
+    }
+  } else {
+    for (int t = 0; t < n_tiles; ++t) st(t, s_a, s_b);   // (each step finishes its own tile)
   }
   wait_fetch();   // no direct load is left in flight when the waves end
 
