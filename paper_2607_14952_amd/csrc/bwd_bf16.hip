@@ -164,7 +164,9 @@ __device__ __forceinline__ void dq_step(const BwdArgs& a, char* __restrict__ nex
   } else {
     const int64_t prow_next = pl.row(pe, t0_next);
     pe = pl.load(t0_after);
-    __builtin_amdgcn_sched_barrier(0);   // the entry load stays ahead of the stage's loads
+    // the entry load stays ahead of the stage's loads; scalar and vector ALU
+    // work may cross, so the next stage's descriptors are built among the MFMAs
+    __builtin_amdgcn_sched_barrier(0x0006);
     const __amdgpu_buffer_rsrc_t rk = kf.page_rsrc(prow_next), rv = vf.page_rsrc(prow_next);
     const int nv = (int)min(k_hi - t0_next, (int64_t)kQBN);
     scores_dp(cur, cur + kTileBytes, qreg, dreg, to, s, dp, [&](int i) {
