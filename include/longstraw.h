@@ -49,8 +49,9 @@
  * with fp32 products and sums, so results differ in rounding order only);
  * dtype LS_BF16 with head_dim = head_dim_v = 256, n_q_heads /
  * n_kv_heads dividing 32, n_q * n_q_heads * 512 < 2^31 bytes of queries,
- * fewer than 2^29 logical pages and q_pos0 + n_q < 2^31 (the kernels use
- * 32-bit buffer offsets and 32-bit key positions within a split).
+ * pool rows n_kv_heads * 512 < 2^24 bytes, fewer than 2^29 logical pages and
+ * q_pos0 + n_q < 2^31 (the kernels use 32-bit buffer offsets, 24-bit row
+ * offsets within a tile and 32-bit key positions within a split).
  */
 #ifndef LONGSTRAW_H
 #define LONGSTRAW_H

@@ -129,6 +129,9 @@ ls_status check_supported(const ls_attn_params* p) {
     return fail(LS_ERR_UNSUPPORTED, "bf16 path: n_q * n_q_heads * head_dim * 2 must be < 2^31");
   if (p->n_logical_pages >= (int64_t(1) << 29))
     return fail(LS_ERR_UNSUPPORTED, "bf16 path: n_logical_pages must be < 2^29");
+  // a tile's row offsets are 24-bit products of the row size
+  if ((int64_t)p->n_kv_heads * p->head_dim * 2 >= (int64_t(1) << 24))
+    return fail(LS_ERR_UNSUPPORTED, "bf16 path: n_kv_heads * head_dim * 2 must be < 2^24 bytes");
   // key positions relative to a split's first tile are held in 32 bits
   if (kv_len_of(p) >= (int64_t(1) << 31))
     return fail(LS_ERR_UNSUPPORTED, "bf16 path: q_pos0 + n_q must be < 2^31");

@@ -170,8 +170,8 @@ __device__ __forceinline__ void dq_step(const BwdArgs& a, char* __restrict__ nex
     const __amdgpu_buffer_rsrc_t rk = kf.page_rsrc(prow_next), rv = vf.page_rsrc(prow_next);
     const int nv = (int)min(k_hi - t0_next, (int64_t)kQBN);
     scores_dp(cur, cur + kTileBytes, qreg, dreg, to, s, dp, [&](int i) {
-      if (i < 4) kf.issue_one(next, rk, i, nv);
-      else vf.issue_one(next + kTileBytes, rv, i - 4, nv);
+      if (i < 4) kf.issue_one_u24(next, rk, i, nv);
+      else vf.issue_one_u24(next + kTileBytes, rv, i - 4, nv);
     }, valu, late);
   }
   if (t0 < kb || t0 + kQBN > k_all) mask_keys(s, t0, kb, my_lim, hh);

@@ -91,6 +91,7 @@ def fwd(p, splits=((0, 4096), (4096, 4160)), out=FAKE * 256, lse=FAKE * 320):
     (dict(softmax_scale=-1.0), -1),
     (dict(expected_epoch=2), -5),                # stale pool
     (dict(n_q_heads=16 * 3, n_kv_heads=1), -2),  # bf16 group 48 does not divide 32
+    (dict(n_q=1, n_q_heads=32768, n_kv_heads=32768), -2),  # pool rows of 2^24 bytes
 ])
 def test_forward_rejects(kw, status):
     assert fwd(good_params(**kw)) == status
