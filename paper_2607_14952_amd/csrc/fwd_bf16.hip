@@ -206,12 +206,21 @@ __device__ __forceinline__ void step(const FwdArgs& a, char* __restrict__ next,
   } else {
     const int64_t prow_next = pl.row(pe, t0_next);
     pe = pl.load(t0_after);
-    __builtin_amdgcn_sched_barrier(0);   // the entry load stays ahead of the stage's loads
+    // the entry load stays ahead of the stage's loads; with one wave per SIMD
+    // (kSpread) ALU work may cross, so the next stage's descriptors are built
+    // among the MFMAs (as in dq)
+    if (kOverlap) __builtin_amdgcn_sched_barrier(0x0006);
+    else __builtin_amdgcn_sched_barrier(0);
     const __amdgpu_buffer_rsrc_t rk = kf.page_rsrc(prow_next), rv = vf.page_rsrc(prow_next);
     const int nv = (int)min(k_hi - t0_next, (int64_t)kBN);
     s = scores<2 * kInstr, kAheadK>(ks_cur, qreg, to, [&](int i) {
-      if (i < kInstr) kf.issue_one(next, rk, i, nv);
-      else vf.issue_one(next + kTileBytes, rv, i - kInstr, nv);
+      if (kOverlap) {
+        if (i < kInstr) kf.issue_one_u24(next, rk, i, nv);
+        else vf.issue_one_u24(next + kTileBytes, rv, i - kInstr, nv);
+      } else {
+        if (i < kInstr) kf.issue_one(next, rk, i, nv);
+        else vf.issue_one(next + kTileBytes, rv, i - kInstr, nv);
+      }
     }, valu);
   }
   if (t0 < kb || t0 + kBN > k_all) mask_keys_rel(s, (int)(t0 - k_lo), (int)(kb - k_lo), lim_rel, hh);
