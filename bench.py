@@ -70,16 +70,23 @@ def useful_flops(cfg):
     return 4 * Hq * D * (pre + resp) + Hq * D * (4 * pre + 8 * resp)
 
 
-def time_ms(fn, reps, stream=None):
+def time_ms(fn, reps, stream=None, lead=0):
     """GPU time per call (ms): `reps` calls enqueued back to back between two
     HIP events, after one untimed call.  Only the first call's host-side
     argument marshalling can fall inside the interval (the GPU is idle when the
     start event is recorded); later calls are enqueued while earlier ones run,
-    so for calls whose GPU time exceeds their host time the rest is hidden."""
+    so for calls whose GPU time exceeds their host time the rest is hidden.
+    With `lead` > 0, that many untimed calls run back to back right before the
+    start event, with no synchronisation in between: the timed calls then run
+    at the clock the chip settles at under that load (after idle it first runs
+    fast, then lowers its clock for a few milliseconds and recovers part of
+    it), and their marshalling overlaps the lead calls."""
     import torch
     fn()
     torch.cuda.synchronize()
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    for _ in range(lead):
+        fn()
     e0.record(stream)
     for _ in range(reps):
         fn()
@@ -102,7 +109,7 @@ def measured_ceilings():
     src = torch.empty(1 << 30, dtype=torch.float32, device="cuda")
     src.fill_(1.0)
     dst = torch.empty_like(src)
-    ms = time_ms(lambda: dst.copy_(src), 5)
+    ms = time_ms(lambda: dst.copy_(src), 10, lead=10)
     copy = 2 * src.numel() * 4 / (ms * 1e-3) / 1e9
     del dst
     torch.cuda.empty_cache()
@@ -120,7 +127,7 @@ def hbm_read_ceiling(buf=None):
         buf = torch.empty(1 << 30, dtype=torch.float32, device="cuda")
         buf.fill_(1.0)
     out = torch.zeros(1, dtype=torch.int32, device=buf.device)
-    ms = time_ms(lambda: B.hbm_read_probe(buf, out), 10)
+    ms = time_ms(lambda: B.hbm_read_probe(buf, out), 20, lead=20)
     nbytes = buf.numel() * buf.element_size()
     return {"hbm_read_gbs": round(nbytes / (ms * 1e-3) / 1e9, 1), "read_bytes": nbytes}
 
@@ -198,7 +205,8 @@ def page_streaming(cfg, dev, rows=16, n_splits=256):
     splits = list(zip(bounds[:-1], bounds[1:]))
     op, lp = B.prefix_attn_fwd(q, kv, splits, prefix_len=P, q_pos0=P, scale=cfg.scale)
     ms = time_ms(lambda: B.prefix_attn_fwd(q, kv, splits, prefix_len=P, q_pos0=P,
-                                           scale=cfg.scale, out_part=op, lse_part=lp), 20)
+                                           scale=cfg.scale, out_part=op, lse_part=lp), 40,
+                 lead=20)
     nbytes = 2 * P * cfg.n_kv_heads * cfg.head_dim * 2
     gbs = nbytes / (ms * 1e-3) / 1e9
     return {"rows": rows, "splits": n_splits, "bytes": nbytes, "ms": round(ms, 3),
