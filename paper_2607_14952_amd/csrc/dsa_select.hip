@@ -13,9 +13,9 @@
 // per wave and reused by all of its heads.  Per tile a wave forms S^T = K Q^T
 // for each of its heads (8 MFMAs 32x32x16 over the 128-wide head, two heads'
 // chains interleaved), folds w ReLU(S) into a partial sum, and writes the
-// partial tile to LDS; after the tile barrier each wave adds the waves'
-// partials for its share of the 32 token rows and stores those rows of I
-// (fp32).  Partials are double buffered, so one barrier per tile serves the
+// partial tile to LDS.  During the next tile's first MFMAs each wave adds the
+// waves' partials for its share of the 32 token rows and stores those rows of
+// I (fp32).  Partials are double buffered, so one barrier per tile serves the
 // ring and the exchange.
 //
 // Top-k kernel.  One workgroup per row.  A histogram of the top 12 bits of an
@@ -29,6 +29,8 @@
 // first), writing positions in ascending order: each of the 8 waves owns a
 // contiguous segment of the row, and per-segment counts set its output base.
 // The row is read three times (five when the fallback runs).
+#include <type_traits>
+
 #include "ls_internal.h"
 #include "mfma_common.h"
 
@@ -45,6 +47,7 @@ constexpr int kISlots = kIAhead + 2;
 #endif
 constexpr int kIChunk = LS_DSA_CHUNK;     // positions per workgroup
 constexpr int kXWave = 32 * 32 * 4;       // one wave's partial tile (fp32)
+typedef __attribute__((__vector_size__(2 * sizeof(float)))) float f32x2;
 constexpr int kIKAhead = 3;               // key operand reads in flight
 
 // Key tile layout: 16-byte chunk c of row r sits at chunk c ^ (r & 15), so the
@@ -75,6 +78,16 @@ struct IKeyFetch {
                                              0);
   }
 };
+
+// ReLU as a signed-integer max of the bits: a float with its sign bit set
+// (negative, or -0) is a negative integer, so the max with 0 gives +0 for it
+// and leaves every other value as it is.  One full-rate instruction, where
+// fmaxf(x, 0) on an MFMA result also spends one quieting a possible signalling
+// NaN.  (A NaN with its sign bit clear passes through, as it does in a ReLU
+// that propagates NaN.)
+__device__ __forceinline__ float relu_bits(float x) {
+  return __int_as_float(max(__float_as_int(x), 0));
+}
 
 // Partial tile of one wave: [token][position] fp32, 16-byte chunk (position/4)
 // stored at chunk ^ (token & 7).
@@ -145,6 +158,43 @@ __global__ __launch_bounds__(64 * kWaves, 1) void dsa_score_kernel(DsaArgs a) {
   wait_fetch();   // (a full wait: the query loads may have been scheduled after the stages)
   tile_barrier();
 
+  // The exchange of a tile's partials: wave w sums tokens kTPW w .. + kTPW - 1
+  // over the waves' partial tiles, kXE positions per lane (all 64 lanes), and
+  // stores them.  Tile t's exchange runs inside step t + 1, among its first
+  // MFMAs (the partials are double buffered, and every wave reads them before
+  // the barrier that ends step t + 1), so no step waits on it between barriers.
+  constexpr int kXE = kTPW / 2;                 // 2 (8 waves) or 4 (4 waves)
+  using XVec = std::conditional_t<kXE == 2, f32x2, f32x4>;
+  const int x_rt = kTPW * w + lane / (32 / kXE);
+  const int x_p = kXE * (lane % (32 / kXE));    // first position of the lane in the tile
+  const int x_off = xoff(x_rt, x_p >> 2) + 4 * (x_p & 3);
+  XVec xr[kWaves];
+  auto x_read = [&](int tt) {
+    const char* xb = xbase + (tt & 1) * kWaves * kXWave;
+#pragma unroll
+    for (int v = 0; v < kWaves; ++v) xr[v] = *reinterpret_cast<const XVec*>(xb + v * kXWave + x_off);
+  };
+  auto x_store = [&](int tt) {
+    const int otok = tok0 + x_rt;
+    if (otok < a.n_q) {
+      XVec sum = xr[0];
+#pragma unroll
+      for (int v = 1; v < kWaves; ++v) sum += xr[v];
+      const int64_t pos = c0 + (int64_t)tt * 32 + x_p;
+      float* dst = a.scores + (int64_t)otok * a.ld + (pos - a.pos_begin);
+      if (pos + kXE <= c1) {
+        *reinterpret_cast<XVec*>(dst) = sum;
+      } else {
+#pragma unroll
+        for (int e = 0; e < kXE; ++e)
+          if (pos + e < c1) dst[e] = sum[e];
+      }
+    }
+  };
+  // the stage's direct loads follow the previous tile's store, so they stay
+  // the newest vector-memory operations for the wait that ends the step
+  constexpr int kXStoreAt = 4;
+
   for (int t = 0; t < n_tiles; ++t) {
     const char* __restrict__ kt = smem + (t % kISlots) * kITile;
     char* __restrict__ next = smem + ((t + kIAhead) % kISlots) * kITile;
@@ -161,6 +211,7 @@ __global__ __launch_bounds__(64 * kWaves, 1) void dsa_score_kernel(DsaArgs a) {
 #pragma unroll
     for (int i = 0; i < kIKAhead; ++i)
       kreg[i] = *reinterpret_cast<const bf16x8*>(kt + ikey_off(l32, 2 * i + hh));
+    if (t > 0) x_read(t - 1);
     mfma_fence();
     f32x16 part = zero16();
 #pragma unroll
@@ -176,14 +227,15 @@ __global__ __launch_bounds__(64 * kWaves, 1) void dsa_score_kernel(DsaArgs a) {
               *reinterpret_cast<const bf16x8*>(kt + ikey_off(l32, 2 * (ks + kIKAhead) + hh));
         s0 = mfma32(kreg[ks], qreg[j][ks], s0);
         s1 = mfma32(kreg[ks], qreg[j + 1][ks], s1);
-        if (j == 0 && ks < kFI) f.issue(next, rn, ks, nvn);
+        if (j == 0 && ks == kXStoreAt && t > 0) x_store(t - 1);
+        if (j == 0 && ks >= kXStoreAt && ks < kXStoreAt + kFI) f.issue(next, rn, ks - kXStoreAt, nvn);
         mfma_fence();
       }
       __builtin_amdgcn_s_setprio(0);
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        part[r] = fmaf(wv[j], fmaxf(s0[r], 0.f), part[r]);
-        part[r] = fmaf(wv[j + 1], fmaxf(s1[r], 0.f), part[r]);
+        part[r] = fmaf(wv[j], relu_bits(s0[r]), part[r]);
+        part[r] = fmaf(wv[j + 1], relu_bits(s1[r]), part[r]);
       }
     }
     // partial tile: lane (token l32, half hh) holds positions 8q + 4hh + {0..3}
@@ -195,27 +247,10 @@ __global__ __launch_bounds__(64 * kWaves, 1) void dsa_score_kernel(DsaArgs a) {
     wait_newest_stage<kFI>();
     __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0): the partial tile is in LDS
     tile_barrier();
-    // wave w: tokens kTPW w + lane/8, positions 4 (lane%8) .. +3 of this tile
-    if ((lane >> 3) < kTPW) {
-      const int rt = kTPW * w + (lane >> 3), c = lane & 7;
-      const char* xb = xbase + (t & 1) * kWaves * kXWave;
-      f32x4 sum = *reinterpret_cast<const f32x4*>(xb + xoff(rt, c));
-#pragma unroll
-      for (int v = 1; v < kWaves; ++v)
-        sum += *reinterpret_cast<const f32x4*>(xb + v * kXWave + xoff(rt, c));
-      const int otok = tok0 + rt;
-      const int64_t pos = c0 + (int64_t)t * 32 + 4 * c;
-      if (otok < a.n_q) {
-        float* dst = a.scores + (int64_t)otok * a.ld + (pos - a.pos_begin);
-        if (pos + 4 <= c1) {
-          *reinterpret_cast<f32x4*>(dst) = sum;
-        } else {
-#pragma unroll
-          for (int e = 0; e < 4; ++e)
-            if (pos + e < c1) dst[e] = sum[e];
-        }
-      }
-    }
+  }
+  if (n_tiles > 0) {
+    x_read(n_tiles - 1);
+    x_store(n_tiles - 1);
   }
   wait_fetch();   // no direct load is left in flight when the waves end
 }
