@@ -45,15 +45,39 @@ constexpr int kKTAhead = 4;   // transposed K operands in flight (two reads each
 #ifndef LS_DQ_KT_EARLY
 #define LS_DQ_KT_EARLY 1
 #endif
+// Every step waits for its LDS reads before its barrier: the stage issued
+// right after a barrier may refill the slot whose transposed K the step before
+// it read.  The last kDqDefer MFMAs of a tile's dq product then run at the
+// start of the next step, right after its first K/V operand reads are issued,
+// so that the matrix core covers those reads' latency; they carry their K^T
+// operands and the tile's dS across the barrier.
+#ifndef LS_DQ_DEFER
+#define LS_DQ_DEFER 2
+#endif
+constexpr int kDqDefer = LS_DQ_DEFER;
+static_assert(kDqDefer >= 0 && kDqDefer <= 16 - kKTAhead, "deferred dq MFMAs");
+struct DqTail {
+  bf16x8 kt[kDqDefer > 0 ? kDqDefer : 1];
+  bf16x8 d0, d1;
+  // dq^T += the deferred products (operand 16 - kDqDefer + j)
+  __device__ __forceinline__ void run(f32x16* acc) const {
+#pragma unroll
+    for (int j = 0; j < kDqDefer; ++j) {
+      const int i = 16 - kDqDefer + j;
+      acc[i >> 1] = mfma32(kt[j], (i & 1) ? d1 : d0, acc[i >> 1]);
+    }
+  }
+};
 
 // S^T = K Q^T and dP^T = V dO^T for one 32-key tile.  After step ks < 8,
 // load(ks) issues one instruction of the next stage's direct loads; after the
 // last kKTAhead steps, late(i) issues the i-th operand read of the dq product
 // that follows.
-template <typename Load, typename Valu, typename Late>
+template <typename Load, typename Valu, typename Late, typename Pre>
 __device__ __forceinline__ void scores_dp(const char* Ks, const char* Vs, const bf16x8* qreg,
                                           const bf16x8* dreg, const TileOffsets& o, f32x16& s,
-                                          f32x16& dp, Load&& load, Valu&& valu, Late&& late) {
+                                          f32x16& dp, Load&& load, Valu&& valu, Late&& late,
+                                          Pre&& pre) {
   bf16x8 kr[16], vr[16];
 #pragma unroll
   for (int i = 0; i < kSDAhead; ++i) {
@@ -61,6 +85,7 @@ __device__ __forceinline__ void scores_dp(const char* Ks, const char* Vs, const 
     vr[i] = tile_row16(Vs, o, i);
   }
   mfma_fence();
+  pre();
   s = zero16();
   dp = zero16();
 #pragma unroll
@@ -85,18 +110,26 @@ __device__ __forceinline__ bf16x8 dq_kt(const char* Ks, const TileOffsets& o, in
   return (i & 1) ? tile_col8(Ks, o, i >> 1, 16, 24) : tile_col8(Ks, o, i >> 1, 0, 8);
 }
 // kt0: the first kKTAhead operands, already read (or null: read them here).
+// kDefer > 0: the last kDefer MFMAs are left to `tail` (operands and dS).
+template <int kDefer = 0>
 __device__ __forceinline__ void dq_update(const char* Ks, const bf16x8& d0, const bf16x8& d1,
                                           f32x16* acc, const TileOffsets& o,
-                                          const bf16x8* kt0 = nullptr) {
+                                          const bf16x8* kt0 = nullptr, DqTail* tail = nullptr) {
   bf16x8 kt[16];
   auto read = [&](int i) { return dq_kt(Ks, o, i); };
 #pragma unroll
   for (int i = 0; i < kKTAhead; ++i) kt[i] = kt0 ? kt0[i] : read(i);
 #pragma unroll
-  for (int i = 0; i < 16; ++i) {
+  for (int i = 0; i < 16 - kDefer; ++i) {
     if (i + kKTAhead < 16) kt[i + kKTAhead] = read(i + kKTAhead);
     acc[i >> 1] = mfma32(kt[i], (i & 1) ? d1 : d0, acc[i >> 1]);
     mfma_fence();
+  }
+  if constexpr (kDefer > 0) {
+#pragma unroll
+    for (int j = 0; j < kDefer; ++j) tail->kt[j] = kt[16 - kDefer + j];
+    tail->d0 = d0;
+    tail->d1 = d1;
   }
 }
 
@@ -147,8 +180,15 @@ __device__ __forceinline__ void dq_step(const BwdArgs& a, char* __restrict__ nex
                                         const bf16x8* qreg, const bf16x8* dreg,
                                         const TileOffsets& to, int hh, float lse2, float delta,
                                         f32x16* acc, f32x16& s_prev, f32x16& dp_prev,
-                                        f32x16& s, f32x16& dp) {
+                                        f32x16& s, f32x16& dp, DqTail& tail) {
   DsPieces ds{s_prev, dp_prev, a.scale_log2, lse2, delta};
+  // the deferred end of the dq product two tiles back (zeros before the
+  // first); the per-key variant (short pages) has no registers to carry it
+  auto pre = [&]() {
+    if constexpr (!kPerKey) {
+      if (!kFirst) tail.run(acc);
+    }
+  };
   auto valu = [&](int k) {
     if (!kFirst) ds.piece(k);
   };
@@ -160,7 +200,7 @@ __device__ __forceinline__ void dq_step(const BwdArgs& a, char* __restrict__ nex
   if (kPerKey) {
     kf.issue_rows(next, a.page_table, a.log2_page, t0_next, k_hi);
     vf.issue_rows(next + kTileBytes, a.page_table, a.log2_page, t0_next, k_hi);
-    scores_dp(cur, cur + kTileBytes, qreg, dreg, to, s, dp, [](int) {}, valu, late);
+    scores_dp(cur, cur + kTileBytes, qreg, dreg, to, s, dp, [](int) {}, valu, late, pre);
   } else {
     const int64_t prow_next = pl.row(pe, t0_next);
     pe = pl.load(t0_after);
@@ -172,10 +212,12 @@ __device__ __forceinline__ void dq_step(const BwdArgs& a, char* __restrict__ nex
     scores_dp(cur, cur + kTileBytes, qreg, dreg, to, s, dp, [&](int i) {
       if (i < 4) kf.issue_one_u24(next, rk, i, nv);
       else vf.issue_one_u24(next + kTileBytes, rv, i - 4, nv);
-    }, valu, late);
+    }, valu, late, pre);
   }
   if (t0 < kb || t0 + kQBN > k_all) mask_keys(s, t0, kb, my_lim, hh);
-  if (!kFirst) dq_update(prev_k, ds.d0, ds.d1, acc, to, kEarly ? kt0 : nullptr);
+  if (!kFirst)
+    dq_update<kPerKey ? 0 : kDqDefer>(prev_k, ds.d0, ds.d1, acc, to, kEarly ? kt0 : nullptr,
+                                      &tail);
 }
 
 template <bool kPerKey>
@@ -265,6 +307,18 @@ __global__ __launch_bounds__(256, 1) void bwd_dq_bf16_d256_kernel(BwdArgs a) {
   for (int i = 0; i < 8; ++i) acc[i] = zero16();
   // masked scores and dP of a tile, in two sets that the steps alternate
   f32x16 s_a, dp_a, s_b, dp_b;
+  DqTail tail;
+#pragma unroll
+  for (int j = 0; j < (kDqDefer > 0 ? kDqDefer : 1); ++j)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) tail.kt[j][e] = (__bf16)0.f;
+  tail.d0 = tail.kt[0];
+  tail.d1 = tail.kt[0];
+  auto end_step = [&]() {
+    wait_vmcnt<(kQAhead - 1) * 8>();
+    __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0): the step's LDS reads have landed
+    tile_barrier();
+  };
 
   // (a full wait here: the Q/dO loads may have been scheduled after the stages)
   wait_fetch();
@@ -275,9 +329,8 @@ __global__ __launch_bounds__(256, 1) void bwd_dq_bf16_d256_kernel(BwdArgs a) {
   {
     dq_step<kPerKey, true>(a, smem + kQAhead * kQStage, smem, smem, kf, vf, pl, pe, tile0(kQAhead),
                            tile0(kQAhead + 1), k_hi, k_lo, kb, k_all, my_lim, qreg, dreg, to, hh,
-                           lse2, delta, acc, s_b, dp_b, s_a, dp_a);
-    wait_vmcnt<(kQAhead - 1) * 8>();
-    tile_barrier();
+                           lse2, delta, acc, s_b, dp_b, s_a, dp_a, tail);
+    end_step();
   }
   auto step = [&](int t, f32x16& s_in, f32x16& dp_in, f32x16& s_out, f32x16& dp_out) {
     const int64_t t0 = k_lo + (int64_t)t * kQBN;
@@ -285,9 +338,8 @@ __global__ __launch_bounds__(256, 1) void bwd_dq_bf16_d256_kernel(BwdArgs a) {
                             smem + (t % kQSlots) * kQStage, smem + ((t - 1) % kQSlots) * kQStage,
                             kf, vf, pl, pe, tile0(t + kQAhead), tile0(t + kQAhead + 1), k_hi, t0,
                             kb, k_all, my_lim, qreg, dreg, to, hh, lse2, delta, acc, s_in, dp_in,
-                            s_out, dp_out);
-    wait_vmcnt<(kQAhead - 1) * 8>();
-    tile_barrier();
+                            s_out, dp_out, tail);
+    end_step();
   };
   int t = 1;
   for (; t + 1 < n_tiles; t += 2) {
@@ -297,6 +349,7 @@ __global__ __launch_bounds__(256, 1) void bwd_dq_bf16_d256_kernel(BwdArgs a) {
   // the last tile's dS and dq product (its scores are in set b when a tile
   // was left over for one more step, else in set a)
   auto finish = [&](f32x16& s_last, f32x16& dp_last) {
+    if constexpr (!kPerKey) tail.run(acc);
     DsPieces ds{s_last, dp_last, a.scale_log2, lse2, delta};
     ds.all();
     dq_update(smem + ((n_tiles - 1) % kQSlots) * kQStage, ds.d0, ds.d1, acc, to);
@@ -470,7 +523,7 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_bf16_d256_kernel(BwdArgs a, i
     __builtin_amdgcn_sched_barrier(0);
     f32x16 s, dp;
     scores_dp(cur, cur + kTileBytes, kreg, vreg, to, s, dp,
-              [&](int i) { fetch(next, row_next, i); }, [](int) {}, [](int) {});
+              [&](int i) { fetch(next, row_next, i); }, [](int) {}, [](int) {}, [] {});
     const float* st = reinterpret_cast<const float*>(cur + 2 * kTileBytes + kRStat * w);
     const int row0 = row_lo + 32 * t;
     const bool edge = a.q_pos0 + (row0 >> lg) < jw + 31 || row0 + 32 > rows_total;

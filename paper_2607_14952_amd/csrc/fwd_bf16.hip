@@ -53,13 +53,14 @@ template <int kWaves> constexpr int kVAhead = kWaves == 4 ? 4 : 2;
 // MFMA ks < kLoads, load(ks) issues one instruction of the next stage's direct
 // loads, so their issue overlaps the MFMA chain; valu(ks) issues a piece of
 // the previous tile's softmax.
-template <int kLoads, int kAheadK, typename Load, typename Valu>
+template <int kLoads, int kAheadK, typename Load, typename Valu, typename Pre>
 __device__ __forceinline__ f32x16 scores(const char* Ks, const bf16x8* qreg, const TileBase& o,
-                                         Load&& load, Valu&& valu) {
+                                         Load&& load, Valu&& valu, Pre&& pre) {
   bf16x8 kreg[16];
 #pragma unroll
   for (int i = 0; i < kAheadK; ++i) kreg[i] = tile_row16(Ks, o, i);
   mfma_fence();
+  pre();
   f32x16 s = zero16();
 #pragma unroll
   for (int ks = 0; ks < 16; ++ks) {
@@ -75,9 +76,31 @@ __device__ __forceinline__ f32x16 scores(const char* Ks, const bf16x8* qreg, con
 // O^T += V^T P^T for one 32-key tile.  P's register block kk holds keys
 // 16kk + {4h..4h+3, 8+4h..8+4h+3}; the V^T operand reads the same keys.
 // Operand i is dims block i/2, key half i%2.
-template <int kAheadV>
+// Every step waits for its LDS reads before its barrier: the stage issued
+// right after a barrier may refill the slot the step before it read.  The
+// last kFwdDefer MFMAs of a PV product then run at the start of the next step,
+// right after its first K operand reads are issued, so that the matrix core
+// covers those reads' latency; they carry their V operands and P across the
+// barrier.
+#ifndef LS_FWD_DEFER
+#define LS_FWD_DEFER 2
+#endif
+constexpr int kFwdDefer = LS_FWD_DEFER;
+struct PvTail {
+  bf16x8 v[kFwdDefer > 0 ? kFwdDefer : 1];
+  bf16x8 p0, p1;
+  __device__ __forceinline__ void run(f32x16* oacc) const {
+#pragma unroll
+    for (int j = 0; j < kFwdDefer; ++j) {
+      const int i = 16 - kFwdDefer + j;
+      oacc[i >> 1] = mfma32(v[j], (i & 1) ? p1 : p0, oacc[i >> 1]);
+    }
+  }
+};
+
+template <int kAheadV, int kDefer = 0>
 __device__ __forceinline__ void pv(const char* Vs, const bf16x8& p0, const bf16x8& p1,
-                                   f32x16* oacc, const TileBase& o) {
+                                   f32x16* oacc, const TileBase& o, PvTail* tail = nullptr) {
   bf16x8 vreg[16];
   auto read = [&](int i) {
     return (i & 1) ? tile_col8(Vs, o, i >> 1, 16, 24) : tile_col8(Vs, o, i >> 1, 0, 8);
@@ -85,10 +108,16 @@ __device__ __forceinline__ void pv(const char* Vs, const bf16x8& p0, const bf16x
 #pragma unroll
   for (int i = 0; i < kAheadV; ++i) vreg[i] = read(i);
 #pragma unroll
-  for (int i = 0; i < 16; ++i) {
+  for (int i = 0; i < 16 - kDefer; ++i) {
     if (i + kAheadV < 16) vreg[i + kAheadV] = read(i + kAheadV);
     oacc[i >> 1] = mfma32(vreg[i], (i & 1) ? p1 : p0, oacc[i >> 1]);
     mfma_fence();
+  }
+  if constexpr (kDefer > 0) {
+#pragma unroll
+    for (int j = 0; j < kDefer; ++j) tail->v[j] = vreg[16 - kDefer + j];
+    tail->p0 = p0;
+    tail->p1 = p1;
   }
 }
 
@@ -158,16 +187,16 @@ struct OnlineSoftmax {
 };
 
 // O^T = alpha * O^T + V^T P^T for the tile whose softmax `sm` holds.
-template <int kAheadV>
+template <int kAheadV, int kDefer = 0>
 __device__ __forceinline__ void rescale_pv(const char* Vs, const OnlineSoftmax& sm,
                                            const float& l_run, f32x16* oacc,
-                                           const TileBase& to) {
+                                           const TileBase& to, PvTail* tail = nullptr) {
   // (l_run < 0 never holds; it keeps the exponentials ahead of this branch)
   if (__any(sm.alpha != 1.f || l_run < 0.f)) {
 #pragma unroll
     for (int i = 0; i < 8; ++i) oacc[i] *= sm.alpha;
   }
-  pv<kAheadV>(Vs, sm.p0, sm.p1, oacc, to);
+  pv<kAheadV, kDefer>(Vs, sm.p0, sm.p1, oacc, to, tail);
 }
 
 // One step: the scores of the tile in `ks_cur` while the tile at t0_next
@@ -193,16 +222,22 @@ __device__ __forceinline__ void step(const FwdArgs& a, char* __restrict__ next,
                                      const bf16x8* qreg,
                                      const TileBase& to, int hh, f32x16* oacc, f32x16& s_prev,
                                      f32x16& s_out,
-                                     float& m_run, float& l_run) {
+                                     float& m_run, float& l_run, PvTail& tail) {
   OnlineSoftmax sm{s_prev, a.scale_log2, m_run, l_run};
   auto valu = [&](int k) {
     if (kOverlap && !kFirst) sm.piece(k);
+  };
+  // the deferred end of the last PV product (zeros before the first); it runs
+  // before this step's rescale
+  constexpr int kDefer = kFwdDefer;
+  auto pre = [&]() {
+    if constexpr (kDefer > 0) tail.run(oacc);
   };
   f32x16 s;
   if (kPerKey) {
     kf.issue_rows(next, a.page_table, a.log2_page, t0_next, k_hi);
     vf.issue_rows(next + kTileBytes, a.page_table, a.log2_page, t0_next, k_hi);
-    s = scores<0, kAheadK>(ks_cur, qreg, to, [](int) {}, valu);
+    s = scores<0, kAheadK>(ks_cur, qreg, to, [](int) {}, valu, pre);
   } else {
     const int64_t prow_next = pl.row(pe, t0_next);
     pe = pl.load(t0_after);
@@ -221,16 +256,16 @@ __device__ __forceinline__ void step(const FwdArgs& a, char* __restrict__ next,
         if (i < kInstr) kf.issue_one(next, rk, i, nv);
         else vf.issue_one(next + kTileBytes, rv, i - kInstr, nv);
       }
-    }, valu);
+    }, valu, pre);
   }
   if (t0 < kb || t0 + kBN > k_all) mask_keys_rel(s, (int)(t0 - k_lo), (int)(kb - k_lo), lim_rel, hh);
   if (kOverlap) {
-    if (!kFirst) rescale_pv<kAheadV>(vs_prev, sm, l_run, oacc, to);
+    if (!kFirst) rescale_pv<kAheadV, kDefer>(vs_prev, sm, l_run, oacc, to, &tail);
     s_out = s;
   } else {
     OnlineSoftmax cur{s, a.scale_log2, m_run, l_run};
     cur.all();
-    rescale_pv<kAheadV>(ks_cur + kTileBytes, cur, l_run, oacc, to);
+    rescale_pv<kAheadV, kDefer>(ks_cur + kTileBytes, cur, l_run, oacc, to, &tail);
   }
 }
 
@@ -332,6 +367,13 @@ __global__ __launch_bounds__(64 * kWaves, 1) void fwd_bf16_d256_kernel(FwdArgs a
   // masked scores of a tile before its softmax (one wave per SIMD, pipelined):
   // two sets that the steps alternate
   f32x16 s_a, s_b;
+  PvTail tail;
+#pragma unroll
+  for (int j = 0; j < (kFwdDefer > 0 ? kFwdDefer : 1); ++j)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) tail.v[j][e] = (__bf16)0.f;
+  tail.p0 = tail.v[0];
+  tail.p1 = tail.v[0];
 
   // (a full wait here: the Q loads may have been scheduled after the stages)
   wait_fetch();
@@ -347,16 +389,18 @@ __global__ __launch_bounds__(64 * kWaves, 1) void fwd_bf16_d256_kernel(FwdArgs a
         a, smem + ((t + kAhead) % kSlots) * kStage, smem + (t % kSlots) * kStage,
         smem + ((t + kSlots - 1) % kSlots) * kStage + kTileBytes, kf, vf, pl, pe, tile0(t + kAhead),
         tile0(t + kAhead + 1), k_hi, t0, k_lo, kb, k_all, lim_rel, qreg, to, hh, oacc, s_in, s_out,
-        m_run, l_run);
+        m_run, l_run, tail);
     wait_vmcnt<(kAhead - 1) * 2 * kInstr>();
+    __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0): the step's LDS reads have landed
     tile_barrier();
   };
   if constexpr (kOverlap) {
     step<kPerKey, true, kOverlap, kInstr, kAK, kAV>(
         a, smem + kAhead * kStage, smem, smem + kTileBytes, kf, vf, pl, pe, tile0(kAhead),
         tile0(kAhead + 1), k_hi, k_lo, k_lo, kb, k_all, lim_rel, qreg, to, hh, oacc, s_b, s_a,
-        m_run, l_run);
+        m_run, l_run, tail);
     wait_vmcnt<(kAhead - 1) * 2 * kInstr>();
+    __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0): the step's LDS reads have landed
     tile_barrier();
     int t = 1;
     for (; t + 1 < n_tiles; t += 2) {
@@ -364,6 +408,7 @@ __global__ __launch_bounds__(64 * kWaves, 1) void fwd_bf16_d256_kernel(FwdArgs a
       st(t + 1, s_b, s_a);
     }
     auto finish = [&](f32x16& s_last) {
+      tail.run(oacc);
       OnlineSoftmax sm{s_last, a.scale_log2, m_run, l_run};
       sm.all();
       rescale_pv<kAV>(smem + ((n_tiles - 1) % kSlots) * kStage + kTileBytes, sm, l_run, oacc, to);
@@ -376,6 +421,7 @@ __global__ __launch_bounds__(64 * kWaves, 1) void fwd_bf16_d256_kernel(FwdArgs a
     }
   } else {
     for (int t = 0; t < n_tiles; ++t) st(t, s_a, s_b);   // (each step finishes its own tile)
+    tail.run(oacc);
   }
   wait_fetch();   // no direct load is left in flight when the waves end
 

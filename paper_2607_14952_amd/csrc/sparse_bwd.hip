@@ -156,7 +156,9 @@ __global__ __launch_bounds__(256, 1) void sparse_bwd_kernel(SparseArgs a) {
   fused_step<true>(a, smem + 2 * kTile, smem, smem, f, pool, pr, w, lane, qreg, dreg, bo, 0, n_t, g,
                    lse2, delta, acc, dsb);
   pr = pn;
-  __builtin_amdgcn_s_waitcnt(0x0F79);   // vmcnt(9): only this iteration's stage in flight
+  // vmcnt(9): only this iteration's stage in flight; lgkmcnt(0): the step's
+  // LDS reads have landed (the next stage refills the slot of the tile before)
+  __builtin_amdgcn_s_waitcnt(0x0079);
   tile_barrier();
   for (int T = 1; T < n_tiles; ++T) {
     pn = fr.rows_of(phys_t, clamp(T + 3), lane);
@@ -165,7 +167,7 @@ __global__ __launch_bounds__(256, 1) void sparse_bwd_kernel(SparseArgs a) {
                       smem + ((T + kSl - 1) % kSl) * kTile, f, pool, pr, w, lane, qreg, dreg, bo, T,
                       n_t, g, lse2, delta, acc, dsb);
     pr = pn;
-    __builtin_amdgcn_s_waitcnt(0x0F79);
+    __builtin_amdgcn_s_waitcnt(0x0079);
     tile_barrier();
   }
   wait_fetch();   // no direct load is left in flight (the last tile's slot was never a target)

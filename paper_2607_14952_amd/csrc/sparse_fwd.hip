@@ -108,8 +108,10 @@ __global__ __launch_bounds__(256, 1) void sparse_fwd_kernel(SparseArgs a) {
   for (int T = 0; T < n_tiles; ++T) {
     fwd_tile(a, smem + ((T + 3) % kFSlots) * kSlotBytes, smem + (T % kFSlots) * kSlotBytes, f, fl,
              pool, w, qreg, so, T, n_t, hh, oacc, m_run, l_run, phys_t, clamp(T + 6), lane);
-    // vmcnt(20): the stages of tiles T + 2 and T + 3 may be in flight
-    __builtin_amdgcn_s_waitcnt(0x4F74);
+    // vmcnt(20): the stages of tiles T + 2 and T + 3 may be in flight;
+    // lgkmcnt(0): this tile's LDS reads have landed (the stage issued after
+    // the barrier refills its slot)
+    __builtin_amdgcn_s_waitcnt(0x4074);
     tile_barrier();
   }
   wait_fetch();   // no direct load is left in flight when the waves end
