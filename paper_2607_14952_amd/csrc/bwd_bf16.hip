@@ -9,7 +9,9 @@
 // (row-major, swizzled);
 // the K^T operand of the third product comes from transposing LDS reads of
 // the same K tile.  The dq product of tile t-1 is issued in the same block as
-// the exponentials of tile t.
+// the exponentials of tile t; its last two MFMAs run after the next tile
+// barrier (every LDS read of a step lands before its barrier, since the stage
+// issued after it may refill the slot).
 //
 // dk/dv kernel: 128 response keys of one KV head per workgroup (lane l of
 // wave w owns key 32w + l % 32) against one chunk of packed query rows; Q and
@@ -55,7 +57,9 @@ constexpr int kKTAhead = 4;   // transposed K operands in flight (two reads each
 #define LS_DQ_DEFER 2
 #endif
 constexpr int kDqDefer = LS_DQ_DEFER;
-static_assert(kDqDefer >= 0 && kDqDefer <= 16 - kKTAhead, "deferred dq MFMAs");
+// (the shortened product loop still reads every operand only if the deferred
+// MFMAs are no more than its read-ahead)
+static_assert(kDqDefer >= 0 && kDqDefer <= kKTAhead, "deferred dq MFMAs");
 struct DqTail {
   bf16x8 kt[kDqDefer > 0 ? kDqDefer : 1];
   bf16x8 d0, d1;

@@ -12,7 +12,10 @@
 // 8 waves, two ahead with 4 (whose pipelined loop also keeps the previous V);
 // each wave waits only for the oldest stage in flight, and no VGPRs stage
 // them.  The K^T operand is one 16-byte LDS read per lane; the V^T operand
-// comes from transposing LDS reads of the row-major V tile.
+// comes from transposing LDS reads of the row-major V tile.  Before each tile
+// barrier a wave also waits for its own LDS reads, since the stage issued
+// after the barrier may refill the slot they read; the last two PV MFMAs of a
+// tile run after that barrier, beside the next tile's first operand reads.
 //
 // With 8 waves two waves share each SIMD, so one wave's softmax (exp2 on the
 // VALU) and LDS reads run beside the other's MFMAs; each wave fits in 256
@@ -101,6 +104,9 @@ struct PvTail {
 template <int kAheadV, int kDefer = 0>
 __device__ __forceinline__ void pv(const char* Vs, const bf16x8& p0, const bf16x8& p1,
                                    f32x16* oacc, const TileBase& o, PvTail* tail = nullptr) {
+  // the shortened loop still reads every operand only if the deferred MFMAs
+  // are no more than its read-ahead
+  static_assert(kDefer >= 0 && kDefer <= kAheadV, "deferred PV MFMAs");
   bf16x8 vreg[16];
   auto read = [&](int i) {
     return (i & 1) ? tile_col8(Vs, o, i >> 1, 16, 24) : tile_col8(Vs, o, i >> 1, 0, 8);
