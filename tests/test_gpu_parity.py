@@ -194,6 +194,26 @@ def test_bf16_few_rows_four_wave_path():
     full_case(cfg)
 
 
+@pytest.mark.parametrize("R", [40, 15], ids=["eight_wave", "four_wave"])
+def test_bf16_tile_counts(R):
+    """Splits and backward ranges of 1 to 6, 15 and 18 key tiles (aligned and ragged), on
+    both forward paths (R x G = 8 packed rows: 320 take the two-waves-per-SIMD
+    kernel, 120 the pipelined one).  The dense kernels finish the last MFMAs of
+    a tile's PV or dq product at the start of the next step, so the one-tile,
+    odd and even step counts each take a different way through the loops and
+    their tails."""
+    P = 1024
+    cfg = BF16_SMALL.scaled(name=f"bf16_tiles_r{R}", prefix_len=P, resp_len=R, plant_frac=0.0)
+    h = inputs.dense_inputs(cfg)
+    dev = device_inputs(h)
+    # tiles are the 32-key blocks a range touches
+    splits = [(0, 32), (32, 96), (96, 192), (192, 320), (320, 333), (333, 400), (400, 560),
+              (560, P), (P, P + R)]
+    out, lse, o_ref, l_ref = check_forward(cfg, h, dev, splits, P=P, q_pos0=P)
+    ranges = [(0, 32), (32, 96), (96, 200), (200, 331), (331, 480), (480, P + 7), (P + 7, P + R)]
+    check_backward(cfg, h, dev, out, lse, o_ref, l_ref, ranges, P=P, q_pos0=P)
+
+
 def test_bf16_single_row_and_response_only():
     cfg = BF16_SMALL.scaled(name="bf16_r1", prefix_len=512, resp_len=1, plant_frac=0.0,
                             n_shards=1, splits_per_shard=1)
