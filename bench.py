@@ -327,7 +327,6 @@ def run_sparse(cfg, args):
                             q_pos0=cfg.q_pos0)
     out = torch.empty((cfg.resp_len, cfg.n_q_heads, cfg.head_dim_v), dtype=torch.float32, device="cuda")
     lse = torch.empty((cfg.n_q_heads, cfg.resp_len), dtype=torch.float32, device="cuda")
-    out_b = torch.empty((cfg.resp_len, cfg.n_q_heads, cfg.head_dim_v), dtype=torch.bfloat16, device="cuda")
     dq = torch.empty((cfg.resp_len, cfg.n_q_heads, cfg.head_dim), dtype=torch.float32, device="cuda")
 
     def step(ev=None):
@@ -344,9 +343,8 @@ def run_sparse(cfg, args):
         B.sparse_attn_fwd(q, kv, idx, out=out, lse=lse, workspace=ws, **kw)
         if ev:
             ev[1].record()
-        B.lse_merge(out.view(1, *out.shape), lse.view(1, *lse.shape), out=out_b,
-                    lse=torch.empty_like(lse))
-        B.sparse_attn_bwd(q, kv, idx, d_out, out_b, lse, dq=dq, workspace=ws, **kw)
+        # the backward takes the forward's fp32 output as written (Delta = rowsum(dO * O))
+        B.sparse_attn_bwd(q, kv, idx, d_out, out, lse, dq=dq, workspace=ws, **kw)
         if ev:
             ev[2].record()
 

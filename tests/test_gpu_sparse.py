@@ -23,7 +23,7 @@ def _gpu_ready():
     B.load_library()
 
 
-def run(cfg, h, *, q_pos0=None, rows=None, backward=True):
+def run(cfg, h, *, q_pos0=None, rows=None, backward=True, out_bf16=True):
     import torch
     q_pos0 = cfg.prefix_len if q_pos0 is None else q_pos0
     q = to_device(h["q"])
@@ -35,7 +35,7 @@ def run(cfg, h, *, q_pos0=None, rows=None, backward=True):
                                  scale=cfg.scale)
     dq = None
     if backward:
-        out_b = out.to(torch.bfloat16)
+        out_b = out.to(torch.bfloat16) if out_bf16 else out
         dq = B.sparse_attn_bwd(q, kv, idx, to_device(h["d_out"]), out_b, lse,
                                prefix_len=cfg.prefix_len, q_pos0=q_pos0, scale=cfg.scale)
     torch.cuda.synchronize()
@@ -53,6 +53,12 @@ SMALL = configs.C5.scaled(name="c5_small", prefix_len=8192, resp_len=70, topk=30
 
 def test_sparse_small():
     run(SMALL, inputs.sparse_inputs(SMALL))
+
+
+def test_sparse_fp32_output_to_backward():
+    """The backward takes the forward's fp32 output as it was written (Delta
+    from fp32 O), as the sparse replay benchmark does."""
+    run(SMALL.scaled(name="c5_small_o32"), inputs.sparse_inputs(SMALL), out_bf16=False)
 
 
 def test_sparse_window_only_and_offset_rows():
