@@ -166,6 +166,43 @@ __global__ __launch_bounds__(256) void prep_kernel(const TD* __restrict__ d_out,
   }
 }
 
+// The same with dv = 64 kE: lane l takes elements kE l .. kE l + kE - 1 of the
+// row, one vector load of each operand, so a wave reads each row in one
+// coalesced instruction instead of kE narrow ones.
+template <typename T, int kE>
+__device__ __forceinline__ void load_as_float(const T* __restrict__ p, float* f) {
+  typedef __attribute__((__vector_size__(kE * sizeof(T)))) T V;
+  const V v = *reinterpret_cast<const V*>(p);
+#pragma unroll
+  for (int e = 0; e < kE; ++e) f[e] = (float)v[e];
+}
+
+template <typename TD, typename TO, int kE>
+__global__ __launch_bounds__(256) void prep_vec_kernel(const TD* __restrict__ d_out,
+                                                       const TO* __restrict__ out,
+                                                       const float* __restrict__ lse, int n_q,
+                                                       int n_heads, float* __restrict__ delta,
+                                                       float* __restrict__ lse2) {
+  constexpr int kDv = 64 * kE;
+  const int64_t rh = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (rh >= (int64_t)n_q * n_heads) return;
+  const int row = (int)(rh / n_heads), head = (int)(rh - (int64_t)row * n_heads);
+  float d[kE], o[kE];
+  load_as_float<TD, kE>(d_out + rh * kDv + kE * lane, d);
+  load_as_float<TO, kE>(out + rh * kDv + kE * lane, o);
+  float acc = 0.f;
+#pragma unroll
+  for (int e = 0; e < kE; ++e) acc = fmaf(d[e], o[e], acc);
+  for (int off = 32; off > 0; off >>= 1) acc += __shfl_xor(acc, off);
+  if (lane == 0) {
+    const int64_t i = (int64_t)head * n_q + row;
+    delta[i] = acc;
+    const float l = lse[i];
+    lse2[i] = (l == -INFINITY) ? INFINITY : l * kLog2e;
+  }
+}
+
 // ---------------------------------------------------------------- HBM read probe
 // Reads n16 16-byte units once and XORs their 32-bit words: a read-only
 // streaming pass with no arithmetic to speak of, the measured read ceiling the
@@ -244,13 +281,29 @@ hipError_t launch_bwd_prep(const void* d_out, const void* out, bool dout_bf16, b
                            const float* lse, int n_q, int n_heads, int dv, float* delta,
                            float* lse2, hipStream_t stream) {
   const unsigned blocks = (unsigned)(((int64_t)n_q * n_heads + 3) / 4);
-#define LS_PREP(TD, TO)                                                                   \
-  hipLaunchKernelGGL((prep_kernel<TD, TO>), dim3(blocks), dim3(256), 0, stream,           \
-                     (const TD*)d_out, (const TO*)out, lse, n_q, n_heads, dv, delta, lse2)
-  if (dout_bf16 && out_bf16) LS_PREP(__bf16, __bf16);
-  else if (dout_bf16) LS_PREP(__bf16, float);
-  else if (out_bf16) LS_PREP(float, __bf16);
-  else LS_PREP(float, float);
+  // whole rows of dv = 256 or 512 with 16-byte aligned bases take the vector
+  // loads (row starts are then aligned for both element sizes)
+  const bool vec = (dv == 256 || dv == 512) &&
+                   (((uintptr_t)d_out | (uintptr_t)out) & 15) == 0;
+#define LS_PREP(TD, TO)                                                                       \
+  if (vec && dv == 512)                                                                       \
+    hipLaunchKernelGGL((prep_vec_kernel<TD, TO, 8>), dim3(blocks), dim3(256), 0, stream,      \
+                       (const TD*)d_out, (const TO*)out, lse, n_q, n_heads, delta, lse2);     \
+  else if (vec)                                                                               \
+    hipLaunchKernelGGL((prep_vec_kernel<TD, TO, 4>), dim3(blocks), dim3(256), 0, stream,      \
+                       (const TD*)d_out, (const TO*)out, lse, n_q, n_heads, delta, lse2);     \
+  else                                                                                        \
+    hipLaunchKernelGGL((prep_kernel<TD, TO>), dim3(blocks), dim3(256), 0, stream,             \
+                       (const TD*)d_out, (const TO*)out, lse, n_q, n_heads, dv, delta, lse2)
+  if (dout_bf16 && out_bf16) {
+    LS_PREP(__bf16, __bf16);
+  } else if (dout_bf16) {
+    LS_PREP(__bf16, float);
+  } else if (out_bf16) {
+    LS_PREP(float, __bf16);
+  } else {
+    LS_PREP(float, float);
+  }
 #undef LS_PREP
   return hipGetLastError();
 }
