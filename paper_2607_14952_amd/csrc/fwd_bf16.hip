@@ -49,8 +49,14 @@ template <int kWaves> constexpr int kSlotsOf = kAheadOf<kWaves> + (kWaves == 4 ?
 // K operand reads in flight (16-byte reads) and V operands in flight (two
 // transposing reads each).  With two waves per SIMD the shallower rings keep
 // each wave within 256 registers.
-template <int kWaves> constexpr int kKAhead = kWaves == 4 ? 6 : 2;
-template <int kWaves> constexpr int kVAhead = kWaves == 4 ? 4 : 2;
+#ifndef LS_FWD_KAHEAD8
+#define LS_FWD_KAHEAD8 2
+#endif
+template <int kWaves> constexpr int kKAhead = kWaves == 4 ? 6 : LS_FWD_KAHEAD8;
+#ifndef LS_FWD_VAHEAD8
+#define LS_FWD_VAHEAD8 3
+#endif
+template <int kWaves> constexpr int kVAhead = kWaves == 4 ? 4 : LS_FWD_VAHEAD8;
 
 // S^T (32 keys x this lane's row) = K Q^T over the 256-wide head.  After
 // MFMA ks < kLoads, load(ks) issues one instruction of the next stage's direct
