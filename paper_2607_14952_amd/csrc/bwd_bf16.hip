@@ -42,7 +42,10 @@ constexpr int kQSlots = kQAhead + 2;
 
 // Operand reads run a fixed number of MFMAs ahead of their use (see mfma_fence).
 constexpr int kSDAhead = 2;   // steps of (K row, V row) reads in flight
-constexpr int kKTAhead = 4;   // transposed K operands in flight (two reads each)
+#ifndef LS_DQ_KTAHEAD
+#define LS_DQ_KTAHEAD 3
+#endif
+constexpr int kKTAhead = LS_DQ_KTAHEAD;   // transposed K operands in flight (two reads each)
 
 #ifndef LS_DQ_KT_EARLY
 #define LS_DQ_KT_EARLY 1
